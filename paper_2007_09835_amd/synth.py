@@ -1,0 +1,360 @@
+"""Seeded synthetic workloads: layer shape tables, masks, weights, inputs.
+
+This module holds no convolution arithmetic; it only decides shapes and draws
+random numbers, so that the GPU path and the CPU oracle see identical bytes.
+
+The paper evaluates on UCF101 clips with pretrained C3D / R(2+1)D weights
+(Section 5, experimental setup), none of which exist here.  The stand-ins keep
+the paper's shapes: 16-frame 112x112 RGB clips, the C3D conv stack and an
+R(2+1)D-18-shaped stack, kernel groups of g_M = g_N = 4 (Section 3: g_N = 4,
+g_M = 4 or 8), and masks drawn uniformly per group.
+
+RNG: numpy ``Generator(PCG64(SeedSequence([2007_09835, *keys])))`` where the
+keys name the workload, the layer and the role of the tensor, so every tensor
+is reproducible on its own.
+"""
+from __future__ import annotations
+
+import dataclasses
+import zlib
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+
+SEED = 2007_09835
+GROUP = 4  # g_M = g_N = 4 in every workload
+
+
+def _key(k) -> int:
+    if isinstance(k, (int, np.integer)):
+        return int(k) & 0xFFFFFFFF
+    return zlib.crc32(str(k).encode())
+
+
+def rng_for(*keys) -> np.random.Generator:
+    """Independent generator for one (workload, layer, role) tuple."""
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([SEED, *map(_key, keys)])))
+
+
+@dataclasses.dataclass
+class ConvLayer:
+    """One 3-D CONV layer of a workload (shapes only)."""
+    name: str
+    c_in: int
+    c_out: int
+    t: int
+    h: int
+    w: int
+    k: Tuple[int, int, int]            # (kt, kh, kw); kt is the kernel depth K_d
+    stride: Tuple[int, int, int] = (1, 1, 1)
+    pad: Tuple[int, int, int] = (0, 0, 0)
+    dense: bool = False                # kept dense in the workload (no KGS mask)
+    relu: bool = True
+    residual_from: Optional[str] = None  # name of the tensor added before ReLU
+    input_from: Optional[str] = None     # name of the tensor this layer reads (None: previous)
+    pool_after: Optional[Tuple[Tuple[int, int, int], Tuple[int, int, int]]] = None
+    keep: Optional[int] = None         # kept positions per group (KGS layers)
+
+    @property
+    def ks(self) -> int:
+        return self.k[0] * self.k[1] * self.k[2]
+
+    @property
+    def out_thw(self) -> Tuple[int, int, int]:
+        return tuple((i + 2 * p - k) // s + 1
+                     for i, k, s, p in zip((self.t, self.h, self.w), self.k, self.stride, self.pad))
+
+    @property
+    def voxels_out(self) -> int:
+        to, ho, wo = self.out_thw
+        return to * ho * wo
+
+    @property
+    def groups(self) -> Tuple[int, int]:
+        return -(-self.c_out // GROUP), -(-self.c_in // GROUP)
+
+    def dense_macs(self, batch: int = 1) -> int:
+        """Multiply-accumulates of the dense layer (the paper's "FLOPs")."""
+        return batch * self.voxels_out * self.c_out * self.c_in * self.ks
+
+
+# --------------------------------------------------------------------------
+# Shape tables
+# --------------------------------------------------------------------------
+
+def c3d_layers() -> List[ConvLayer]:
+    """C3D convolution stack on one 16x112x112 clip: eight 3x3x3 pad-1 convs
+    with ReLU, max-pool 1x2x2 after conv1 and 2x2x2 after conv2/3b/4b."""
+    p1 = ((1, 2, 2), (1, 2, 2))
+    p2 = ((2, 2, 2), (2, 2, 2))
+    spec = [("conv1", 3, 64, 16, 112, p1, True),
+            ("conv2", 64, 128, 16, 56, p2, False),
+            ("conv3a", 128, 256, 8, 28, None, False),
+            ("conv3b", 256, 256, 8, 28, p2, False),
+            ("conv4a", 256, 512, 4, 14, None, False),
+            ("conv4b", 512, 512, 4, 14, p2, False),
+            ("conv5a", 512, 512, 2, 7, None, False),
+            ("conv5b", 512, 512, 2, 7, None, False)]
+    return [ConvLayer(n, ci, co, t, hw, hw, (3, 3, 3), (1, 1, 1), (1, 1, 1), dense=d, relu=True,
+                      pool_after=pool)
+            for n, ci, co, t, hw, pool, d in spec]
+
+
+def r2plus1d_mid(n_in: int, n_out: int) -> int:
+    """Mid-width of a (2+1)-D factorised conv with the parameter count of the
+    full 3x3x3 conv it replaces: floor(27 N_i N_o / (9 N_i + 3 N_o))."""
+    return (27 * n_in * n_out) // (9 * n_in + 3 * n_out)
+
+
+def r2plus1d_layers() -> List[ConvLayer]:
+    """R(2+1)D-18-shaped stack on one 16x112x112 clip.
+
+    Stem: 1x7x7 stride (1,2,2) 3->45 then 3x1x1 45->64 (both dense).  Four
+    stages of two residual blocks at widths 64/128/256/512; a block is two
+    (2+1)-D convs, each a 1x3x3 spatial conv to the mid-width followed by a
+    3x1x1 temporal conv; the first block of stages 3-5 is strided by 2 in
+    T, H and W and has a dense 1x1x1 stride-2 shortcut.  The residual add and
+    the final ReLU of a block are fused into its last temporal conv.
+    """
+    layers: List[ConvLayer] = []
+    t, hw = 16, 112
+    layers.append(ConvLayer("stem_s", 3, 45, t, hw, hw, (1, 7, 7), (1, 2, 2), (0, 3, 3), dense=True))
+    hw = 56
+    layers.append(ConvLayer("stem_t", 45, 64, t, hw, hw, (3, 1, 1), (1, 1, 1), (1, 0, 0), dense=True))
+    prev = "stem_t"
+    c = 64
+    for stage, width in enumerate((64, 128, 256, 512), start=2):
+        for blk in range(2):
+            s = 2 if (blk == 0 and stage > 2) else 1
+            block_in = prev
+            shortcut = block_in
+            if s == 2:
+                sc = ConvLayer(f"l{stage}b{blk}_down", c, width, t, hw, hw, (1, 1, 1), (2, 2, 2),
+                               (0, 0, 0), dense=True, relu=False, input_from=block_in)
+                layers.append(sc)
+                shortcut = sc.name
+            cin = c
+            for conv in range(2):
+                st = s if conv == 0 else 1
+                mid = r2plus1d_mid(cin, width)
+                sp = ConvLayer(f"l{stage}b{blk}c{conv}_s", cin, mid, t, hw, hw, (1, 3, 3),
+                               (1, st, st), (0, 1, 1), input_from=(block_in if conv == 0 else None))
+                layers.append(sp)
+                t2, hw2 = t, (hw + 2 - 3) // st + 1
+                last = conv == 1
+                tp = ConvLayer(f"l{stage}b{blk}c{conv}_t", mid, width, t2, hw2, hw2, (3, 1, 1),
+                               (st, 1, 1), (1, 0, 0), relu=True,
+                               residual_from=(shortcut if last else None))
+                layers.append(tp)
+                t, hw = (t2 + 2 - 3) // st + 1, hw2
+                cin = width
+            c = width
+            prev = layers[-1].name
+    return layers
+
+
+# --------------------------------------------------------------------------
+# Masks
+# --------------------------------------------------------------------------
+
+def kgs_mask(rng: np.random.Generator, p_groups: int, q_groups: int, ks: int,
+             keep) -> np.ndarray:
+    """KGS mask [P][Q][K_s]: for every group (p-major, q-minor) keep ``keep``
+    kernel positions drawn uniformly without replacement.  ``keep`` may be an
+    int or a [P][Q] array of per-group counts."""
+    keep_arr = np.broadcast_to(np.asarray(keep, dtype=np.int64), (p_groups, q_groups))
+    mask = np.zeros((p_groups, q_groups, ks), dtype=np.uint8)
+    for p in range(p_groups):
+        for q in range(q_groups):
+            k = int(keep_arr[p, q])
+            if k:
+                mask[p, q, rng.choice(ks, size=k, replace=False)] = 1
+    return mask
+
+
+def vanilla_mask(rng: np.random.Generator, p_groups: int, q_groups: int, ks: int,
+                 rate: float) -> np.ndarray:
+    """Vanilla structured mask: round(P*Q/rate) whole groups kept, chosen
+    uniformly without replacement; every other group is pruned entirely."""
+    n_keep = int(round(p_groups * q_groups / rate))
+    mask = np.zeros((p_groups * q_groups, ks), dtype=np.uint8)
+    mask[rng.choice(p_groups * q_groups, size=n_keep, replace=False)] = 1
+    return mask.reshape(p_groups, q_groups, ks)
+
+
+def stack_keep_counts(layers: Sequence[ConvLayer], rate: float, tag: str,
+                      band: float = 0.05) -> List[Optional[int]]:
+    """Per-layer kept positions for a whole-stack MAC pruning rate ``rate``.
+
+    Uniform solution k* = K_s (D/R - D_dense) / (D - D_dense), randomised
+    rounding to floor/ceil with probability frac(k*), then a greedy repair
+    (one position at a time on the layer that brings the rate closest to the
+    target) until the rate lies within ``rate +- band``.
+    """
+    rng = rng_for(tag, "keep", int(rate * 1000))
+    d_total = sum(l.dense_macs() for l in layers)
+    d_dense = sum(l.dense_macs() for l in layers if l.dense)
+    if rate <= 1.0:
+        return [None if l.dense else l.ks for l in layers]
+    ks = [l.ks for l in layers if not l.dense]
+    if len(set(ks)) != 1:
+        raise ValueError("uniform k* needs one kernel volume")
+    kstar = ks[0] * (d_total / rate - d_dense) / (d_total - d_dense)
+    keep: List[Optional[int]] = []
+    for l in layers:
+        if l.dense:
+            keep.append(None)
+        else:
+            lo = int(np.floor(kstar))
+            keep.append(min(l.ks, max(1, lo + int(rng.random() < kstar - lo))))
+
+    def achieved(kp):
+        kept = sum(l.dense_macs() * (1.0 if k is None else k / l.ks) for l, k in zip(layers, kp))
+        return d_total / kept
+
+    for _ in range(1000):
+        r = achieved(keep)
+        if abs(r - rate) <= band:
+            return keep
+        step = 1 if r > rate else -1
+        best, best_err = None, None
+        for i, (l, k) in enumerate(zip(layers, keep)):
+            if k is None or not (1 <= k + step <= l.ks):
+                continue
+            trial = list(keep)
+            trial[i] = k + step
+            err = abs(achieved(trial) - rate)
+            if best_err is None or err < best_err:
+                best, best_err = i, err
+        if best is None:
+            break
+        keep[best] += step
+    raise ValueError("could not reach the requested pruning rate")
+
+
+def stack_rate(layers: Sequence[ConvLayer], masks: Sequence[Optional[np.ndarray]]) -> float:
+    """Whole-stack pruning rate: dense MACs over kept MACs, where a KGS layer
+    keeps V * sum over groups of g_m_eff * g_n_eff * k (border positions are
+    counted nominally, as the paper's FLOP counts do)."""
+    dense = 0
+    kept = 0
+    for l, m in zip(layers, masks):
+        d = l.dense_macs()
+        dense += d
+        if m is None:
+            kept += d
+        else:
+            kept += l.voxels_out * kept_weights(l, m)
+    return dense / kept
+
+
+def kept_weights(l: ConvLayer, mask: np.ndarray) -> int:
+    """Number of weights kept by a mask: sum over groups of g_m_eff*g_n_eff*k."""
+    p_groups, q_groups = l.groups
+    gm = np.full(p_groups, GROUP)
+    gm[-1] = l.c_out - GROUP * (p_groups - 1)
+    gn = np.full(q_groups, GROUP)
+    gn[-1] = l.c_in - GROUP * (q_groups - 1)
+    k = mask.sum(axis=2, dtype=np.int64)
+    return int((gm[:, None] * gn[None, :] * k).sum())
+
+
+# --------------------------------------------------------------------------
+# Tensors
+# --------------------------------------------------------------------------
+
+def to_dtype(a: np.ndarray, dtype: str):
+    """Round a float64 array to the workload dtype (round-to-nearest-even)
+    and return it as a CPU torch tensor of that dtype."""
+    import torch
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float64)).to(tdt)
+
+
+def kaiming(rng: np.random.Generator, c_out: int, c_in: int, k: Tuple[int, int, int]) -> np.ndarray:
+    """Kaiming-normal weights N(0, 2 / (c_in * kt * kh * kw))."""
+    fan_in = c_in * k[0] * k[1] * k[2]
+    return rng.normal(0.0, np.sqrt(2.0 / fan_in), size=(c_out, c_in, *k))
+
+
+@dataclasses.dataclass
+class LayerData:
+    layer: ConvLayer
+    w: np.ndarray                  # float64 [M][N][kt][kh][kw] (round with to_dtype)
+    bias: np.ndarray               # float64 [M] (bias stays fp32 on the GPU)
+    mask: Optional[np.ndarray]     # uint8 [P][Q][K_s] or None (dense layer)
+
+
+def layer_params(tag: str, layer: ConvLayer, mask_kind: str = "kgs", rate: float = 3.0,
+                 w_std: Optional[float] = None, b_std: float = 0.01) -> LayerData:
+    """Weights, bias and mask of one layer.  ``mask_kind`` is "kgs" (uses
+    layer.keep per group), "vanilla" (whole groups at ``rate``) or "dense"."""
+    wr = rng_for(tag, layer.name, "w")
+    if w_std is None:
+        w = kaiming(wr, layer.c_out, layer.c_in, layer.k)
+    else:
+        w = wr.normal(0.0, w_std, size=(layer.c_out, layer.c_in, *layer.k))
+    b = rng_for(tag, layer.name, "b").normal(0.0, b_std, size=layer.c_out)
+    p_groups, q_groups = layer.groups
+    if layer.dense or mask_kind == "dense":
+        mask = None
+    elif mask_kind == "vanilla":
+        mask = vanilla_mask(rng_for(tag, layer.name, "mask"), p_groups, q_groups, layer.ks, rate)
+    else:
+        mask = kgs_mask(rng_for(tag, layer.name, "mask"), p_groups, q_groups, layer.ks, layer.keep)
+    return LayerData(layer, w, b, mask)
+
+
+def clip_input(tag: str, batch: int = 1, kind: str = "uniform01",
+               c: int = 3, t: int = 16, h: int = 112, w: int = 112) -> np.ndarray:
+    """Input volume [n][c][t][h][w], float64: U(0,1) RGB-like clips
+    ("uniform01"), U(-1,1) ("uniform11") or |N(0,1)| post-ReLU-like
+    activations ("halfnormal")."""
+    r = rng_for(tag, "x", batch, c, t, h, w)
+    shape = (batch, c, t, h, w)
+    if kind == "uniform01":
+        return r.random(shape)
+    if kind == "uniform11":
+        return r.uniform(-1.0, 1.0, shape)
+    if kind == "halfnormal":
+        return np.abs(r.standard_normal(shape))
+    raise ValueError(kind)
+
+
+# --------------------------------------------------------------------------
+# The five workloads
+# --------------------------------------------------------------------------
+
+def single_layer_small() -> Tuple[ConvLayer, dict]:
+    """KGS layer 16->32 on 8x28x28, 3x3x3 s1 p1, 9 of 27 positions kept per
+    group, W ~ N(0, 0.05^2), b ~ N(0, 0.01^2), x ~ U(-1, 1), ReLU, fp32."""
+    l = ConvLayer("small", 16, 32, 8, 28, 28, (3, 3, 3), (1, 1, 1), (1, 1, 1), keep=9)
+    return l, dict(tag="small16x32", w_std=0.05, x_kind="uniform11", dtype="f32")
+
+
+def single_layer_conv3b() -> Tuple[ConvLayer, dict]:
+    """C3D conv3b-shaped KGS layer 256->256 on 8x28x28, 10 of 27 kept
+    (about 2.7x), Kaiming-normal weights, |N(0,1)| inputs, ReLU."""
+    l = ConvLayer("conv3b", 256, 256, 8, 28, 28, (3, 3, 3), (1, 1, 1), (1, 1, 1), keep=10)
+    return l, dict(tag="conv3b256", w_std=None, x_kind="halfnormal")
+
+
+def c3d_stack(rate: float = 3.0, tag: str = "c3d") -> List[ConvLayer]:
+    """C3D stack with per-layer keep counts for a whole-stack rate (conv1
+    dense)."""
+    layers = c3d_layers()
+    for l, k in zip(layers, stack_keep_counts(layers, rate, tag)):
+        l.keep = k
+    return layers
+
+
+def r2plus1d_stack(tag: str = "r2plus1d") -> List[ConvLayer]:
+    """R(2+1)D-18 stack: spatial KGS convs keep 3 or 4 of 9 positions,
+    temporal ones 1 or 2 of 3, drawn per layer; stem and shortcuts dense."""
+    layers = r2plus1d_layers()
+    r = rng_for(tag, "keep")
+    for l in layers:
+        if l.dense:
+            continue
+        l.keep = int(r.integers(3, 5)) if l.ks == 9 else int(r.integers(1, 3))
+    return layers
