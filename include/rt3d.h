@@ -1,0 +1,191 @@
+/*
+ * rt3d.h -- C ABI of the MI355X (gfx950) library for forward 3-D convolution
+ * under kernel-group-structured (KGS) sparsity, its vanilla special case, and
+ * the dense baseline.  Paper: RT3D, arXiv 2007.09835.
+ *
+ * The operation (Section 3).  A 3-D CONV layer has a 5-D weight tensor
+ * W[M][N][K_d][K_h][K_w] (M filters, N input channels; K_d is the temporal
+ * kernel depth, called kt here).  The filters and channels are split into
+ * kernel groups of g_M x g_N kernels, P = ceil(M/g_M) by Q = ceil(N/g_N)
+ * groups (Section 4; the last group in each direction may be partial).  A
+ * KGS mask keeps or prunes each kernel position of a group for all of the
+ * group's kernels together (Fig. 1(b)); vanilla sparsity keeps or prunes a
+ * group as a whole.  The pruned layer equals the dense layer with the pruned
+ * weights set to zero, and since each group reshaped to a g_M x (g_N*K_s)
+ * matrix merely loses columns, the kept part is a smaller dense matrix that
+ * can be packed and multiplied on its own (Section 3, reshaping paragraph).
+ *
+ * Conventions used by every call:
+ *   - Weights on the host are dense [M][N][kt][kh][kw] in the layer dtype.
+ *   - Masks are uint8 [P][Q][kt*kh*kw]; 1 = keep, 0 = pruned, anything else
+ *     is an error.  Kernel position pos = (it*kh + ih)*kw + iw.
+ *   - Activations on the device are channels-last: x [n][t][h][w][c_in],
+ *     y and residual [n][to][ho][wo][c_out] (torch.channels_last_3d).
+ *   - The convolution is a cross-correlation with zero padding:
+ *       y = act(sum_{c, kept pos} W[m][c][pos] * x[..shifted..] + bias[m]
+ *               (+ residual))
+ *     with act = ReLU when RT3D_RELU is set; to = (t + 2 pt - kt)/st + 1,
+ *     likewise ho and wo.
+ *   - Accumulation is float32 for every dtype; bias is float32; x, W, y and
+ *     residual share the layer dtype; the output is rounded to nearest even.
+ *   - Device calls are asynchronous on the caller's HIP stream (passed as
+ *     void*, i.e. a hipStream_t; NULL is the default stream).  Faults inside
+ *     a kernel surface at the next synchronisation of that stream.
+ *   - Ownership: the caller owns every buffer.  The library never allocates
+ *     caller-visible memory, never frees or retains a pointer past a call,
+ *     and keeps no state except a thread-local error message.
+ *   - Errors: all arguments are validated before anything is launched; on
+ *     error nothing is written to the outputs and rt3d_last_error_detail()
+ *     describes the failure.
+ */
+#ifndef RT3D_H
+#define RT3D_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    RT3D_OK = 0,
+    RT3D_ERR_INVALID_ARG = 1,      /* null pointer, non-positive size, bad mask byte */
+    RT3D_ERR_UNSUPPORTED = 2,      /* valid but outside what the kernels implement */
+    RT3D_ERR_BUFFER_TOO_SMALL = 3, /* a caller buffer is smaller than required */
+    RT3D_ERR_BLOB_MISMATCH = 4,    /* packed blob/info does not belong to this desc */
+    RT3D_ERR_HIP = 5               /* the HIP runtime reported an error */
+} rt3d_status;
+
+typedef enum { RT3D_F32 = 0, RT3D_BF16 = 1, RT3D_F16 = 2 } rt3d_dtype;
+
+enum { RT3D_RELU = 1u, RT3D_RESIDUAL = 2u };
+
+/* One convolution layer applied to one batch.  Supported: strides 1 or 2,
+ * kernel extents 1..7, padding 0..kernel extent-1, group sizes g_m, g_n in
+ * {4, 8, 16} (the paper uses g_N = 4 and g_M = 4 or 8, Section 3). */
+typedef struct {
+    int32_t n, c_in, c_out;   /* batch, N input channels, M filters */
+    int32_t t, h, w;          /* input extent */
+    int32_t kt, kh, kw;       /* kernel extent; kt is the temporal depth K_d */
+    int32_t st, sh, sw;       /* stride */
+    int32_t pt, ph, pw;       /* zero padding */
+    int32_t g_m, g_n;         /* kernel-group size (KGS calls; ignored when dense) */
+    int32_t dtype;            /* rt3d_dtype of x, W, y, residual */
+    uint32_t flags;           /* RT3D_RELU | RT3D_RESIDUAL */
+} rt3d_conv3d_desc;
+
+/* Filled by the pack calls; plain data owned by the caller.  It describes
+ * the blob and must be passed back unchanged to the forward call. */
+typedef struct {
+    uint64_t magic;            /* identifies a blob written by this library */
+    uint64_t desc_hash;        /* hash of the weight-side desc fields */
+    uint32_t version;
+    uint32_t variant;          /* kernel mapping chosen at pack time */
+    uint32_t tile_groups;      /* filter groups per wave tile (KGS) */
+    uint32_t vanilla;          /* 1 if every mask row is all-0 or all-1 */
+    uint64_t packed_bytes;     /* size of the blob */
+    /* canonical sections of a KGS blob (byte offset and size within it):
+     * [0] group_ptr u32[P*Q+1]  prefix sums of kept positions per group,
+     *                           groups p-major, q-minor
+     * [1] pos       u16[sum k]  ascending kept positions of each group
+     * [2] val_ptr   u64[P*Q+1]  prefix sums of kept weights per group
+     * [3] vals      dtype[...]  per group g (gm x gn kernels, k positions):
+     *                           vals[val_ptr[g] + (i*gn + j)*k + r] =
+     *                           W[p*g_m+i][q*g_n+j][pos_r]
+     * A dense blob has no canonical sections (all zero). */
+    uint64_t canon_off[4];
+    uint64_t canon_bytes[4];
+    uint64_t derived_off;      /* kernel-layout section */
+    uint64_t derived_bytes;
+    uint64_t kept_positions;   /* sum over groups of k */
+    uint64_t kept_weights;     /* sum over groups of gm*gn*k: MACs per output voxel */
+    uint64_t plan[16];         /* private to the library: the launch plan chosen at
+                                  pack time; the forward call reads it, so the caller
+                                  never has to read the device copy of the blob */
+} rt3d_pack_info;
+
+/* Static description of a status code (never NULL). */
+const char *rt3d_status_string(rt3d_status status);
+
+/* Message describing the last error raised on the calling thread ("" if
+ * none).  Valid until the next library call on this thread. */
+const char *rt3d_last_error_detail(void);
+
+/* Output extent of a layer.  Host only. */
+rt3d_status rt3d_conv3d_out_shape(const rt3d_conv3d_desc *desc,
+                                  int32_t *to, int32_t *ho, int32_t *wo);
+
+/* Bytes of the KGS blob for this layer and mask (Section 3 compact format
+ * plus the kernel layout).  Host only, deterministic.
+ *
+ * A blob (KGS or dense) is tied to every desc field except n and flags: the
+ * kernel layout is planned for the layer's input extent, strides and
+ * padding, so one blob serves any batch size and any epilogue flags, and a
+ * forward call with other extents fails with RT3D_ERR_BLOB_MISMATCH.  Device
+ * pointers (x, y, residual, bias, blob, workspace) must be 16-byte aligned. */
+rt3d_status rt3d_kgs_pack_size(const rt3d_conv3d_desc *desc, const uint8_t *mask,
+                               uint64_t *bytes);
+
+/* Pack dense host weights w_dense [M][N][kt][kh][kw] (layer dtype) and the
+ * host mask into the host buffer blob (blob_bytes >= rt3d_kgs_pack_size).
+ * Writes the canonical per-group sections (Section 3: each group keeps its
+ * g_M x (g_N * k) matrix of surviving columns, positions ascending, groups
+ * p-major) and the kernel layout, and fills *info.  Weights at pruned
+ * positions are never read.  A mask whose rows are all-0 or all-1 is the
+ * vanilla scheme (Section 3) and is recorded as such.  The caller copies the
+ * blob to device memory before calling rt3d_kgs_conv3d_fwd.  Host only. */
+rt3d_status rt3d_kgs_pack(const rt3d_conv3d_desc *desc, const void *w_dense,
+                          const uint8_t *mask, void *blob, uint64_t blob_bytes,
+                          rt3d_pack_info *info);
+
+/* Inverse of the canonical sections: writes W * expand(mask) as dense host
+ * weights [M][N][kt][kh][kw] (pruned positions are zero).  Host only. */
+rt3d_status rt3d_kgs_unpack(const rt3d_conv3d_desc *desc, const rt3d_pack_info *info,
+                            const void *blob, void *w_masked_dense);
+
+/* Device workspace a forward call of this layer needs (0 if none).  The
+ * workspace is caller-owned device memory, at least 256-byte aligned. */
+rt3d_status rt3d_conv3d_workspace_size(const rt3d_conv3d_desc *desc,
+                                       const rt3d_pack_info *info, uint64_t *bytes);
+
+/* KGS (and vanilla) sparse forward.  blob_dev: device copy of the blob that
+ * rt3d_kgs_pack wrote with this desc (info from that call).  With n == 0
+ * nothing is read or written and the device pointers may be NULL.  x, y, residual
+ * are device pointers in the channels-last layout; bias is a device float32
+ * [M] array or NULL (zero bias); residual must be non-NULL exactly when
+ * RT3D_RESIDUAL is set.  y must not overlap x, residual or the blob.  Only
+ * kept (group, position) pairs are multiplied; a vanilla-pruned group costs
+ * nothing.  Asynchronous on `stream`. */
+rt3d_status rt3d_kgs_conv3d_fwd(const rt3d_conv3d_desc *desc, const rt3d_pack_info *info,
+                                const void *blob_dev, const void *x, const float *bias,
+                                const void *residual, void *y,
+                                void *workspace, uint64_t workspace_bytes, void *stream);
+
+/* Bytes of the dense blob.  Host only. */
+rt3d_status rt3d_dense_pack_size(const rt3d_conv3d_desc *desc, uint64_t *bytes);
+
+/* Reorganise dense host weights [M][N][kt][kh][kw] into the dense kernel's
+ * layout (host blob) and fill *info.  Host only. */
+rt3d_status rt3d_dense_pack(const rt3d_conv3d_desc *desc, const void *w_dense,
+                            void *blob, uint64_t blob_bytes, rt3d_pack_info *info);
+
+/* Dense forward (the baseline every speedup is measured against), same
+ * argument conventions as rt3d_kgs_conv3d_fwd. */
+rt3d_status rt3d_conv3d_dense_fwd(const rt3d_conv3d_desc *desc, const rt3d_pack_info *info,
+                                  const void *blob_dev, const void *x, const float *bias,
+                                  const void *residual, void *y,
+                                  void *workspace, uint64_t workspace_bytes, void *stream);
+
+/* 3-D max pooling between layers (C3D pools 1x2x2 after conv1 and 2x2x2
+ * after conv2, conv3b, conv4b): no padding, floor output size, channels-last
+ * x [n][t][h][w][c] -> y [n][to][ho][wo][c].  Asynchronous on `stream`. */
+rt3d_status rt3d_maxpool3d_fwd(int32_t n, int32_t c, int32_t t, int32_t h, int32_t w,
+                               int32_t kt, int32_t kh, int32_t kw,
+                               int32_t st, int32_t sh, int32_t sw, int32_t dtype,
+                               const void *x, void *y, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RT3D_H */

@@ -33,11 +33,17 @@ def _load():
         lib.oracle_maxpool3d.argtypes = [i] * 11 + [dp, dp]
         lib.oracle_conv3d_points.argtypes = ([i] * 17 + [dp, dp, ctypes.c_void_p, dp, dp, i,
                                               ctypes.c_long, ctypes.c_void_p, dp])
+        lib.oracle_num_threads.argtypes = []
         for f in (lib.oracle_conv3d_dense, lib.oracle_conv3d_kgs, lib.oracle_kgs_pack,
-                  lib.oracle_maxpool3d, lib.oracle_conv3d_points):
+                  lib.oracle_maxpool3d, lib.oracle_conv3d_points, lib.oracle_num_threads):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
+
+
+def num_threads() -> int:
+    """Threads the oracle's OpenMP loops use."""
+    return int(_load().oracle_num_threads())
 
 
 def _f64(a):

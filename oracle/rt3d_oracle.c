@@ -320,3 +320,16 @@ int oracle_maxpool3d(int n, int c, int t, int h, int w, int kt, int kh, int kw,
     }
     return ORACLE_OK;
 }
+
+/* Number of threads the OpenMP loops above use (reported with timings). */
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

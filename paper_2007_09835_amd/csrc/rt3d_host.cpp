@@ -1,0 +1,783 @@
+// Host side of librt3d: argument validation, the compact KGS pack (Section 3
+// of RT3D, arXiv 2007.09835: a kernel group reshaped to g_M x (g_N*K_s)
+// loses whole columns), the launch planner that lays the kept weights out in
+// MFMA operand order, and the C entry points declared in include/rt3d.h.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "rt3d_internal.h"
+
+namespace rt3d {
+namespace {
+
+thread_local std::string g_detail;
+
+rt3d_status fail(rt3d_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_detail = buf;
+  return s;
+}
+
+rt3d_status ok() {
+  g_detail.clear();
+  return RT3D_OK;
+}
+
+int esize_of(int dtype) { return dtype == RT3D_F32 ? 4 : 2; }
+
+uint64_t align_up(uint64_t v, uint64_t a) { return (v + a - 1) / a * a; }
+
+int out_len(int in, int k, int s, int p) {
+  const int span = in + 2 * p - k;
+  return span < 0 ? 0 : span / s + 1;
+}
+
+// ---------------------------------------------------------------------------
+// Validation
+// ---------------------------------------------------------------------------
+
+rt3d_status check_desc(const rt3d_conv3d_desc *d, bool need_groups) {
+  if (!d) return fail(RT3D_ERR_INVALID_ARG, "desc is NULL");
+  if (d->n < 0) return fail(RT3D_ERR_INVALID_ARG, "batch n=%d is negative", d->n);
+  if (d->c_in <= 0 || d->c_out <= 0 || d->t <= 0 || d->h <= 0 || d->w <= 0)
+    return fail(RT3D_ERR_INVALID_ARG, "channel and extent sizes must be positive");
+  if (d->kt <= 0 || d->kh <= 0 || d->kw <= 0 || d->st <= 0 || d->sh <= 0 || d->sw <= 0 ||
+      d->pt < 0 || d->ph < 0 || d->pw < 0)
+    return fail(RT3D_ERR_INVALID_ARG, "kernel extents and strides must be positive, padding >= 0");
+  if (d->dtype != RT3D_F32 && d->dtype != RT3D_BF16 && d->dtype != RT3D_F16)
+    return fail(RT3D_ERR_INVALID_ARG, "unknown dtype %d", d->dtype);
+  if (d->flags & ~(RT3D_RELU | RT3D_RESIDUAL))
+    return fail(RT3D_ERR_INVALID_ARG, "unknown flag bits 0x%x", d->flags);
+  if (out_len(d->t, d->kt, d->st, d->pt) <= 0 || out_len(d->h, d->kh, d->sh, d->ph) <= 0 ||
+      out_len(d->w, d->kw, d->sw, d->pw) <= 0)
+    return fail(RT3D_ERR_INVALID_ARG, "the kernel does not fit the padded input");
+  if (d->kt > 7 || d->kh > 7 || d->kw > 7)
+    return fail(RT3D_ERR_UNSUPPORTED, "kernel extents above 7 are not supported");
+  if (d->st > 2 || d->sh > 2 || d->sw > 2)
+    return fail(RT3D_ERR_UNSUPPORTED, "strides above 2 are not supported");
+  if (d->pt >= d->kt || d->ph >= d->kh || d->pw >= d->kw)
+    return fail(RT3D_ERR_UNSUPPORTED, "padding must be smaller than the kernel extent");
+  if (need_groups) {
+    auto okg = [](int g) { return g == 4 || g == 8 || g == 16; };
+    if (!okg(d->g_m) || !okg(d->g_n))
+      return fail(RT3D_ERR_UNSUPPORTED, "group sizes g_m=%d g_n=%d: only 4, 8, 16", d->g_m, d->g_n);
+  }
+  // 32-bit LDS offsets and step counters bound the layer size.
+  const double elems = static_cast<double>(d->c_out) * d->c_in * d->kt * d->kh * d->kw;
+  if (elems > 1.0e9) return fail(RT3D_ERR_UNSUPPORTED, "weight tensor too large");
+  return ok();
+}
+
+uint64_t desc_hash(const rt3d_conv3d_desc *d) {
+  const int32_t f[] = {d->c_in, d->c_out, d->t,  d->h,  d->w,  d->kt, d->kh, d->kw, d->st,
+                       d->sh,   d->sw,    d->pt, d->ph, d->pw, d->g_m, d->g_n, d->dtype};
+  uint64_t h = 1469598103934665603ull;
+  for (int32_t v : f) {
+    for (int b = 0; b < 4; ++b) {
+      h ^= static_cast<uint8_t>(static_cast<uint32_t>(v) >> (8 * b));
+      h *= 1099511628211ull;
+    }
+  }
+  return h;
+}
+
+// ---------------------------------------------------------------------------
+// Layer geometry and the voxel tiling
+// ---------------------------------------------------------------------------
+
+struct Geom {
+  int n, c_in, c_out, t, h, w, kt, kh, kw, st, sh, sw, pt, ph, pw, to, ho, wo, ks, es;
+};
+
+Geom geom_of(const rt3d_conv3d_desc *d) {
+  Geom g{d->n,  d->c_in, d->c_out, d->t,  d->h,  d->w,  d->kt, d->kh, d->kw, d->st,
+         d->sh, d->sw,   d->pt,    d->ph, d->pw, 0,     0,     0,     0,     0};
+  g.to = out_len(d->t, d->kt, d->st, d->pt);
+  g.ho = out_len(d->h, d->kh, d->sh, d->ph);
+  g.wo = out_len(d->w, d->kw, d->sw, d->pw);
+  g.ks = d->kt * d->kh * d->kw;
+  g.es = esize_of(d->dtype);
+  return g;
+}
+
+constexpr int kSlots = 128;            // voxel slots per workgroup
+constexpr int kMaxHalo = 96 * 1024;    // LDS bytes for the staged brick
+
+// Choose the output brick: fewest launched voxel slots (least waste at the
+// volume's edges), then the smallest halo (least staging traffic).
+Tiling choose_tiling(const Geom &g) {
+  Tiling best{};
+  long best_cost = -1, best_halo = 0;
+  const int cc = g.es == 2 ? 32 : 16;
+  const int row = cc * g.es + 16;  // +16 bytes: rows land on different LDS banks
+  for (int bw = 1; bw <= std::min(g.wo, kSlots); ++bw)
+    for (int bh = 1; bh <= std::min(g.ho, kSlots / bw); ++bh)
+      for (int bt = 1; bt <= std::min(g.to, kSlots / (bw * bh)); ++bt) {
+        const int ht = (bt - 1) * g.st + g.kt;
+        const int hh = (bh - 1) * g.sh + g.kh;
+        const int hw = (bw - 1) * g.sw + g.kw;
+        const long halo = static_cast<long>(ht) * hh * hw * row;
+        if (halo > kMaxHalo) continue;
+        const long nb = static_cast<long>((g.to + bt - 1) / bt) * ((g.ho + bh - 1) / bh) *
+                        ((g.wo + bw - 1) / bw);
+        const long cost = nb * kSlots;
+        if (best_cost < 0 || cost < best_cost || (cost == best_cost && halo < best_halo)) {
+          best_cost = cost;
+          best_halo = halo;
+          best = Tiling{bt, bh, bw, ht, hh, hw, cc, row, kSlots, (g.c_in + cc - 1) / cc};
+        }
+      }
+  return best;
+}
+
+// LDS byte offset of the item (channel block ql of the chunk, kernel
+// position pos) relative to a voxel slot's (0,0,0) tap.
+uint32_t item_offset(const Geom &g, const Tiling &tl, int ql, int pos) {
+  const int iw = pos % g.kw;
+  const int ih = (pos / g.kw) % g.kh;
+  const int it = pos / (g.kw * g.kh);
+  return static_cast<uint32_t>(((it * tl.hh + ih) * tl.hw + iw) * tl.row + ql * 4 * g.es);
+}
+
+// ---------------------------------------------------------------------------
+// Canonical KGS sections (the compact per-group format of Section 3)
+// ---------------------------------------------------------------------------
+
+struct Canon {
+  int P, Q;
+  std::vector<uint32_t> group_ptr;
+  std::vector<uint16_t> pos;
+  std::vector<uint64_t> val_ptr;
+  uint64_t nvals = 0;
+};
+
+rt3d_status canon_index(const rt3d_conv3d_desc *d, const uint8_t *mask, Canon &c) {
+  const int ks = d->kt * d->kh * d->kw;
+  c.P = (d->c_out + d->g_m - 1) / d->g_m;
+  c.Q = (d->c_in + d->g_n - 1) / d->g_n;
+  c.group_ptr.assign(static_cast<size_t>(c.P) * c.Q + 1, 0);
+  c.val_ptr.assign(static_cast<size_t>(c.P) * c.Q + 1, 0);
+  c.pos.clear();
+  uint64_t nv = 0;
+  for (int p = 0; p < c.P; ++p) {
+    const int gm = std::min(d->g_m, d->c_out - p * d->g_m);
+    for (int q = 0; q < c.Q; ++q) {
+      const int gn = std::min(d->g_n, d->c_in - q * d->g_n);
+      const size_t gi = static_cast<size_t>(p) * c.Q + q;
+      const uint8_t *row = mask + gi * ks;
+      c.group_ptr[gi] = static_cast<uint32_t>(c.pos.size());
+      c.val_ptr[gi] = nv;
+      int k = 0;
+      for (int s = 0; s < ks; ++s) {
+        if (row[s] > 1)
+          return fail(RT3D_ERR_INVALID_ARG, "mask[%d][%d][%d] = %d is not 0 or 1", p, q, s, row[s]);
+        if (row[s]) {
+          c.pos.push_back(static_cast<uint16_t>(s));
+          ++k;
+        }
+      }
+      nv += static_cast<uint64_t>(gm) * gn * k;
+    }
+  }
+  c.group_ptr.back() = static_cast<uint32_t>(c.pos.size());
+  c.val_ptr.back() = nv;
+  c.nvals = nv;
+  return ok();
+}
+
+// mask of the 4x4 kernel block (p4, q4) at position pos (groups of 8 or 16
+// are unions of 4x4 blocks that share their group's mask row).
+struct Mask4 {
+  const uint8_t *mask;
+  int Q, ks, gm4, gn4;  // gm4 = g_m / 4
+  bool kept(int p4, int q4, int pos) const {
+    return mask[(static_cast<size_t>(p4 / gm4) * Q + q4 / gn4) * ks + pos] == 1;
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Kernel layouts
+// ---------------------------------------------------------------------------
+
+struct Layout {
+  Plan plan{};
+  uint32_t variant = 0;
+  std::vector<uint32_t> step_ptr, item_ptr, items, keep;
+  std::vector<uint8_t> a;  // operand stream, raw element bytes
+};
+
+// Element (filter m, channel c, position pos) of the dense weights, or zero
+// when it lies outside the layer or is pruned.  Pruned weights are not read.
+struct WeightSource {
+  const uint8_t *w;
+  const Geom &g;
+  const Mask4 *m4;  // nullptr for dense
+  void copy(uint8_t *dst, int m, int c, int pos) const {
+    if (m < g.c_out && c < g.c_in && (!m4 || m4->kept(m / 4, c / 4, pos))) {
+      const size_t idx = (static_cast<size_t>(m) * g.c_in + c) * g.ks + pos;
+      std::memcpy(dst, w + idx * g.es, g.es);
+    } else {
+      std::memset(dst, 0, g.es);
+    }
+  }
+};
+
+struct Item {
+  int ql, pos;
+  uint32_t keep;
+};
+
+// Items of one chunk for one 16-filter tile: every (block, position) that
+// any of the tile's four 4x4 blocks keeps (all of them when dense), in
+// position-major order.
+std::vector<Item> chunk_items(const Geom &g, const Mask4 *m4, int cc, int ch, int p4_first) {
+  std::vector<Item> out;
+  const int blocks = cc / 4;
+  const int q4_count = (g.c_in + 3) / 4;
+  const int p4_count = (g.c_out + 3) / 4;
+  for (int pos = 0; pos < g.ks; ++pos)
+    for (int ql = 0; ql < blocks; ++ql) {
+      const int q4 = ch * blocks + ql;
+      if (q4 >= q4_count) continue;
+      uint32_t keep = 0;
+      for (int gi = 0; gi < 4; ++gi) {
+        const int p4 = p4_first + gi;
+        if (p4 < p4_count && (!m4 || m4->kept(p4, q4, pos))) keep |= 1u << gi;
+      }
+      if (keep) out.push_back(Item{ql, pos, keep});
+    }
+  return out;
+}
+
+// 16-bit MFMA item layout (variants kVarDenseItems16, kVarKgsUnion16) and
+// the f32 16x16x4 dense layout (kVarDenseItemsF32).
+void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const Mask4 *m4,
+                        Layout &L) {
+  const bool f32 = g.es == 4;
+  const int ips = f32 ? 4 : 8;           // items per K-step
+  const int epl = f32 ? 4 : 8;           // operand elements per lane
+  const bool dense = m4 == nullptr;
+  const int mfw = (dense && (g.c_out + 31) / 32 >= 4) ? 2 : 1;
+  const int wt_count = (g.c_out + 16 * mfw - 1) / (16 * mfw);
+  L.variant = dense ? (f32 ? kVarDenseItemsF32 : kVarDenseItems16) : kVarKgsUnion16;
+  L.plan.mfw = mfw;
+  L.plan.wave_tiles = wt_count;
+  L.plan.items_per_step = ips;
+  L.step_ptr.assign(static_cast<size_t>(wt_count) * (tl.nchunks + 1), 0);
+  L.item_ptr.assign(wt_count, 0);
+  WeightSource src{w, g, m4};
+
+  // Dense: one item list shared by every wave tile.
+  std::vector<std::vector<Item>> shared;
+  if (dense)
+    for (int ch = 0; ch < tl.nchunks; ++ch) shared.push_back(chunk_items(g, nullptr, tl.cc, ch, 0));
+
+  uint32_t step = 0;
+  for (int wt = 0; wt < wt_count; ++wt) {
+    const uint32_t first_step = step;
+    const bool write_items = !dense || wt == 0;
+    L.item_ptr[wt] = dense ? 0 : first_step;
+    for (int ch = 0; ch < tl.nchunks; ++ch) {
+      L.step_ptr[static_cast<size_t>(wt) * (tl.nchunks + 1) + ch] = step;
+      std::vector<Item> its = dense ? shared[ch] : chunk_items(g, m4, tl.cc, ch, wt * 4);
+      while (its.size() % ips) its.push_back(Item{-1, 0, 0});  // zero-weight filler
+      const int nsteps = static_cast<int>(its.size()) / ips;
+      for (int s = 0; s < nsteps; ++s) {
+        const Item *si = &its[static_cast<size_t>(s) * ips];
+        if (write_items)
+          for (int e = 0; e < ips; ++e)
+            L.items.push_back(si[e].ql < 0 ? 0u : item_offset(g, tl, si[e].ql, si[e].pos));
+        // A operand for this step, MFMA lane order.
+        const size_t base = L.a.size();
+        L.a.resize(base + static_cast<size_t>(mfw) * 64 * epl * g.es);
+        uint8_t *dst = L.a.data() + base;
+        for (int i = 0; i < mfw; ++i)
+          for (int lane = 0; lane < 64; ++lane)
+            for (int e = 0; e < epl; ++e) {
+              const int m = wt * 16 * mfw + 16 * i + (lane & 15);
+              const int lg = lane >> 4;
+              // 16-bit: lane group lg holds items 2lg, 2lg+1, 4 channels each.
+              // f32: lane group lg holds item lg, element e = channel e.
+              const Item &it = f32 ? si[lg] : si[2 * lg + e / 4];
+              const int cin = f32 ? e : e % 4;
+              uint8_t *out = dst + ((static_cast<size_t>(i) * 64 + lane) * epl + e) * g.es;
+              if (it.ql < 0) {
+                std::memset(out, 0, g.es);
+              } else {
+                const int c = 4 * (ch * (tl.cc / 4) + it.ql) + cin;
+                src.copy(out, m, c, it.pos);
+              }
+            }
+        ++step;
+      }
+    }
+    L.step_ptr[static_cast<size_t>(wt) * (tl.nchunks + 1) + tl.nchunks] = step;
+  }
+}
+
+// Exact f32 KGS layout (kVarKgsExactF32): per 16-filter tile and chunk, the
+// union items with their kept-group bits and one 64-float A column set each
+// (lane l = 4*(4*group + channel) + row).
+void build_exact_f32_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const Mask4 *m4,
+                            Layout &L) {
+  const int wt_count = (g.c_out + 15) / 16;
+  L.variant = kVarKgsExactF32;
+  L.plan.mfw = 1;
+  L.plan.wave_tiles = wt_count;
+  L.plan.items_per_step = 1;
+  L.step_ptr.assign(static_cast<size_t>(wt_count) * (tl.nchunks + 1), 0);
+  L.item_ptr.assign(wt_count, 0);
+  WeightSource src{w, g, m4};
+  uint32_t item = 0;
+  for (int wt = 0; wt < wt_count; ++wt) {
+    L.item_ptr[wt] = item;
+    for (int ch = 0; ch < tl.nchunks; ++ch) {
+      L.step_ptr[static_cast<size_t>(wt) * (tl.nchunks + 1) + ch] = item;
+      for (const Item &it : chunk_items(g, m4, tl.cc, ch, wt * 4)) {
+        L.items.push_back(item_offset(g, tl, it.ql, it.pos));
+        L.keep.push_back(it.keep);
+        const size_t base = L.a.size();
+        L.a.resize(base + 64 * 4);
+        for (int lane = 0; lane < 64; ++lane) {
+          const int blk = lane >> 2, row = lane & 3;
+          const int gi = blk >> 2, cin = blk & 3;
+          const int m = wt * 16 + 4 * gi + row;
+          const int c = 4 * (ch * (tl.cc / 4) + it.ql) + cin;
+          uint8_t *out = L.a.data() + base + lane * 4;
+          if (it.keep & (1u << gi)) src.copy(out, m, c, it.pos);
+          else std::memset(out, 0, 4);
+        }
+        ++item;
+      }
+    }
+    L.step_ptr[static_cast<size_t>(wt) * (tl.nchunks + 1) + tl.nchunks] = item;
+  }
+}
+
+// Assemble header + canonical + layout sections.  With out == nullptr only
+// the size is computed.
+struct Sections {
+  uint64_t header, canon[4], step_ptr, item_ptr, items, keep, a, total;
+};
+
+Sections section_offsets(const Canon *c, int es, const Layout &L) {
+  Sections s{};
+  uint64_t off = align_up(sizeof(rt3d_pack_info), kAlign);
+  s.header = 0;
+  if (c) {
+    const uint64_t sz[4] = {c->group_ptr.size() * 4, c->pos.size() * 2, c->val_ptr.size() * 8,
+                            c->nvals * static_cast<uint64_t>(es)};
+    for (int i = 0; i < 4; ++i) {
+      s.canon[i] = off;
+      off = align_up(off + sz[i], kAlign);
+    }
+  }
+  s.step_ptr = off;
+  off = align_up(off + L.step_ptr.size() * 4, kAlign);
+  s.item_ptr = off;
+  off = align_up(off + L.item_ptr.size() * 4, kAlign);
+  s.items = off;
+  off = align_up(off + L.items.size() * 4, kAlign);
+  s.keep = off;
+  off = align_up(off + L.keep.size() * 4, kAlign);
+  s.a = off;
+  off = align_up(off + L.a.size(), kAlign);
+  s.total = off;
+  return s;
+}
+
+void fill_info(const rt3d_conv3d_desc *d, const Canon *c, const Layout &L, const Tiling &tl,
+               const Sections &s, bool vanilla, rt3d_pack_info *info) {
+  std::memset(info, 0, sizeof(*info));
+  info->magic = kMagic;
+  info->version = kVersion;
+  info->desc_hash = desc_hash(d);
+  info->variant = L.variant;
+  info->tile_groups = 4;
+  info->vanilla = vanilla ? 1 : 0;
+  info->packed_bytes = s.total;
+  if (c) {
+    const uint64_t sz[4] = {c->group_ptr.size() * 4, c->pos.size() * 2, c->val_ptr.size() * 8,
+                            c->nvals * static_cast<uint64_t>(esize_of(d->dtype))};
+    for (int i = 0; i < 4; ++i) {
+      info->canon_off[i] = s.canon[i];
+      info->canon_bytes[i] = sz[i];
+    }
+    info->kept_positions = c->pos.size();
+    info->kept_weights = c->nvals;
+  } else {
+    info->kept_positions = 0;
+    info->kept_weights = static_cast<uint64_t>(d->c_out) * d->c_in * d->kt * d->kh * d->kw;
+  }
+  info->derived_off = s.step_ptr;
+  info->derived_bytes = s.total - s.step_ptr;
+  Plan p = L.plan;
+  p.tiling = tl;
+  p.step_ptr_off = s.step_ptr;
+  p.item_ptr_off = s.item_ptr;
+  p.items_off = s.items;
+  p.a_off = s.a;
+  p.keep_off = s.keep;
+  std::memcpy(info->plan, &p, sizeof(p));
+}
+
+void write_blob(uint8_t *out, const rt3d_pack_info &info, const Canon *c, const uint8_t *w,
+                const rt3d_conv3d_desc *d, const Layout &L, const Sections &s) {
+  std::memset(out, 0, s.total);
+  std::memcpy(out, &info, sizeof(info));
+  if (c) {
+    std::memcpy(out + s.canon[0], c->group_ptr.data(), c->group_ptr.size() * 4);
+    std::memcpy(out + s.canon[1], c->pos.data(), c->pos.size() * 2);
+    std::memcpy(out + s.canon[2], c->val_ptr.data(), c->val_ptr.size() * 8);
+    // vals: group (p, q), rows i (filter), then j (channel), then kept r.
+    const int es = esize_of(d->dtype);
+    const int ks = d->kt * d->kh * d->kw;
+    uint8_t *vals = out + s.canon[3];
+    for (int p = 0; p < c->P; ++p) {
+      const int gm = std::min(d->g_m, d->c_out - p * d->g_m);
+      for (int q = 0; q < c->Q; ++q) {
+        const int gn = std::min(d->g_n, d->c_in - q * d->g_n);
+        const size_t gi = static_cast<size_t>(p) * c->Q + q;
+        const uint32_t k0 = c->group_ptr[gi], k = c->group_ptr[gi + 1] - k0;
+        uint8_t *dst = vals + c->val_ptr[gi] * es;
+        for (int i = 0; i < gm; ++i)
+          for (int j = 0; j < gn; ++j)
+            for (uint32_t r = 0; r < k; ++r) {
+              const size_t widx =
+                  (static_cast<size_t>(p * d->g_m + i) * d->c_in + q * d->g_n + j) * ks + c->pos[k0 + r];
+              std::memcpy(dst + ((static_cast<size_t>(i) * gn + j) * k + r) * es, w + widx * es, es);
+            }
+      }
+    }
+  }
+  std::memcpy(out + s.step_ptr, L.step_ptr.data(), L.step_ptr.size() * 4);
+  std::memcpy(out + s.item_ptr, L.item_ptr.data(), L.item_ptr.size() * 4);
+  if (!L.items.empty()) std::memcpy(out + s.items, L.items.data(), L.items.size() * 4);
+  if (!L.keep.empty()) std::memcpy(out + s.keep, L.keep.data(), L.keep.size() * 4);
+  if (!L.a.empty()) std::memcpy(out + s.a, L.a.data(), L.a.size());
+}
+
+// Build everything for a KGS pack (w may be null when only sizing).
+rt3d_status plan_kgs(const rt3d_conv3d_desc *d, const uint8_t *mask, const uint8_t *w,
+                     Canon &c, Layout &L, Tiling &tl, bool &vanilla) {
+  rt3d_status st = canon_index(d, mask, c);
+  if (st != RT3D_OK) return st;
+  const int ks = d->kt * d->kh * d->kw;
+  vanilla = true;
+  for (size_t gi = 0; gi + 1 < c.group_ptr.size(); ++gi) {
+    const uint32_t k = c.group_ptr[gi + 1] - c.group_ptr[gi];
+    if (k != 0 && k != static_cast<uint32_t>(ks)) {
+      vanilla = false;
+      break;
+    }
+  }
+  const Geom g = geom_of(d);
+  tl = choose_tiling(g);
+  if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
+  Mask4 m4{mask, c.Q, ks, d->g_m / 4, d->g_n / 4};
+  static const uint8_t zero = 0;
+  const uint8_t *wsrc = w ? w : &zero;
+  if (!w) {
+    // Sizing only: build the layout from a weight source that is never
+    // dereferenced beyond the mask check by using an all-zero byte span.
+    // The layout size does not depend on weight values.
+  }
+  if (g.es == 4) {
+    if (!w) {
+      // size-only pass: reuse the builders with a scratch weight tensor
+      std::vector<uint8_t> scratch(static_cast<size_t>(g.c_out) * g.c_in * ks * g.es, 0);
+      build_exact_f32_layout(g, tl, scratch.data(), &m4, L);
+    } else {
+      build_exact_f32_layout(g, tl, wsrc, &m4, L);
+    }
+  } else {
+    if (!w) {
+      std::vector<uint8_t> scratch(static_cast<size_t>(g.c_out) * g.c_in * ks * g.es, 0);
+      build_items_layout(g, tl, scratch.data(), &m4, L);
+    } else {
+      build_items_layout(g, tl, wsrc, &m4, L);
+    }
+  }
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// Forward helpers
+// ---------------------------------------------------------------------------
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+rt3d_status check_info(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, bool sparse) {
+  if (!info) return fail(RT3D_ERR_INVALID_ARG, "info is NULL");
+  if (info->magic != kMagic || info->version != kVersion)
+    return fail(RT3D_ERR_BLOB_MISMATCH, "info was not written by this library version");
+  if (info->desc_hash != desc_hash(d))
+    return fail(RT3D_ERR_BLOB_MISMATCH, "blob was packed for a different layer description");
+  const bool is_sparse = info->variant == kVarKgsUnion16 || info->variant == kVarKgsExactF32;
+  if (is_sparse != sparse)
+    return fail(RT3D_ERR_BLOB_MISMATCH, sparse ? "dense blob passed to the KGS forward"
+                                               : "KGS blob passed to the dense forward");
+  return ok();
+}
+
+rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, const void *blob,
+                     const void *x, const float *bias, const void *residual, void *y,
+                     void *stream, bool sparse) {
+  rt3d_status st = check_desc(d, sparse);
+  if (st != RT3D_OK) return st;
+  st = check_info(d, info, sparse);
+  if (st != RT3D_OK) return st;
+  if (d->n == 0) return ok();  // empty batch: nothing is read or written
+  if (!blob || !x || !y) return fail(RT3D_ERR_INVALID_ARG, "blob, x and y must be non-NULL");
+  const bool want_res = (d->flags & RT3D_RESIDUAL) != 0;
+  if (want_res != (residual != nullptr))
+    return fail(RT3D_ERR_INVALID_ARG, "residual must be given exactly when RT3D_RESIDUAL is set");
+  if (!aligned16(blob) || !aligned16(x) || !aligned16(y) || (residual && !aligned16(residual)) ||
+      (bias && !aligned16(bias)))
+    return fail(RT3D_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  Plan p;
+  std::memcpy(&p, info->plan, sizeof(p));
+  const Geom g = geom_of(d);
+  const Tiling &tl = p.tiling;
+  const uint8_t *b = static_cast<const uint8_t *>(blob);
+  ConvArgs a{};
+  a.x = x;
+  a.y = y;
+  a.res = residual;
+  a.bias = bias;
+  a.step_ptr = reinterpret_cast<const uint32_t *>(b + p.step_ptr_off);
+  a.item_ptr = reinterpret_cast<const uint32_t *>(b + p.item_ptr_off);
+  a.items = reinterpret_cast<const uint32_t *>(b + p.items_off);
+  a.keep = reinterpret_cast<const uint32_t *>(b + p.keep_off);
+  a.a = b + p.a_off;
+  a.n = g.n; a.c_in = g.c_in; a.c_out = g.c_out; a.t = g.t; a.h = g.h; a.w = g.w;
+  a.to = g.to; a.ho = g.ho; a.wo = g.wo;
+  a.st = g.st; a.sh = g.sh; a.sw = g.sw; a.pt = g.pt; a.ph = g.ph; a.pw = g.pw;
+  a.bt = tl.bt; a.bh = tl.bh; a.bw = tl.bw;
+  a.nbt = (g.to + tl.bt - 1) / tl.bt;
+  a.nbh = (g.ho + tl.bh - 1) / tl.bh;
+  a.nbw = (g.wo + tl.bw - 1) / tl.bw;
+  a.ht = tl.ht; a.hh = tl.hh; a.hw = tl.hw; a.cc = tl.cc; a.row = tl.row; a.nchunks = tl.nchunks;
+  a.wave_tiles = p.wave_tiles;
+  a.relu = (d->flags & RT3D_RELU) ? 1 : 0;
+  int e;
+  switch (info->variant) {
+    case kVarDenseItems16:
+    case kVarKgsUnion16:
+      e = launch_items16(a, d->dtype, p.mfw, stream);
+      break;
+    case kVarDenseItemsF32:
+      e = launch_items_f32(a, p.mfw, stream);
+      break;
+    case kVarKgsExactF32:
+      e = launch_kgs_exact_f32(a, stream);
+      break;
+    default:
+      return fail(RT3D_ERR_BLOB_MISMATCH, "unknown kernel variant %u", info->variant);
+  }
+  if (e != hipSuccess)
+    return fail(RT3D_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(static_cast<hipError_t>(e)));
+  return ok();
+}
+
+}  // namespace
+}  // namespace rt3d
+
+using namespace rt3d;
+
+extern "C" {
+
+const char *rt3d_status_string(rt3d_status s) {
+  switch (s) {
+    case RT3D_OK: return "ok";
+    case RT3D_ERR_INVALID_ARG: return "invalid argument";
+    case RT3D_ERR_UNSUPPORTED: return "unsupported configuration";
+    case RT3D_ERR_BUFFER_TOO_SMALL: return "buffer too small";
+    case RT3D_ERR_BLOB_MISMATCH: return "packed blob does not match the layer";
+    case RT3D_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char *rt3d_last_error_detail(void) { return g_detail.c_str(); }
+
+rt3d_status rt3d_conv3d_out_shape(const rt3d_conv3d_desc *d, int32_t *to, int32_t *ho,
+                                  int32_t *wo) {
+  rt3d_status st = check_desc(d, false);
+  if (st != RT3D_OK) return st;
+  if (!to || !ho || !wo) return fail(RT3D_ERR_INVALID_ARG, "output pointers must be non-NULL");
+  const Geom g = geom_of(d);
+  *to = g.to;
+  *ho = g.ho;
+  *wo = g.wo;
+  return ok();
+}
+
+rt3d_status rt3d_kgs_pack_size(const rt3d_conv3d_desc *d, const uint8_t *mask, uint64_t *bytes) {
+  rt3d_status st = check_desc(d, true);
+  if (st != RT3D_OK) return st;
+  if (!mask || !bytes) return fail(RT3D_ERR_INVALID_ARG, "mask and bytes must be non-NULL");
+  Canon c;
+  Layout L;
+  Tiling tl;
+  bool vanilla;
+  st = plan_kgs(d, mask, nullptr, c, L, tl, vanilla);
+  if (st != RT3D_OK) return st;
+  *bytes = section_offsets(&c, esize_of(d->dtype), L).total;
+  return ok();
+}
+
+rt3d_status rt3d_kgs_pack(const rt3d_conv3d_desc *d, const void *w_dense, const uint8_t *mask,
+                          void *blob, uint64_t blob_bytes, rt3d_pack_info *info) {
+  rt3d_status st = check_desc(d, true);
+  if (st != RT3D_OK) return st;
+  if (!w_dense || !mask || !blob || !info)
+    return fail(RT3D_ERR_INVALID_ARG, "w_dense, mask, blob and info must be non-NULL");
+  Canon c;
+  Layout L;
+  Tiling tl;
+  bool vanilla;
+  st = plan_kgs(d, mask, static_cast<const uint8_t *>(w_dense), c, L, tl, vanilla);
+  if (st != RT3D_OK) return st;
+  const Sections s = section_offsets(&c, esize_of(d->dtype), L);
+  if (blob_bytes < s.total)
+    return fail(RT3D_ERR_BUFFER_TOO_SMALL, "blob needs %llu bytes, got %llu",
+                static_cast<unsigned long long>(s.total), static_cast<unsigned long long>(blob_bytes));
+  rt3d_pack_info tmp;
+  fill_info(d, &c, L, tl, s, vanilla, &tmp);
+  write_blob(static_cast<uint8_t *>(blob), tmp, &c, static_cast<const uint8_t *>(w_dense), d, L, s);
+  *info = tmp;
+  return ok();
+}
+
+rt3d_status rt3d_kgs_unpack(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, const void *blob,
+                            void *w_out) {
+  rt3d_status st = check_desc(d, true);
+  if (st != RT3D_OK) return st;
+  if (!blob || !w_out) return fail(RT3D_ERR_INVALID_ARG, "blob and w_out must be non-NULL");
+  st = check_info(d, info, true);
+  if (st != RT3D_OK) return st;
+  const uint8_t *b = static_cast<const uint8_t *>(blob);
+  const int es = esize_of(d->dtype);
+  const int ks = d->kt * d->kh * d->kw;
+  const int P = (d->c_out + d->g_m - 1) / d->g_m, Q = (d->c_in + d->g_n - 1) / d->g_n;
+  const uint32_t *gp = reinterpret_cast<const uint32_t *>(b + info->canon_off[0]);
+  const uint16_t *pos = reinterpret_cast<const uint16_t *>(b + info->canon_off[1]);
+  const uint64_t *vp = reinterpret_cast<const uint64_t *>(b + info->canon_off[2]);
+  const uint8_t *vals = b + info->canon_off[3];
+  uint8_t *w = static_cast<uint8_t *>(w_out);
+  std::memset(w, 0, static_cast<size_t>(d->c_out) * d->c_in * ks * es);
+  for (int p = 0; p < P; ++p) {
+    const int gm = std::min(d->g_m, d->c_out - p * d->g_m);
+    for (int q = 0; q < Q; ++q) {
+      const int gn = std::min(d->g_n, d->c_in - q * d->g_n);
+      const size_t gi = static_cast<size_t>(p) * Q + q;
+      const uint32_t k0 = gp[gi], k = gp[gi + 1] - k0;
+      for (int i = 0; i < gm; ++i)
+        for (int j = 0; j < gn; ++j)
+          for (uint32_t r = 0; r < k; ++r) {
+            const size_t widx =
+                (static_cast<size_t>(p * d->g_m + i) * d->c_in + q * d->g_n + j) * ks + pos[k0 + r];
+            std::memcpy(w + widx * es, vals + (vp[gi] + (static_cast<size_t>(i) * gn + j) * k + r) * es, es);
+          }
+    }
+  }
+  return ok();
+}
+
+rt3d_status rt3d_conv3d_workspace_size(const rt3d_conv3d_desc *d, const rt3d_pack_info *info,
+                                       uint64_t *bytes) {
+  rt3d_status st = check_desc(d, false);
+  if (st != RT3D_OK) return st;
+  if (!info || !bytes) return fail(RT3D_ERR_INVALID_ARG, "info and bytes must be non-NULL");
+  if (info->magic != kMagic) return fail(RT3D_ERR_BLOB_MISMATCH, "info was not written by this library");
+  *bytes = 0;
+  return ok();
+}
+
+rt3d_status rt3d_kgs_conv3d_fwd(const rt3d_conv3d_desc *d, const rt3d_pack_info *info,
+                                const void *blob_dev, const void *x, const float *bias,
+                                const void *residual, void *y, void *workspace,
+                                uint64_t workspace_bytes, void *stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  return run_conv(d, info, blob_dev, x, bias, residual, y, stream, true);
+}
+
+rt3d_status rt3d_dense_pack_size(const rt3d_conv3d_desc *d, uint64_t *bytes) {
+  rt3d_status st = check_desc(d, false);
+  if (st != RT3D_OK) return st;
+  if (!bytes) return fail(RT3D_ERR_INVALID_ARG, "bytes must be non-NULL");
+  const Geom g = geom_of(d);
+  const Tiling tl = choose_tiling(g);
+  if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
+  std::vector<uint8_t> scratch(static_cast<size_t>(g.c_out) * g.c_in * g.ks * g.es, 0);
+  Layout L;
+  build_items_layout(g, tl, scratch.data(), nullptr, L);
+  *bytes = section_offsets(nullptr, g.es, L).total;
+  return ok();
+}
+
+rt3d_status rt3d_dense_pack(const rt3d_conv3d_desc *d, const void *w_dense, void *blob,
+                            uint64_t blob_bytes, rt3d_pack_info *info) {
+  rt3d_status st = check_desc(d, false);
+  if (st != RT3D_OK) return st;
+  if (!w_dense || !blob || !info)
+    return fail(RT3D_ERR_INVALID_ARG, "w_dense, blob and info must be non-NULL");
+  const Geom g = geom_of(d);
+  const Tiling tl = choose_tiling(g);
+  if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
+  Layout L;
+  build_items_layout(g, tl, static_cast<const uint8_t *>(w_dense), nullptr, L);
+  const Sections s = section_offsets(nullptr, g.es, L);
+  if (blob_bytes < s.total)
+    return fail(RT3D_ERR_BUFFER_TOO_SMALL, "blob needs %llu bytes, got %llu",
+                static_cast<unsigned long long>(s.total), static_cast<unsigned long long>(blob_bytes));
+  rt3d_pack_info tmp;
+  fill_info(d, nullptr, L, tl, s, false, &tmp);
+  write_blob(static_cast<uint8_t *>(blob), tmp, nullptr, nullptr, d, L, s);
+  *info = tmp;
+  return ok();
+}
+
+rt3d_status rt3d_conv3d_dense_fwd(const rt3d_conv3d_desc *d, const rt3d_pack_info *info,
+                                  const void *blob_dev, const void *x, const float *bias,
+                                  const void *residual, void *y, void *workspace,
+                                  uint64_t workspace_bytes, void *stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  return run_conv(d, info, blob_dev, x, bias, residual, y, stream, false);
+}
+
+rt3d_status rt3d_maxpool3d_fwd(int32_t n, int32_t c, int32_t t, int32_t h, int32_t w, int32_t kt,
+                               int32_t kh, int32_t kw, int32_t st, int32_t sh, int32_t sw,
+                               int32_t dtype, const void *x, void *y, void *stream) {
+  if (n < 0 || c <= 0 || t <= 0 || h <= 0 || w <= 0 || kt <= 0 || kh <= 0 || kw <= 0 || st <= 0 ||
+      sh <= 0 || sw <= 0)
+    return fail(RT3D_ERR_INVALID_ARG, "pooling sizes must be positive");
+  if (dtype != RT3D_F32 && dtype != RT3D_BF16 && dtype != RT3D_F16)
+    return fail(RT3D_ERR_INVALID_ARG, "unknown dtype %d", dtype);
+  if (kt > t || kh > h || kw > w) return fail(RT3D_ERR_INVALID_ARG, "window larger than the input");
+  if (n == 0) return ok();
+  if (!x || !y) return fail(RT3D_ERR_INVALID_ARG, "x and y must be non-NULL");
+  if (!aligned16(x) || !aligned16(y))
+    return fail(RT3D_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
+  const int to = (t - kt) / st + 1, ho = (h - kh) / sh + 1, wo = (w - kw) / sw + 1;
+  const int e = launch_maxpool(n, c, t, h, w, kt, kh, kw, st, sh, sw, to, ho, wo, dtype, x, y, stream);
+  if (e != hipSuccess)
+    return fail(RT3D_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(static_cast<hipError_t>(e)));
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,77 @@
+// Internal definitions shared by the host planner and the HIP kernels of
+// librt3d.  Not part of the public ABI.
+#pragma once
+
+#include <stdint.h>
+
+#include "../../include/rt3d.h"
+
+namespace rt3d {
+
+constexpr uint64_t kMagic = 0x314b4e3344335452ull;  // "RT3D3NK1" little-endian
+constexpr uint32_t kVersion = 1;
+constexpr uint64_t kAlign = 256;                    // section alignment in a blob
+
+// Kernel mappings (the `variant` field of rt3d_pack_info).
+enum Variant : uint32_t {
+  kVarDenseItems16 = 1,  // dense, 16x16x32 MFMA (bf16/f16), all (block, position) items
+  kVarDenseItemsF32 = 2, // dense, 16x16x4 f32 MFMA
+  kVarKgsUnion16 = 3,    // KGS, 16x16x32 MFMA over the union of a 16-filter tile's items
+  kVarKgsExactF32 = 4,   // KGS, 4x4x1 f32 MFMA, exact per 4x4 kernel block
+};
+
+// Voxel tiling shared by every conv kernel: a workgroup computes a brick of
+// bt x bh x bw output voxels of one batch item (64 voxel slots per wave
+// step), staging the input brick plus halo for a chunk of `cc` channels in
+// LDS with rows of `row` bytes per voxel.
+struct Tiling {
+  int32_t bt, bh, bw;      // output brick
+  int32_t ht, hh, hw;      // halo extent in input voxels
+  int32_t cc;              // channels per LDS chunk
+  int32_t row;             // LDS bytes per halo voxel (cc * esize + pad)
+  int32_t slots;           // voxel slots per workgroup (multiple of 64)
+  int32_t nchunks;         // ceil(c_in / cc)
+};
+
+// Launch plan chosen at pack time, kept in rt3d_pack_info::plan (and hence
+// in the blob header, which is a copy of the info struct).
+struct Plan {
+  Tiling tiling;
+  int32_t mfw;             // 16-filter MFMA rows per wave tile
+  int32_t wave_tiles;      // number of wave tiles
+  int32_t items_per_step;  // items consumed per K-step
+  int32_t pad0;
+  uint64_t step_ptr_off;   // u32 [wave_tiles][nchunks + 1]
+  uint64_t item_ptr_off;   // u32 [wave_tiles]
+  uint64_t items_off;      // u32 [...] LDS byte offset of each item
+  uint64_t a_off;          // dtype [...], MFMA operand order
+  uint64_t keep_off;       // u32 [...] (exact f32 variant: kept-group bits per item)
+};
+static_assert(sizeof(Plan) <= sizeof(((rt3d_pack_info *)0)->plan), "plan does not fit");
+
+// Everything a conv kernel needs, passed by value.
+struct ConvArgs {
+  const void *x;
+  void *y;
+  const void *res;
+  const float *bias;
+  const uint32_t *step_ptr;
+  const uint32_t *item_ptr;
+  const uint32_t *items;
+  const uint32_t *keep;
+  const void *a;
+  int32_t n, c_in, c_out, t, h, w, to, ho, wo;
+  int32_t st, sh, sw, pt, ph, pw;
+  int32_t bt, bh, bw, nbt, nbh, nbw;
+  int32_t ht, hh, hw, cc, row, nchunks;
+  int32_t wave_tiles, relu;
+};
+
+// Kernel launchers (rt3d_kernels.hip).  Return hipSuccess or the launch error.
+int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream);
+int launch_items_f32(const ConvArgs &a, int mfw, void *stream);
+int launch_kgs_exact_f32(const ConvArgs &a, void *stream);
+int launch_maxpool(int n, int c, int t, int h, int w, int kt, int kh, int kw, int st, int sh,
+                   int sw, int to, int ho, int wo, int dtype, const void *x, void *y, void *stream);
+
+}  // namespace rt3d

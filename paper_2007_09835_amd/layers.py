@@ -1,0 +1,72 @@
+"""Layer objects over the C ABI: pack once on the host, keep the blob and
+bias on the device, launch the HIP kernels per call.
+
+Memory management and argument marshalling only; every arithmetic step of a
+forward pass runs in librt3d's kernels.  Activations are channels-last
+contiguous device tensors [n, t, h, w, c].
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import rt3d
+
+TORCH_DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
+
+
+class Conv3d:
+    """One packed 3-D convolution (dense when ``mask`` is None, else KGS).
+
+    ``w`` is a host tensor [M][N][kt][kh][kw] already in the layer dtype;
+    ``bias`` a host float array [M] (or None); ``mask`` uint8 [P][Q][K_s].
+    """
+
+    def __init__(self, c_in: int, c_out: int, thw: Sequence[int], k, stride, pad, w,
+                 bias=None, mask: Optional[np.ndarray] = None, dtype: str = "bf16",
+                 relu: bool = True, residual: bool = False, g=(4, 4), device="cuda"):
+        self.dtype = dtype
+        self.sparse = mask is not None
+        self.desc = rt3d.make_desc(1, c_in, c_out, tuple(thw), tuple(k), tuple(stride), tuple(pad),
+                                   tuple(g), dtype, relu=relu, residual=residual)
+        if self.sparse:
+            blob, self.info = rt3d.rt3d_kgs_pack(self.desc, w, mask)
+        else:
+            blob, self.info = rt3d.rt3d_dense_pack(self.desc, w)
+        self.blob = torch.from_numpy(blob).to(device)
+        self.bias = None if bias is None else torch.as_tensor(
+            np.asarray(bias, dtype=np.float32)).to(device)
+        self.out_thw = rt3d.rt3d_conv3d_out_shape(self.desc)
+        self.c_out = c_out
+        self.device = device
+
+    def desc_for(self, n: int) -> rt3d.Conv3dDesc:
+        d = rt3d.Conv3dDesc.from_buffer_copy(self.desc)
+        d.n = n
+        return d
+
+    def out_shape(self, n: int):
+        return (n, *self.out_thw, self.c_out)
+
+    def __call__(self, x: torch.Tensor, residual: Optional[torch.Tensor] = None,
+                 out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        n = x.shape[0]
+        if out is None:
+            out = torch.empty(self.out_shape(n), dtype=TORCH_DTYPES[self.dtype], device=x.device)
+        fwd = rt3d.rt3d_kgs_conv3d_fwd if self.sparse else rt3d.rt3d_conv3d_dense_fwd
+        fwd(self.desc_for(n), self.info, self.blob, x, self.bias, residual, out, None, stream)
+        return out
+
+
+def maxpool3d(x: torch.Tensor, k, stride, dtype: str, out: Optional[torch.Tensor] = None,
+              stream=None) -> torch.Tensor:
+    n, t, h, w, c = x.shape
+    to, ho, wo = ((t - k[0]) // stride[0] + 1, (h - k[1]) // stride[1] + 1,
+                  (w - k[2]) // stride[2] + 1)
+    if out is None:
+        out = torch.empty((n, to, ho, wo, c), dtype=x.dtype, device=x.device)
+    rt3d.rt3d_maxpool3d_fwd(x, out, k, stride, dtype, stream)
+    return out

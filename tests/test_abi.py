@@ -1,0 +1,210 @@
+"""Host-side tests of the C ABI (no GPU needed).
+
+* the library loads and exports every function include/rt3d.h declares;
+* the canonical KGS sections written by rt3d_kgs_pack are bit-identical to
+  the oracle's pack (Section 3 compact format) for every dtype, group size
+  and partial-group shape;
+* unpack(pack(W, mask)) == W * expand(mask) bit-exactly;
+* bookkeeping (kept positions / weights, vanilla detection, sizes);
+* every documented error path returns its status code.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2007_09835_amd import rt3d
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def built():
+    from paper_2007_09835_amd import build
+    build.build(force=False)
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "rt3d.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rt3d_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = header_functions()
+    assert len(names) >= 12
+    lib = ctypes.CDLL(rt3d.LIB_PATH)
+    for name in names:
+        assert hasattr(lib, name), name
+    assert sorted(rt3d.EXPORTED) == names
+
+
+def _np_dtype(dt):
+    return {"f32": np.float32, "f16": np.float16, "bf16": np.uint16}[dt]
+
+
+def _weights(rng, shape, dt):
+    w = rng.standard_normal(shape).astype(np.float32)
+    if dt == "f32":
+        return w
+    if dt == "f16":
+        return w.astype(np.float16)
+    return torch.from_numpy(w).to(torch.bfloat16).view(torch.uint16).numpy()
+
+
+PACK_CASES = [
+    # c_out, c_in, k, g_m, g_n, keep_frac
+    (32, 16, (3, 3, 3), 4, 4, 0.33),
+    (13, 10, (3, 3, 3), 4, 4, 0.4),
+    (9, 7, (1, 3, 3), 4, 4, 0.5),
+    (6, 11, (3, 1, 1), 4, 4, 0.6),
+    (24, 20, (3, 3, 3), 8, 4, 0.3),
+    (40, 36, (1, 1, 1), 16, 8, 0.5),
+    (5, 6, (1, 1, 3), 4, 4, 0.5),
+    (8, 8, (3, 3, 3), 4, 4, 0.0),
+    (8, 8, (3, 3, 3), 4, 4, 1.0),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(PACK_CASES)))
+@pytest.mark.parametrize("dt", ["f32", "bf16", "f16"])
+def test_canonical_pack_matches_oracle_bitwise(ci, dt):
+    c_out, c_in, k, g_m, g_n, frac = PACK_CASES[ci]
+    rng = np.random.default_rng(1000 + ci)
+    w = _weights(rng, (c_out, c_in, *k), dt)
+    P, Q, ks = -(-c_out // g_m), -(-c_in // g_n), k[0] * k[1] * k[2]
+    mask = (rng.random((P, Q, ks)) < frac).astype(np.uint8)
+    desc = rt3d.make_desc(1, c_in, c_out, (4, 5, 6), k, (1, 1, 1), tuple(x // 2 for x in k),
+                          (g_m, g_n), dt)
+    blob, info = rt3d.rt3d_kgs_pack(desc, w, mask)
+    gp, pos, vp, vals = rt3d.canonical_sections(info, blob, _np_dtype(dt))
+    ogp, opos, ovp, ovals = oracle.kgs_pack(w, mask, g_m, g_n)
+    assert np.array_equal(gp, ogp)
+    assert np.array_equal(pos, opos)
+    assert np.array_equal(vp, ovp)
+    assert vals.tobytes() == ovals.tobytes()
+    assert info.kept_positions == mask.sum()
+    assert info.kept_weights == len(ovals)
+    assert info.packed_bytes == len(blob) == rt3d.rt3d_kgs_pack_size(desc, mask)
+    # round trip
+    out = np.zeros_like(w)
+    rt3d.rt3d_kgs_unpack(desc, info, blob, out)
+    full = np.repeat(np.repeat(mask, g_m, 0), g_n, 1)[:c_out, :c_in].reshape(c_out, c_in, *k)
+    expect = np.where(full == 1, w, np.zeros_like(w))
+    assert out.tobytes() == expect.tobytes()
+
+
+def test_pack_never_reads_pruned_weights():
+    """Pruned positions hold NaN; the blob must be identical to packing the
+    zero-filled weights (except nothing reads them at all)."""
+    rng = np.random.default_rng(5)
+    w = rng.standard_normal((16, 8, 3, 3, 3)).astype(np.float32)
+    mask = (rng.random((4, 2, 27)) < 0.3).astype(np.uint8)
+    full = np.repeat(np.repeat(mask, 4, 0), 4, 1).reshape(w.shape)
+    w_nan = np.where(full == 1, w, np.float32(np.nan))
+    w_zero = np.where(full == 1, w, np.float32(0))
+    for dt_w in (w_nan, w_zero):
+        desc = rt3d.make_desc(1, 8, 16, (4, 4, 4), dtype="f32")
+        blob, info = rt3d.rt3d_kgs_pack(desc, dt_w, mask)
+        if dt_w is w_nan:
+            b_nan = blob
+        else:
+            b_zero = blob
+    assert b_nan.tobytes() == b_zero.tobytes()
+
+
+def test_vanilla_mask_is_detected():
+    rng = np.random.default_rng(2)
+    w = rng.standard_normal((16, 16, 3, 3, 3)).astype(np.float32)
+    mask = np.zeros((4, 4, 27), dtype=np.uint8)
+    mask[rng.random((4, 4)) < 0.4] = 1
+    desc = rt3d.make_desc(1, 16, 16, (4, 4, 4), dtype="bf16")
+    wb = _weights(rng, w.shape, "bf16")
+    _, info = rt3d.rt3d_kgs_pack(desc, wb, mask)
+    assert info.vanilla == 1
+    mask[0, 0, 0] ^= 1
+    _, info = rt3d.rt3d_kgs_pack(desc, wb, mask)
+    assert info.vanilla == 0
+
+
+def test_dense_pack_sizes_and_info():
+    desc = rt3d.make_desc(2, 64, 128, (16, 56, 56), dtype="bf16")
+    w = _weights(np.random.default_rng(0), (128, 64, 3, 3, 3), "bf16")
+    blob, info = rt3d.rt3d_dense_pack(desc, w)
+    assert info.packed_bytes == len(blob) == rt3d.rt3d_dense_pack_size(desc)
+    assert info.kept_weights == 128 * 64 * 27
+    assert rt3d.rt3d_conv3d_out_shape(desc) == (16, 56, 56)
+    assert rt3d.rt3d_conv3d_workspace_size(desc, info) == 0
+
+
+def _expect_status(status, fn, *args):
+    with pytest.raises(rt3d.Rt3dError) as ei:
+        fn(*args)
+    assert ei.value.status == status, ei.value.detail
+    assert ei.value.detail
+
+
+def test_error_paths():
+    rng = np.random.default_rng(3)
+    w = rng.standard_normal((8, 8, 3, 3, 3)).astype(np.float32)
+    mask = np.ones((2, 2, 27), dtype=np.uint8)
+    good = rt3d.make_desc(1, 8, 8, (4, 4, 4), dtype="f32")
+    blob, info = rt3d.rt3d_kgs_pack(good, w, mask)
+
+    bad_mask = mask.copy()
+    bad_mask[1, 1, 5] = 2
+    _expect_status(rt3d.RT3D_ERR_INVALID_ARG, rt3d.rt3d_kgs_pack, good, w, bad_mask)
+    _expect_status(rt3d.RT3D_ERR_INVALID_ARG, rt3d.rt3d_kgs_pack_size,
+                   rt3d.make_desc(1, 0, 8, (4, 4, 4)), mask)
+    _expect_status(rt3d.RT3D_ERR_UNSUPPORTED, rt3d.rt3d_kgs_pack_size,
+                   rt3d.make_desc(1, 8, 8, (4, 4, 4), stride=(3, 1, 1)), mask)
+    _expect_status(rt3d.RT3D_ERR_UNSUPPORTED, rt3d.rt3d_kgs_pack_size,
+                   rt3d.make_desc(1, 8, 8, (4, 4, 4), g=(2, 4)), mask)
+    big = rt3d.make_desc(1, 8, 8, (9, 9, 9), k=(9, 1, 1), pad=(0, 0, 0))
+    _expect_status(rt3d.RT3D_ERR_UNSUPPORTED, rt3d.rt3d_kgs_pack_size, big,
+                   np.ones((2, 2, 9), np.uint8))
+    _expect_status(rt3d.RT3D_ERR_INVALID_ARG, rt3d.rt3d_kgs_pack_size,
+                   rt3d.make_desc(1, 8, 8, (1, 1, 1), k=(3, 3, 3), pad=(0, 0, 0)), mask)
+    _expect_status(rt3d.RT3D_ERR_INVALID_ARG, rt3d.rt3d_conv3d_out_shape,
+                   rt3d.make_desc(1, 8, 8, (4, 4, 4), dtype=7))
+
+    # too-small buffer, straight through the C ABI
+    lib = rt3d.load()
+    small = np.zeros(16, np.uint8)
+    inf = rt3d.PackInfo()
+    st = lib.rt3d_kgs_pack(ctypes.byref(good), w.ctypes.data, mask.ctypes.data, small.ctypes.data,
+                           16, ctypes.byref(inf))
+    assert st == rt3d.RT3D_ERR_BUFFER_TOO_SMALL
+    st = lib.rt3d_kgs_pack(ctypes.byref(good), None, mask.ctypes.data, small.ctypes.data, 16,
+                           ctypes.byref(inf))
+    assert st == rt3d.RT3D_ERR_INVALID_ARG
+
+    # blob/desc mismatch and the dense/KGS confusion are caught before any launch
+    other = rt3d.make_desc(1, 8, 8, (4, 4, 5), dtype="f32")
+    out = np.zeros_like(w)
+    _expect_status(rt3d.RT3D_ERR_BLOB_MISMATCH, rt3d.rt3d_kgs_unpack, other, info, blob, out)
+    st = lib.rt3d_conv3d_dense_fwd(ctypes.byref(good), ctypes.byref(info), 16, 16, None, None, 16,
+                                   None, 0, None)
+    assert st == rt3d.RT3D_ERR_BLOB_MISMATCH
+    tampered = rt3d.PackInfo.from_buffer_copy(info)
+    tampered.magic = 0
+    st = lib.rt3d_kgs_conv3d_fwd(ctypes.byref(good), ctypes.byref(tampered), 16, 16, None, None, 16,
+                                 None, 0, None)
+    assert st == rt3d.RT3D_ERR_BLOB_MISMATCH
+    # residual flag without a residual pointer, misaligned pointers
+    res_desc = rt3d.make_desc(1, 8, 8, (4, 4, 4), dtype="f32", residual=True)
+    _, rinfo = rt3d.rt3d_kgs_pack(res_desc, w, mask)
+    st = lib.rt3d_kgs_conv3d_fwd(ctypes.byref(res_desc), ctypes.byref(rinfo), 256, 256, None, None,
+                                 256, None, 0, None)
+    assert st == rt3d.RT3D_ERR_INVALID_ARG
+    st = lib.rt3d_kgs_conv3d_fwd(ctypes.byref(good), ctypes.byref(info), 256, 258, None, None, 256,
+                                 None, 0, None)
+    assert st == rt3d.RT3D_ERR_INVALID_ARG
+    st = lib.rt3d_maxpool3d_fwd(1, 8, 4, 4, 4, 5, 2, 2, 1, 2, 2, 0, 256, 256, None)
+    assert st == rt3d.RT3D_ERR_INVALID_ARG
+    assert lib.rt3d_status_string(99)
+    assert lib.rt3d_status_string(rt3d.RT3D_ERR_HIP) == b"HIP runtime error"

@@ -1,0 +1,233 @@
+"""GPU parity: the HIP kernels through the C ABI against the CPU oracle.
+
+Bars: fp32 relative L2 <= 1e-4, bf16 / fp16 <= 1e-2 (float32 accumulation
+in the kernels, float64 in the oracle, outputs rounded to the layer dtype).
+Small layers are compared element by element in full; full-size workload
+layers are compared on sampled outputs that the oracle computes one by one.
+Invariants that need no oracle (all-zero mask, vanilla-pruned groups,
+determinism) are checked bit-exactly.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from harness import TOL, LayerCase, from_device_ndhwc, rel_l2, rounded, sample_indices, to_device_ndhwc
+from paper_2007_09835_amd import build, layers, synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def built():
+    build.build(force=False)
+
+
+def masked(tag, c_out, c_in, k, keep, g=(4, 4)):
+    P, Q = -(-c_out // g[0]), -(-c_in // g[1])
+    return synth.kgs_mask(synth.rng_for(tag, "mask"), P, Q, k[0] * k[1] * k[2], keep)
+
+
+def check_full(case, label):
+    got = case.run_gpu()
+    ref = case.oracle_full()
+    err = rel_l2(got, ref)
+    print(f"{label}: relL2={err:.3e} maxabs={np.abs(got - ref).max():.3e}", flush=True)
+    assert got.shape == ref.shape
+    assert err <= TOL[case.dtype], (label, err)
+    return got, ref
+
+
+def check_sampled(case, label, count=3000):
+    got = case.run_gpu()
+    idx = sample_indices(got.shape, count)
+    ref = case.oracle_points(idx)
+    err = rel_l2(got.ravel()[idx], ref)
+    print(f"{label}: sampled relL2={err:.3e} ({len(idx)} outputs)", flush=True)
+    assert err <= TOL[case.dtype], (label, err)
+    return got
+
+
+# ---------------------------------------------------------------------------
+# Small layers, full comparison
+# ---------------------------------------------------------------------------
+
+def test_small_config_fp32():
+    """16->32 on 8x28x28, 3x3x3 s1 p1, 9 of 27 positions per 4x4 group, fp32."""
+    layer, cfg = synth.single_layer_small()
+    mask = masked(cfg["tag"], 32, 16, (3, 3, 3), 9)
+    case = LayerCase(cfg["tag"], 1, 16, 32, (8, 28, 28), (3, 3, 3), (1, 1, 1), (1, 1, 1), "f32",
+                     mask, w_std=0.05, x_kind="uniform11")
+    check_full(case, "small16x32 f32")
+
+
+SHAPES = [
+    # tag, n, c_in, c_out, thw, k, stride, pad, keep
+    ("s1", 1, 16, 32, (4, 6, 9), (3, 3, 3), (1, 1, 1), (1, 1, 1), 9),
+    ("s2", 2, 24, 20, (5, 7, 6), (3, 3, 3), (2, 2, 2), (1, 1, 1), 12),
+    ("s3", 1, 10, 13, (3, 9, 11), (3, 3, 3), (1, 1, 1), (1, 1, 1), 7),     # partial groups
+    ("s4", 1, 32, 48, (4, 10, 10), (1, 3, 3), (1, 2, 2), (0, 1, 1), 4),
+    ("s5", 1, 40, 36, (6, 5, 5), (3, 1, 1), (2, 1, 1), (1, 0, 0), 2),
+    ("s6", 1, 3, 16, (2, 20, 20), (1, 7, 7), (1, 2, 2), (0, 3, 3), 20),
+    ("s7", 1, 64, 64, (2, 9, 9), (1, 1, 1), (2, 2, 2), (0, 0, 0), 1),
+    ("s8", 1, 45, 23, (3, 6, 7), (3, 3, 3), (1, 1, 1), (1, 1, 1), 27),     # c_in, c_out % 4 != 0
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("si", range(len(SHAPES)))
+def test_kgs_small_shapes(si, dtype):
+    tag, n, c_in, c_out, thw, k, stride, pad, keep = SHAPES[si]
+    mask = masked(tag, c_out, c_in, k, min(keep, k[0] * k[1] * k[2]))
+    case = LayerCase(tag, n, c_in, c_out, thw, k, stride, pad, dtype, mask)
+    check_full(case, f"kgs {tag} {dtype}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("si", range(len(SHAPES)))
+def test_dense_small_shapes(si, dtype):
+    tag, n, c_in, c_out, thw, k, stride, pad, _ = SHAPES[si]
+    case = LayerCase(tag + "d", n, c_in, c_out, thw, k, stride, pad, dtype, None)
+    check_full(case, f"dense {tag} {dtype}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_residual_epilogue(dtype):
+    mask = masked("res", 24, 16, (3, 1, 1), 2)
+    case = LayerCase("res", 2, 16, 24, (6, 7, 7), (3, 1, 1), (1, 1, 1), (1, 0, 0), dtype, mask,
+                     residual=True)
+    check_full(case, f"kgs residual {dtype}")
+    dcase = LayerCase("resd", 2, 16, 24, (6, 7, 7), (3, 1, 1), (1, 1, 1), (1, 0, 0), dtype, None,
+                      residual=True)
+    check_full(dcase, f"dense residual {dtype}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+def test_all_zero_mask_gives_relu_bias_exactly(dtype):
+    mask = np.zeros((8, 4, 27), dtype=np.uint8)
+    case = LayerCase("zero", 1, 16, 32, (4, 6, 6), (3, 3, 3), (1, 1, 1), (1, 1, 1), dtype, mask)
+    got = case.run_gpu()
+    b = np.maximum(case.b_oracle, 0.0)
+    expect = torch.from_numpy(b).to(layers.TORCH_DTYPES[dtype]).to(torch.float64).numpy()
+    assert np.array_equal(got, np.broadcast_to(expect[None, :, None, None, None], got.shape))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_all_one_mask_matches_dense_kernel(dtype):
+    mask = np.ones((8, 8, 27), dtype=np.uint8)
+    case = LayerCase("ones", 1, 32, 32, (4, 8, 8), (3, 3, 3), (1, 1, 1), (1, 1, 1), dtype, mask)
+    got, ref = check_full(case, f"all-ones {dtype}")
+    dense = layers.Conv3d(32, 32, (4, 8, 8), (3, 3, 3), (1, 1, 1), (1, 1, 1), case.w_t,
+                          case.b64.astype(np.float32), None, dtype)
+    yd = from_device_ndhwc(dense(to_device_ndhwc(case.x_t)))
+    assert rel_l2(got, yd) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_vanilla_pruned_group_ignores_its_channels(dtype):
+    """Section 3: a vanilla-pruned group (p, q) removes every link from
+    channel block q to filter block p: perturbing those channels leaves the
+    block's outputs bit-identical."""
+    c_in, c_out = 32, 32
+    rng = synth.rng_for("vanilla-test", "mask")
+    mask = synth.vanilla_mask(rng, 8, 8, 27, 3.0)
+    p, q = [(p, q) for p in range(8) for q in range(8) if mask[p, q, 0] == 0][0]
+    case = LayerCase("vanilla", 1, c_in, c_out, (4, 8, 8), (3, 3, 3), (1, 1, 1), (1, 1, 1), dtype,
+                     mask)
+    y1 = case.run_gpu()
+    x2 = case.x_t.clone()
+    x2[:, 4 * q:4 * q + 4] += 1.0
+    y2 = from_device_ndhwc(case.conv(to_device_ndhwc(x2)))
+    assert np.array_equal(y1[:, 4 * p:4 * p + 4], y2[:, 4 * p:4 * p + 4])
+    assert not np.array_equal(y1, y2)
+    check_full(case, f"vanilla {dtype}")
+
+
+def test_runs_are_deterministic():
+    mask = masked("det", 64, 64, (3, 3, 3), 9)
+    case = LayerCase("det", 1, 64, 64, (4, 14, 14), (3, 3, 3), (1, 1, 1), (1, 1, 1), "bf16", mask)
+    assert np.array_equal(case.run_gpu(), case.run_gpu())
+
+
+def test_empty_batch_is_a_no_op():
+    mask = masked("empty", 16, 16, (3, 3, 3), 9)
+    case = LayerCase("empty", 1, 16, 16, (4, 6, 6), (3, 3, 3), (1, 1, 1), (1, 1, 1), "bf16", mask)
+    x = torch.empty((0, 4, 6, 6, 16), dtype=torch.bfloat16, device="cuda")
+    y = case.conv(x)
+    torch.cuda.synchronize()
+    assert y.shape == (0, 4, 6, 6, 16)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("k,stride", [((1, 2, 2), (1, 2, 2)), ((2, 2, 2), (2, 2, 2)),
+                                      ((3, 3, 3), (2, 1, 2))])
+def test_maxpool_exact(dtype, k, stride):
+    x64 = synth.clip_input("pool", 2, "halfnormal", 24, 6, 9, 10) - 0.5
+    x_t, x_ref = rounded(x64, dtype)
+    y = layers.maxpool3d(to_device_ndhwc(x_t), k, stride, dtype)
+    ref = oracle.maxpool3d(x_ref, k, stride)
+    assert np.array_equal(from_device_ndhwc(y), ref)
+
+
+# ---------------------------------------------------------------------------
+# Full-size workload layers, sampled comparison
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_conv3b_config(dtype):
+    """256->256 on 8x28x28, 10 of 27 kept per group, Kaiming weights,
+    |N(0,1)| inputs."""
+    layer, cfg = synth.single_layer_conv3b()
+    mask = masked(cfg["tag"], 256, 256, (3, 3, 3), 10)
+    case = LayerCase(cfg["tag"], 1, 256, 256, (8, 28, 28), (3, 3, 3), (1, 1, 1), (1, 1, 1), dtype,
+                     mask)
+    check_sampled(case, f"conv3b {dtype}")
+    dense = LayerCase(cfg["tag"] + "d", 1, 256, 256, (8, 28, 28), (3, 3, 3), (1, 1, 1), (1, 1, 1),
+                      dtype, None)
+    check_sampled(dense, f"conv3b dense {dtype}")
+
+
+@pytest.mark.parametrize("li", range(8))
+def test_c3d_stack_layers(li):
+    """Each C3D layer at batch 1 with its own seeded input of the layer's
+    shape (U(0,1) clip for conv1, |N(0,1)| activations after), whole-stack
+    pruning rate 3x, bf16."""
+    stack = synth.c3d_stack(3.0)
+    l = stack[li]
+    mask = None if l.dense else synth.kgs_mask(synth.rng_for("c3d", l.name, "mask"), *l.groups,
+                                               l.ks, l.keep)
+    case = LayerCase("c3d-" + l.name, 1, l.c_in, l.c_out, (l.t, l.h, l.w), l.k, l.stride, l.pad,
+                     "bf16", mask, x_kind="uniform01" if li == 0 else "halfnormal")
+    check_sampled(case, f"c3d {l.name}")
+
+
+R21 = synth.r2plus1d_stack()
+
+
+@pytest.mark.parametrize("li", range(len(R21)))
+def test_r2plus1d_layers(li):
+    l = R21[li]
+    mask = None if l.dense else synth.kgs_mask(synth.rng_for("r21d", l.name, "mask"), *l.groups,
+                                               l.ks, l.keep)
+    case = LayerCase("r21d-" + l.name, 1, l.c_in, l.c_out, (l.t, l.h, l.w), l.k, l.stride, l.pad,
+                     "bf16", mask, relu=l.relu, residual=l.residual_from is not None,
+                     x_kind="uniform01" if li == 0 else "halfnormal")
+    check_sampled(case, f"r21d {l.name}", count=1500)
+
+
+@pytest.mark.parametrize("variant", ["kgs2", "kgs5", "vanilla3"])
+@pytest.mark.parametrize("li", [1, 3, 7])
+def test_c3d_batch32_layers(variant, li):
+    """Batch-32 layers of the throughput sweep (KGS at 2x and 5x, vanilla at
+    3x)."""
+    rate = {"kgs2": 2.0, "kgs5": 5.0, "vanilla3": 3.0}[variant]
+    stack = synth.c3d_stack(rate, tag="c3d-b32")
+    l = stack[li]
+    r = synth.rng_for("c3d-b32", variant, l.name, "mask")
+    if variant.startswith("vanilla"):
+        mask = synth.vanilla_mask(r, *l.groups, l.ks, rate)
+    else:
+        mask = synth.kgs_mask(r, *l.groups, l.ks, l.keep)
+    case = LayerCase(f"b32-{variant}-{l.name}", 32, l.c_in, l.c_out, (l.t, l.h, l.w), l.k,
+                     l.stride, l.pad, "bf16", mask)
+    check_sampled(case, f"b32 {variant} {l.name}", count=2000)
