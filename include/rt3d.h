@@ -143,8 +143,13 @@ rt3d_status rt3d_kgs_pack(const rt3d_conv3d_desc *desc, const void *w_dense,
 rt3d_status rt3d_kgs_unpack(const rt3d_conv3d_desc *desc, const rt3d_pack_info *info,
                             const void *blob, void *w_masked_dense);
 
-/* Device workspace a forward call of this layer needs (0 if none).  The
- * workspace is caller-owned device memory, at least 256-byte aligned. */
+/* Device workspace with which a forward call of this layer (at desc->n) runs
+ * at full parallelism (0 if it needs none).  Layers whose output alone cannot
+ * fill the GPU split their input channels across workgroups; the float32
+ * partial sums go to this caller-owned device buffer (16-byte aligned) and a
+ * second kernel adds them in a fixed order, so results stay bit-reproducible.
+ * A forward call given less workspace (or none) uses fewer splits; it never
+ * fails for lack of workspace. */
 rt3d_status rt3d_conv3d_workspace_size(const rt3d_conv3d_desc *desc,
                                        const rt3d_pack_info *info, uint64_t *bytes);
 

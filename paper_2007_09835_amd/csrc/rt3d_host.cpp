@@ -8,6 +8,7 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -119,8 +120,16 @@ constexpr int kMaxHalo = 96 * 1024;    // LDS bytes for the staged brick
 Tiling choose_tiling(const Geom &g) {
   Tiling best{};
   long best_cost = -1, best_halo = 0;
-  const int cc = g.es == 2 ? 32 : 16;
-  const int row = cc * g.es + 16;  // +16 bytes: rows land on different LDS banks
+  // Channels per LDS chunk: 32 (16-bit) or 16 (fp32), narrower when the
+  // layer has fewer input channels (a whole 16-byte piece at least).
+  const int epp = 16 / g.es;
+  int cc = epp;  // smallest power-of-two multiple of a piece covering c_in, capped
+  while (cc < g.c_in && cc < (g.es == 2 ? 32 : 16)) cc *= 2;
+  // LDS row pitch: an odd number of bank-width units (8 bytes for the 16-bit
+  // kernels, which read 8-byte item slices; 16 bytes for fp32) so that 16
+  // voxels whose halo indices differ modulo 16 fall on 16 distinct banks.
+  const int unit = g.es == 2 ? 8 : 16;
+  const int row = cc * g.es + unit;
   for (int bw = 1; bw <= std::min(g.wo, kSlots); ++bw)
     for (int bh = 1; bh <= std::min(g.ho, kSlots / bw); ++bh)
       for (int bt = 1; bt <= std::min(g.to, kSlots / (bw * bh)); ++bt) {
@@ -131,7 +140,22 @@ Tiling choose_tiling(const Geom &g) {
         if (halo > kMaxHalo) continue;
         const long nb = static_cast<long>((g.to + bt - 1) / bt) * ((g.ho + bh - 1) / bh) *
                         ((g.wo + bw - 1) / bw);
-        const long cost = nb * kSlots;
+        // LDS bank-conflict degree of a 16-voxel fragment: the largest number
+        // of its voxels whose halo row index coincides modulo 16 (modulo 8
+        // for the 16-byte fp32 reads).
+        const int modulus = g.es == 2 ? 16 : 8;
+        int conflict = 1;
+        for (int f = 0; f < kSlots / 16; ++f) {
+          int hits[16] = {0};
+          for (int n = 0; n < 16; ++n) {
+            const int sl = 16 * f + n;
+            const int tt = sl / (bh * bw), hh2 = (sl / bw) % bh, ww = sl % bw;
+            if (tt >= bt) continue;
+            const int v = ((tt * g.st) * hh + hh2 * g.sh) * hw + ww * g.sw;
+            conflict = std::max(conflict, ++hits[v % modulus]);
+          }
+        }
+        const long cost = nb * kSlots * (3 + conflict);
         if (best_cost < 0 || cost < best_cost || (cost == best_cost && halo < best_halo)) {
           best_cost = cost;
           best_halo = halo;
@@ -268,7 +292,25 @@ void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
   const int ips = f32 ? 4 : 8;           // items per K-step
   const int epl = f32 ? 4 : 8;           // operand elements per lane
   const bool dense = m4 == nullptr;
-  const int mfw = (dense && (g.c_out + 31) / 32 >= 4) ? 2 : 1;
+  // Dense layers share every B fragment across the wave's filter rows: use
+  // the widest wave tile that still leaves four wave tiles per workgroup.
+  // Dense wave-tile width (16*mfw filters sharing each B fragment): wider
+  // tiles cut LDS traffic but need c_out >= 64*mfw to keep four waves busy
+  // and enough voxels to keep the GPU filled without deep channel splits.
+  // Measured on MI355X over the C3D layers: 1 below 256 filters, 4 for wide
+  // layers with >= 2000 output voxels per launch, 2 otherwise.
+  int mfw = 1;
+  if (dense && g.c_out >= 256) {
+    const long voxels = static_cast<long>(std::max(g.n, 1)) * g.to * g.ho * g.wo;
+    mfw = voxels >= 2000 ? 4 : 2;
+  }
+  if (dense) {
+    // Benchmark A/B switch for the dense wave-tile width (1, 2 or 4).
+    if (const char *env = std::getenv("RT3D_DENSE_MFW")) {
+      const int v = std::atoi(env);
+      if (v == 1 || v == 2 || v == 4) mfw = v;
+    }
+  }
   const int wt_count = (g.c_out + 16 * mfw - 1) / (16 * mfw);
   L.variant = dense ? (f32 ? kVarDenseItemsF32 : kVarDenseItems16) : kVarKgsUnion16;
   L.plan.mfw = mfw;
@@ -531,9 +573,32 @@ rt3d_status check_info(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, bo
   return ok();
 }
 
+// Launch shape for a batch: waves per workgroup and channel-chunk splits so
+// that the grid covers the GPU several times over, limited by the workspace
+// the caller provides (ws_cap bytes; UINT64_MAX when sizing).
+Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint64_t ws_cap) {
+  const Geom g = geom_of(d);
+  const Tiling &tl = p.tiling;
+  const long bricks = static_cast<long>(g.n) * ((g.to + tl.bt - 1) / tl.bt) *
+                      ((g.ho + tl.bh - 1) / tl.bh) * ((g.wo + tl.bw - 1) / tl.bw);
+  constexpr long kTarget = 1024;  // workgroups: 4 per CU on 256 CUs
+  // Four waves per workgroup share one staged brick; parallelism beyond the
+  // bricks and filter tiles comes from channel splits.
+  Launch L{4, 1, 0};
+  const long wgs = bricks * ((p.wave_tiles + L.wpw - 1) / L.wpw);
+  int splits = 1;
+  if (wgs < kTarget) splits = static_cast<int>(std::min<long>(tl.nchunks, (kTarget + wgs - 1) / wgs));
+  const long total_vox = static_cast<long>(g.n) * g.to * g.ho * g.wo;
+  const uint64_t per_split = static_cast<uint64_t>(total_vox) * ((g.c_out + 3) / 4 * 4) * 4;
+  while (splits > 1 && per_split * splits > ws_cap) --splits;
+  L.splits = splits;
+  L.ws_bytes = splits > 1 ? per_split * splits : 0;
+  return L;
+}
+
 rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, const void *blob,
                      const void *x, const float *bias, const void *residual, void *y,
-                     void *stream, bool sparse) {
+                     void *workspace, uint64_t ws_bytes, void *stream, bool sparse) {
   rt3d_status st = check_desc(d, sparse);
   if (st != RT3D_OK) return st;
   st = check_info(d, info, sparse);
@@ -544,10 +609,11 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   if (want_res != (residual != nullptr))
     return fail(RT3D_ERR_INVALID_ARG, "residual must be given exactly when RT3D_RESIDUAL is set");
   if (!aligned16(blob) || !aligned16(x) || !aligned16(y) || (residual && !aligned16(residual)) ||
-      (bias && !aligned16(bias)))
+      (bias && !aligned16(bias)) || (workspace && !aligned16(workspace)))
     return fail(RT3D_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
   Plan p;
   std::memcpy(&p, info->plan, sizeof(p));
+  const Launch launch = plan_launch(d, p, workspace ? ws_bytes : 0);
   const Geom g = geom_of(d);
   const Tiling &tl = p.tiling;
   const uint8_t *b = static_cast<const uint8_t *>(blob);
@@ -571,6 +637,11 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   a.ht = tl.ht; a.hh = tl.hh; a.hw = tl.hw; a.cc = tl.cc; a.row = tl.row; a.nchunks = tl.nchunks;
   a.wave_tiles = p.wave_tiles;
   a.relu = (d->flags & RT3D_RELU) ? 1 : 0;
+  a.wpw = launch.wpw;
+  a.splits = launch.splits;
+  a.c_out4 = (g.c_out + 3) / 4 * 4;
+  a.total_vox = static_cast<long>(g.n) * g.to * g.ho * g.wo;
+  a.ws = static_cast<float *>(workspace);
   int e;
   switch (info->variant) {
     case kVarDenseItems16:
@@ -586,6 +657,7 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
     default:
       return fail(RT3D_ERR_BLOB_MISMATCH, "unknown kernel variant %u", info->variant);
   }
+  if (e == hipSuccess && a.splits > 1) e = launch_reduce_splits(a, d->dtype, stream);
   if (e != hipSuccess)
     return fail(RT3D_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(static_cast<hipError_t>(e)));
   return ok();
@@ -701,8 +773,11 @@ rt3d_status rt3d_conv3d_workspace_size(const rt3d_conv3d_desc *d, const rt3d_pac
   rt3d_status st = check_desc(d, false);
   if (st != RT3D_OK) return st;
   if (!info || !bytes) return fail(RT3D_ERR_INVALID_ARG, "info and bytes must be non-NULL");
-  if (info->magic != kMagic) return fail(RT3D_ERR_BLOB_MISMATCH, "info was not written by this library");
-  *bytes = 0;
+  if (info->magic != kMagic || info->version != kVersion || info->desc_hash != desc_hash(d))
+    return fail(RT3D_ERR_BLOB_MISMATCH, "info does not belong to this layer description");
+  Plan p;
+  std::memcpy(&p, info->plan, sizeof(p));
+  *bytes = plan_launch(d, p, UINT64_MAX).ws_bytes;
   return ok();
 }
 
@@ -710,9 +785,7 @@ rt3d_status rt3d_kgs_conv3d_fwd(const rt3d_conv3d_desc *d, const rt3d_pack_info 
                                 const void *blob_dev, const void *x, const float *bias,
                                 const void *residual, void *y, void *workspace,
                                 uint64_t workspace_bytes, void *stream) {
-  (void)workspace;
-  (void)workspace_bytes;
-  return run_conv(d, info, blob_dev, x, bias, residual, y, stream, true);
+  return run_conv(d, info, blob_dev, x, bias, residual, y, workspace, workspace_bytes, stream, true);
 }
 
 rt3d_status rt3d_dense_pack_size(const rt3d_conv3d_desc *d, uint64_t *bytes) {
@@ -755,9 +828,7 @@ rt3d_status rt3d_conv3d_dense_fwd(const rt3d_conv3d_desc *d, const rt3d_pack_inf
                                   const void *blob_dev, const void *x, const float *bias,
                                   const void *residual, void *y, void *workspace,
                                   uint64_t workspace_bytes, void *stream) {
-  (void)workspace;
-  (void)workspace_bytes;
-  return run_conv(d, info, blob_dev, x, bias, residual, y, stream, false);
+  return run_conv(d, info, blob_dev, x, bias, residual, y, workspace, workspace_bytes, stream, false);
 }
 
 rt3d_status rt3d_maxpool3d_fwd(int32_t n, int32_t c, int32_t t, int32_t h, int32_t w, int32_t kt,

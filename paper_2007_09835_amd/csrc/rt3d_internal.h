@@ -65,12 +65,26 @@ struct ConvArgs {
   int32_t bt, bh, bw, nbt, nbh, nbw;
   int32_t ht, hh, hw, cc, row, nchunks;
   int32_t wave_tiles, relu;
+  int32_t wpw;        // waves (wave tiles) per workgroup
+  int32_t splits;     // channel-chunk splits (grid.z); > 1 writes fp32 partials to ws
+  int32_t c_out4;     // c_out rounded up to 4 (partial row pitch)
+  int32_t pad0;
+  long total_vox;     // n * to * ho * wo
+  float *ws;          // [splits][total_vox][c_out4] partial sums (splits > 1)
+};
+
+// Launch shape chosen at forward time from the batch size.
+struct Launch {
+  int wpw;
+  int splits;
+  uint64_t ws_bytes;
 };
 
 // Kernel launchers (rt3d_kernels.hip).  Return hipSuccess or the launch error.
 int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream);
 int launch_items_f32(const ConvArgs &a, int mfw, void *stream);
 int launch_kgs_exact_f32(const ConvArgs &a, void *stream);
+int launch_reduce_splits(const ConvArgs &a, int dtype, void *stream);
 int launch_maxpool(int n, int c, int t, int h, int w, int kt, int kh, int kw, int st, int sh,
                    int sw, int to, int ho, int wo, int dtype, const void *x, void *y, void *stream);
 

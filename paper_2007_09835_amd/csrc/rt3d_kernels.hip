@@ -38,6 +38,11 @@ __device__ __forceinline__ void static_for(F &&f) {
   static_for_impl(std::make_integer_sequence<int, N>{}, f);
 }
 
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ uint32_t uniform(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(v)));
+}
+
 // ---------------------------------------------------------------------------
 // Brick geometry
 // ---------------------------------------------------------------------------
@@ -115,20 +120,109 @@ __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, cons
       if (vec) {
         v = *reinterpret_cast<const uint4 *>(src);
       } else {
-        union {
-          uint4 u;
-          uint8_t bytes[16];
-        } tmp;
-        tmp.u = make_uint4(0, 0, 0, 0);
+        // Channel count not a multiple of the piece: element-wise, zero tail.
         const int n_el = min(EPP, a.c_in - c);
-        for (int e = 0; e < n_el; ++e)
-          for (int k = 0; k < ES; ++k) tmp.bytes[e * ES + k] = src[e * ES + k];
-        v = tmp.u;
+        uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int e = 0; e < EPP; ++e) {
+          if (e < n_el) {
+            uint32_t bits;
+            if constexpr (ES == 4) bits = reinterpret_cast<const uint32_t *>(src)[e];
+            else bits = reinterpret_cast<const uint16_t *>(src)[e];
+            w[(e * ES) >> 2] |= bits << (((e * ES) & 3) * 8);
+          }
+        }
+        v = make_uint4(w[0], w[1], w[2], w[3]);
       }
     }
-    *reinterpret_cast<uint4 *>(lds + hv * a.row + piece * 16) = v;
+    uint2 *dst = reinterpret_cast<uint2 *>(lds + hv * a.row + piece * 16);
+    dst[0] = make_uint2(v.x, v.y);  // rows are 8-byte aligned (odd pitch in
+    dst[1] = make_uint2(v.z, v.w);  // 8-byte units keeps reads conflict-free)
   }
 }
+
+// Chunk stager with register prefetch.  Thread t owns the 16-byte halo
+// pieces t + k*blockDim (k < MAXI).  init() resolves their input voxels once
+// per workgroup; issue() starts the global loads of one channel chunk into
+// registers (all of them back to back, so one memory latency per chunk);
+// commit() writes them to LDS.  The kernels issue chunk c+1 before computing
+// chunk c, so the loads overlap the MFMA work.  `ok` is false when the halo
+// needs more than MAXI pieces per thread; the kernels then use stage_halo.
+template <int ES, int MAXI>
+struct Stager {
+  static constexpr int EPP = 16 / ES;
+  int vox[MAXI];   // flat input voxel; -1 padding (zeros); -2 no piece
+  uint4 d[MAXI];
+  int total, shift, ppr;
+  bool ok;
+
+  __device__ __forceinline__ void init(const ConvArgs &a, const Brick &b) {
+    ppr = a.cc / EPP;  // 1, 2 or 4
+    shift = ppr == 4 ? 2 : (ppr == 2 ? 1 : 0);
+    total = a.ht * a.hh * a.hw * ppr;
+    ok = total <= MAXI * static_cast<int>(blockDim.x);
+#pragma unroll
+    for (int k = 0; k < MAXI; ++k) {
+      const int idx = threadIdx.x + k * blockDim.x;
+      int v = -2;
+      if (idx < total) {
+        const int hv = idx >> shift;
+        const int xw = hv % a.hw;
+        const int rest = hv / a.hw;
+        const int xh = rest % a.hh;
+        const int xt = rest / a.hh;
+        const int zt = b.zt0 + xt, zh = b.zh0 + xh, zw = b.zw0 + xw;
+        v = (zt >= 0 && zt < a.t && zh >= 0 && zh < a.h && zw >= 0 && zw < a.w)
+                ? ((b.nb * a.t + zt) * a.h + zh) * a.w + zw
+                : -1;
+      }
+      vox[k] = v;
+    }
+  }
+
+  __device__ __forceinline__ void issue(const ConvArgs &a, int c0) {
+    const bool vec = (a.c_in % EPP) == 0;
+    const uint8_t *xb = static_cast<const uint8_t *>(a.x);
+#pragma unroll
+    for (int k = 0; k < MAXI; ++k) {
+      const int idx = threadIdx.x + k * blockDim.x;
+      const int c = c0 + (idx & (ppr - 1)) * EPP;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (vox[k] >= 0 && c < a.c_in) {
+        const uint8_t *src = xb + (static_cast<long>(vox[k]) * a.c_in + c) * ES;
+        if (vec) {
+          v = *reinterpret_cast<const uint4 *>(src);
+        } else {
+          const int n_el = min(EPP, a.c_in - c);
+          uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+          for (int e = 0; e < EPP; ++e) {
+            if (e < n_el) {
+              uint32_t bits;
+              if constexpr (ES == 4) bits = reinterpret_cast<const uint32_t *>(src)[e];
+              else bits = reinterpret_cast<const uint16_t *>(src)[e];
+              w[(e * ES) >> 2] |= bits << (((e * ES) & 3) * 8);
+            }
+          }
+          v = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+      }
+      d[k] = v;
+    }
+  }
+
+  __device__ __forceinline__ void commit(uint8_t *lds, const ConvArgs &a) const {
+#pragma unroll
+    for (int k = 0; k < MAXI; ++k) {
+      const int idx = threadIdx.x + k * blockDim.x;
+      if (vox[k] != -2) {
+        uint2 *dst = reinterpret_cast<uint2 *>(lds + (idx >> shift) * a.row + (idx & (ppr - 1)) * 16);
+        dst[0] = make_uint2(d[k].x, d[k].y);
+        dst[1] = make_uint2(d[k].z, d[k].w);
+      }
+    }
+  }
+};
 
 // ---------------------------------------------------------------------------
 // Epilogue: y = act(acc + bias (+ residual)), four consecutive filters of one
@@ -157,15 +251,18 @@ __device__ __forceinline__ void store4(const ConvArgs &a, long vox, int m0, floa
       } else {
         union { uint2 u; T e[4]; } rr;
         rr.u = *reinterpret_cast<const uint2 *>(res);
+        #pragma unroll
         for (int r = 0; r < 4; ++r) v[r] += to_f32(rr.e[r]);
       }
     }
     if (a.relu)
+      #pragma unroll
       for (int r = 0; r < 4; ++r) v[r] = v[r] > 0.f ? v[r] : 0.f;
     if constexpr (sizeof(T) == 4) {
       *reinterpret_cast<float4 *>(y) = make_float4(v[0], v[1], v[2], v[3]);
     } else {
       union { uint2 u; T e[4]; } out;
+      #pragma unroll
       for (int r = 0; r < 4; ++r) out.e[r] = static_cast<T>(v[r]);
       *reinterpret_cast<uint2 *>(y) = out.u;
     }
@@ -180,6 +277,24 @@ __device__ __forceinline__ void store4(const ConvArgs &a, long vox, int m0, floa
   }
 }
 
+// Final store (one split) or fp32 partial store into the split workspace.
+template <typename T>
+__device__ __forceinline__ void emit4(const ConvArgs &a, long vox, int m0, float v0, float v1,
+                                      float v2, float v3) {
+  if (a.splits == 1) {
+    store4<T>(a, vox, m0, v0, v1, v2, v3);
+  } else if (m0 < a.c_out) {
+    float *dst = a.ws + (static_cast<long>(blockIdx.z) * a.total_vox + vox) * a.c_out4 + m0;
+    *reinterpret_cast<float4 *>(dst) = make_float4(v0, v1, v2, v3);
+  }
+}
+
+// Channel chunks handled by this workgroup's split.
+__device__ __forceinline__ void split_range(const ConvArgs &a, int &ch0, int &ch1) {
+  ch0 = static_cast<int>((static_cast<long>(blockIdx.z) * a.nchunks) / a.splits);
+  ch1 = static_cast<int>((static_cast<long>(blockIdx.z + 1) * a.nchunks) / a.splits);
+}
+
 // ---------------------------------------------------------------------------
 // 16-bit item kernel: v_mfma_f32_16x16x32_{bf16,f16}.
 //
@@ -189,8 +304,10 @@ __device__ __forceinline__ void store4(const ConvArgs &a, long vox, int m0, floa
 // lane group g = lane/16 reads items 2g and 2g+1 (4 channels each, 8 bytes)
 // for its voxel n, and the A stream is stored in exactly that lane order.
 //
-// Four waves share one brick; wave w computes wave tile blockIdx.y*4 + w:
-// 16*MFW filters x 16*NF voxel slots.  Dense layers give every wave tile the
+// The waves of a workgroup share one brick; wave w computes wave tile
+// blockIdx.y*wpw + w: 16*MFW filters x 16*NF voxel slots.  blockIdx.z
+// selects a range of channel chunks (split-K) when the layer alone cannot
+// fill the GPU.  Dense layers give every wave tile the
 // full item list (and MFW > 1 shares each B fragment across filter rows);
 // KGS layers give each 16-filter tile the union of the items its four kernel
 // groups keep, with the pruned entries of that union stored as zero weights.
@@ -199,57 +316,120 @@ __device__ __forceinline__ void store4(const ConvArgs &a, long vox, int m0, floa
 template <typename T, int MFW, int NF>
 __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
   using V8 = std::conditional_t<std::is_same_v<T, __bf16>, bf16x8, f16x8>;
+  // Software pipeline of a wave (step t = one K-step of 8 items):
+  //   item offsets for step t+4 and the A operand for step t+2 are in flight
+  //   from global memory, and the B fragments of step t+1 are read from LDS,
+  //   while the MFMAs of step t run.  Rings: offsets 4, A 2, B 2.
   extern __shared__ __align__(16) uint8_t lds[];
-  const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
-  const int wt = blockIdx.y * 4 + wave;
+  const int wt = uniform(static_cast<int>(blockIdx.y) * a.wpw + (static_cast<int>(threadIdx.x) >> 6));
   const bool active = wt < a.wave_tiles;
   const Brick b = decode_brick(a);
 
   int vb[NF];
+  #pragma unroll
   for (int j = 0; j < NF; ++j) vb[j] = decode_slot(a, b, 16 * j + (lane & 15)).lds;
 
   f32x4 acc[MFW][NF];
+  #pragma unroll
   for (int i = 0; i < MFW; ++i)
+    #pragma unroll
     for (int j = 0; j < NF; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const uint32_t *sp = a.step_ptr + static_cast<long>(active ? wt : 0) * (a.nchunks + 1);
-  const uint32_t step0 = sp[0];
-  const uint32_t row0 = a.item_ptr[active ? wt : 0];
-  const V8 *A = static_cast<const V8 *>(a.a);
+  const uint32_t step0 = uniform(sp[0]);
+  const uint32_t row0 = uniform(a.item_ptr[active ? wt : 0]);
+  const V8 *A = static_cast<const V8 *>(a.a) + lane;
+  const uint2 *IT = reinterpret_cast<const uint2 *>(a.items) + g;  // 4 uint2 per step
 
-  for (int ch = 0; ch < a.nchunks; ++ch) {
-    __syncthreads();
-    stage_halo<2>(lds, a, b, ch * a.cc);
-    __syncthreads();
-    if (!active) continue;
-    const uint32_t s_end = sp[ch + 1];
-    for (uint32_t s = sp[ch]; s < s_end; ++s) {
-      const uint2 off = *reinterpret_cast<const uint2 *>(a.items + (static_cast<long>(row0) + (s - step0)) * 8 + 2 * g);
-      V8 av[MFW];
-      for (int i = 0; i < MFW; ++i) av[i] = A[(static_cast<long>(s) * MFW + i) * 64 + lane];
-      for (int j = 0; j < NF; ++j) {
-        const uint2 lo = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.x);
-        const uint2 hi = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.y);
-        const uint4 raw = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        const V8 bv = __builtin_bit_cast(V8, raw);
-        for (int i = 0; i < MFW; ++i) {
-          if constexpr (std::is_same_v<T, __bf16>)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bv, acc[i][j], 0, 0, 0);
-          else
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[i], bv, acc[i][j], 0, 0, 0);
-        }
-      }
+  uint2 roff[4];
+  V8 ra[2][MFW];
+  V8 rb[2][NF];
+  auto fetch_off = [&](int slot, uint32_t s) {
+    roff[slot] = IT[(static_cast<long>(row0) + (s - step0)) * 4];
+  };
+  auto fetch_a = [&](int slot, uint32_t s) {
+    #pragma unroll
+    for (int i = 0; i < MFW; ++i) ra[slot][i] = A[(static_cast<long>(s) * MFW + i) * 64];
+  };
+  auto load_b = [&](int slot, uint2 off) {
+    #pragma unroll
+    for (int j = 0; j < NF; ++j) {
+      const uint2 lo = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.x);
+      const uint2 hi = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.y);
+      rb[slot][j] = __builtin_bit_cast(V8, make_uint4(lo.x, lo.y, hi.x, hi.y));
     }
+  };
+  auto mma = [&](int slot) {
+    #pragma unroll
+    for (int j = 0; j < NF; ++j)
+      #pragma unroll
+      for (int i = 0; i < MFW; ++i) {
+        if constexpr (std::is_same_v<T, __bf16>)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ra[slot][i], rb[slot][j], acc[i][j], 0, 0, 0);
+        else
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ra[slot][i], rb[slot][j], acc[i][j], 0, 0, 0);
+      }
+  };
+
+  int ch0, ch1;
+  split_range(a, ch0, ch1);
+  Stager<2, 8> st;
+  st.init(a, b);
+  if (st.ok && ch0 < ch1) st.issue(a, ch0 * a.cc);
+  for (int ch = ch0; ch < ch1; ++ch) {
+    __syncthreads();  // every wave is done with the previous chunk
+    if (st.ok) st.commit(lds, a);
+    else stage_halo<2>(lds, a, b, ch * a.cc);
+    __syncthreads();
+    if (st.ok && ch + 1 < ch1) st.issue(a, (ch + 1) * a.cc);  // overlaps this chunk's MFMAs
+    if (!active) continue;
+    const uint32_t s_beg = uniform(sp[ch]), s_end = uniform(sp[ch + 1]);
+    if (s_beg == s_end) continue;
+    const uint32_t last = s_end - 1;
+    // Every fetch is unconditional (indices clamped to the last step: a
+    // harmless re-read) so the loop body is straight-line and the memory
+    // wait counters stay exact.
+    #pragma unroll
+    for (int d = 0; d < 4; ++d) fetch_off(d, min(s_beg + d, last));
+    #pragma unroll
+    for (int d = 0; d < 2; ++d) fetch_a(d, min(s_beg + d, last));
+    load_b(0, roff[0]);
+    uint32_t s = s_beg;
+    for (; s + 4 <= s_end; s += 4) {
+      static_for<4>([&](auto dc) {
+        constexpr int D = decltype(dc)::value;
+        load_b((D + 1) & 1, roff[(D + 1) & 3]);
+        mma(D & 1);
+        fetch_a(D & 1, min(s + D + 2, last));
+        fetch_off(D, min(s + D + 4, last));
+        // Keep the stages in place: without this fence the scheduler sinks
+        // the prefetches next to their uses two steps later.
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    }
+    // Tail: 0..3 steps.  Step s+D uses A slot D&1 (refilled two steps
+    // ahead as in the main loop), B slot D&1 and offset slot D.
+    const uint32_t rem = s_end - s;
+    static_for<3>([&](auto dc) {
+      constexpr int D = decltype(dc)::value;
+      if (D < rem) {
+        if (D + 1 < rem) load_b((D + 1) & 1, roff[(D + 1) & 3]);
+        mma(D & 1);
+        if (D + 2 < rem) fetch_a(D & 1, s + D + 2);
+      }
+    });
   }
   if (!active) return;
+  #pragma unroll
   for (int j = 0; j < NF; ++j) {
     const Slot sl = decode_slot(a, b, 16 * j + (lane & 15));
     if (!sl.valid) continue;
+    #pragma unroll
     for (int i = 0; i < MFW; ++i) {
       const int m0 = wt * 16 * MFW + 16 * i + 4 * g;
-      store4<T>(a, sl.out, m0, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      emit4<T>(a, sl.out, m0, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
     }
   }
 }
@@ -263,54 +443,93 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
 
 template <int MFW, int NF>
 __global__ __launch_bounds__(256) void items_f32_kernel(ConvArgs a) {
+  constexpr int DEPTH = 3;
   extern __shared__ __align__(16) uint8_t lds[];
-  const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
-  const int wt = blockIdx.y * 4 + wave;
+  const int wt = uniform(static_cast<int>(blockIdx.y) * a.wpw + (static_cast<int>(threadIdx.x) >> 6));
   const bool active = wt < a.wave_tiles;
   const Brick b = decode_brick(a);
 
   int vb[NF];
+  #pragma unroll
   for (int j = 0; j < NF; ++j) vb[j] = decode_slot(a, b, 16 * j + (lane & 15)).lds;
 
   f32x4 acc[MFW][NF];
+  #pragma unroll
   for (int i = 0; i < MFW; ++i)
+    #pragma unroll
     for (int j = 0; j < NF; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const uint32_t *sp = a.step_ptr + static_cast<long>(active ? wt : 0) * (a.nchunks + 1);
-  const uint32_t step0 = sp[0];
-  const uint32_t row0 = a.item_ptr[active ? wt : 0];
-  const float4 *A = static_cast<const float4 *>(a.a);
+  const uint32_t step0 = uniform(sp[0]);
+  const uint32_t row0 = uniform(a.item_ptr[active ? wt : 0]);
+  const float4 *A = static_cast<const float4 *>(a.a) + lane;
+  const uint32_t *IT = a.items + g;
 
-  for (int ch = 0; ch < a.nchunks; ++ch) {
-    __syncthreads();
-    stage_halo<4>(lds, a, b, ch * a.cc);
-    __syncthreads();
-    if (!active) continue;
-    const uint32_t s_end = sp[ch + 1];
-    for (uint32_t s = sp[ch]; s < s_end; ++s) {
-      const uint32_t off = a.items[(static_cast<long>(row0) + (s - step0)) * 4 + g];
-      float4 av[MFW];
-      for (int i = 0; i < MFW; ++i) av[i] = A[(static_cast<long>(s) * MFW + i) * 64 + lane];
-      for (int j = 0; j < NF; ++j) {
-        const float4 bv = *reinterpret_cast<const float4 *>(lds + vb[j] + off);
-        for (int i = 0; i < MFW; ++i) {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i].x, bv.x, acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i].y, bv.y, acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i].z, bv.z, acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i].w, bv.w, acc[i][j], 0, 0, 0);
-        }
+  float4 ra[DEPTH][MFW];
+  uint32_t roff[DEPTH];
+  auto fetch = [&](int slot, uint32_t s) {
+    roff[slot] = IT[(static_cast<long>(row0) + (s - step0)) * 4];
+    #pragma unroll
+    for (int i = 0; i < MFW; ++i) ra[slot][i] = A[(static_cast<long>(s) * MFW + i) * 64];
+  };
+  auto compute = [&](int slot) {
+    float4 bv[NF];
+    #pragma unroll
+    for (int j = 0; j < NF; ++j) bv[j] = *reinterpret_cast<const float4 *>(lds + vb[j] + roff[slot]);
+    #pragma unroll
+    for (int j = 0; j < NF; ++j)
+      #pragma unroll
+      for (int i = 0; i < MFW; ++i) {
+        const float4 av = ra[slot][i];
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv[j].x, acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv[j].y, acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv[j].z, acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv[j].w, acc[i][j], 0, 0, 0);
       }
+  };
+
+  int ch0, ch1;
+  split_range(a, ch0, ch1);
+  Stager<4, 8> st;
+  st.init(a, b);
+  if (st.ok && ch0 < ch1) st.issue(a, ch0 * a.cc);
+  for (int ch = ch0; ch < ch1; ++ch) {
+    __syncthreads();  // every wave is done with the previous chunk
+    if (st.ok) st.commit(lds, a);
+    else stage_halo<4>(lds, a, b, ch * a.cc);
+    __syncthreads();
+    if (st.ok && ch + 1 < ch1) st.issue(a, (ch + 1) * a.cc);  // overlaps this chunk's MFMAs
+    if (!active) continue;
+    const uint32_t s_beg = uniform(sp[ch]), s_end = uniform(sp[ch + 1]);
+    if (s_beg == s_end) continue;
+    for (int d = 0; d < DEPTH; ++d) fetch(d, min(s_beg + d, s_end - 1));
+    uint32_t s = s_beg;
+    const uint32_t s_last = s_end - 1;
+    for (; s + DEPTH <= s_end; s += DEPTH) {
+      // Straight-line body: the refill is unconditional (clamped to the last
+      // step, a harmless re-read) so the memory-wait counters stay exact.
+      static_for<DEPTH>([&](auto dc) {
+        constexpr int D = decltype(dc)::value;
+        compute(D);
+        fetch(D, min(s + D + DEPTH, s_last));
+      });
     }
+    static_for<DEPTH - 1>([&](auto dc) {
+      constexpr int D = decltype(dc)::value;
+      if (s + D < s_end) compute(D);
+    });
   }
   if (!active) return;
+  #pragma unroll
   for (int j = 0; j < NF; ++j) {
     const Slot sl = decode_slot(a, b, 16 * j + (lane & 15));
     if (!sl.valid) continue;
+    #pragma unroll
     for (int i = 0; i < MFW; ++i) {
       const int m0 = wt * 16 * MFW + 16 * i + 4 * g;
-      store4<float>(a, sl.out, m0, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      emit4<float>(a, sl.out, m0, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
     }
   }
 }
@@ -337,37 +556,48 @@ __device__ __forceinline__ f32x4 mfma441(float av, float bv, f32x4 c) {
 template <int SUB>
 __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
   extern __shared__ __align__(16) uint8_t lds[];
-  const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  const int wt = blockIdx.y * 4 + wave;
+  const int wt = uniform(static_cast<int>(blockIdx.y) * a.wpw + (static_cast<int>(threadIdx.x) >> 6));
   const bool active = wt < a.wave_tiles;
   const Brick b = decode_brick(a);
 
   int vb[SUB];
+  #pragma unroll
   for (int s = 0; s < SUB; ++s) vb[s] = decode_slot(a, b, 64 * s + lane).lds;
 
   f32x4 acc[4][SUB];
+  #pragma unroll
   for (int gi = 0; gi < 4; ++gi)
+    #pragma unroll
     for (int s = 0; s < SUB; ++s) acc[gi][s] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const uint32_t *sp = a.step_ptr + static_cast<long>(active ? wt : 0) * (a.nchunks + 1);
   const float *A = static_cast<const float *>(a.a);
 
-  for (int ch = 0; ch < a.nchunks; ++ch) {
+  int ch0, ch1;
+  split_range(a, ch0, ch1);
+  Stager<4, 8> st;
+  st.init(a, b);
+  if (st.ok && ch0 < ch1) st.issue(a, ch0 * a.cc);
+  for (int ch = ch0; ch < ch1; ++ch) {
+    __syncthreads();  // every wave is done with the previous chunk
+    if (st.ok) st.commit(lds, a);
+    else stage_halo<4>(lds, a, b, ch * a.cc);
     __syncthreads();
-    stage_halo<4>(lds, a, b, ch * a.cc);
-    __syncthreads();
+    if (st.ok && ch + 1 < ch1) st.issue(a, (ch + 1) * a.cc);  // overlaps this chunk's MFMAs
     if (!active) continue;
-    const uint32_t it_end = sp[ch + 1];
-    for (uint32_t it = sp[ch]; it < it_end; ++it) {
-      const uint32_t off = a.items[it];
-      const uint32_t keep = a.keep[it];
+    const uint32_t it_end = uniform(sp[ch + 1]);
+    for (uint32_t it = uniform(sp[ch]); it < it_end; ++it) {
+      const uint32_t off = uniform(a.items[it]);
+      const uint32_t keep = uniform(a.keep[it]);
       const float av = A[static_cast<long>(it) * 64 + lane];
       float4 bv[SUB];
+      #pragma unroll
       for (int s = 0; s < SUB; ++s) bv[s] = *reinterpret_cast<const float4 *>(lds + vb[s] + off);
       static_for<4>([&](auto gc) {
         constexpr int G = decltype(gc)::value;
         if (keep & (1u << G)) {
+          #pragma unroll
           for (int s = 0; s < SUB; ++s) {
             acc[G][s] = mfma441<4 * G + 0>(av, bv[s].x, acc[G][s]);
             acc[G][s] = mfma441<4 * G + 1>(av, bv[s].y, acc[G][s]);
@@ -379,13 +609,37 @@ __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
     }
   }
   if (!active) return;
+  #pragma unroll
   for (int s = 0; s < SUB; ++s) {
     const Slot sl = decode_slot(a, b, 64 * s + lane);
     if (!sl.valid) continue;
+    #pragma unroll
     for (int gi = 0; gi < 4; ++gi) {
       const int m0 = wt * 16 + 4 * gi;
-      store4<float>(a, sl.out, m0, acc[gi][s][0], acc[gi][s][1], acc[gi][s][2], acc[gi][s][3]);
+      emit4<float>(a, sl.out, m0, acc[gi][s][0], acc[gi][s][1], acc[gi][s][2], acc[gi][s][3]);
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Split reduction: y = act(sum over splits, in split order, + bias
+// (+ residual)).  Fixed summation order keeps results run-to-run identical.
+// ---------------------------------------------------------------------------
+
+template <typename T>
+__global__ __launch_bounds__(256) void reduce_splits_kernel(ConvArgs a) {
+  const int groups = a.c_out4 >> 2;
+  const long total = a.total_vox * groups;
+  for (long idx = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
+       idx += static_cast<long>(gridDim.x) * blockDim.x) {
+    const long vox = idx / groups;
+    const int m0 = static_cast<int>(idx - vox * groups) * 4;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int z = 0; z < a.splits; ++z) {
+      const float4 v = *reinterpret_cast<const float4 *>(a.ws + (static_cast<long>(z) * a.total_vox + vox) * a.c_out4 + m0);
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+    store4<T>(a, vox, m0, acc.x, acc.y, acc.z, acc.w);
   }
 }
 
@@ -441,10 +695,11 @@ int launch_conv(K kernel, const ConvArgs &a, void *stream) {
     attr_done = true;
   }
   const long blocks_x = static_cast<long>(a.n) * a.nbt * a.nbh * a.nbw;
-  const int blocks_y = (a.wave_tiles + 3) / 4;
+  const int blocks_y = (a.wave_tiles + a.wpw - 1) / a.wpw;
   if (blocks_x == 0 || blocks_y == 0) return hipSuccess;
-  dim3 grid(static_cast<unsigned>(blocks_x), static_cast<unsigned>(blocks_y));
-  hipLaunchKernelGGL(kernel, grid, dim3(256), lds, static_cast<hipStream_t>(stream), a);
+  dim3 grid(static_cast<unsigned>(blocks_x), static_cast<unsigned>(blocks_y),
+            static_cast<unsigned>(a.splits));
+  hipLaunchKernelGGL(kernel, grid, dim3(64 * a.wpw), lds, static_cast<hipStream_t>(stream), a);
   return hipGetLastError();
 }
 
@@ -454,9 +709,11 @@ int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream) {
   if (dtype == RT3D_BF16) {
     if (mfw == 1) return launch_conv(items16_kernel<__bf16, 1, 8>, a, stream);
     if (mfw == 2) return launch_conv(items16_kernel<__bf16, 2, 8>, a, stream);
+    if (mfw == 4) return launch_conv(items16_kernel<__bf16, 4, 8>, a, stream);
   } else if (dtype == RT3D_F16) {
     if (mfw == 1) return launch_conv(items16_kernel<_Float16, 1, 8>, a, stream);
     if (mfw == 2) return launch_conv(items16_kernel<_Float16, 2, 8>, a, stream);
+    if (mfw == 4) return launch_conv(items16_kernel<_Float16, 4, 8>, a, stream);
   }
   return hipErrorInvalidValue;
 }
@@ -464,7 +721,23 @@ int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream) {
 int launch_items_f32(const ConvArgs &a, int mfw, void *stream) {
   if (mfw == 1) return launch_conv(items_f32_kernel<1, 8>, a, stream);
   if (mfw == 2) return launch_conv(items_f32_kernel<2, 8>, a, stream);
+  if (mfw == 4) return launch_conv(items_f32_kernel<4, 8>, a, stream);
   return hipErrorInvalidValue;
+}
+
+int launch_reduce_splits(const ConvArgs &a, int dtype, void *stream) {
+  const long total = a.total_vox * (a.c_out4 / 4);
+  if (total == 0) return hipSuccess;
+  long blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == RT3D_F32)
+    hipLaunchKernelGGL(reduce_splits_kernel<float>, dim3(blocks), dim3(256), 0, s, a);
+  else if (dtype == RT3D_BF16)
+    hipLaunchKernelGGL(reduce_splits_kernel<__bf16>, dim3(blocks), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(reduce_splits_kernel<_Float16>, dim3(blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
 }
 
 int launch_kgs_exact_f32(const ConvArgs &a, void *stream) {

@@ -27,11 +27,14 @@ class Conv3d:
 
     def __init__(self, c_in: int, c_out: int, thw: Sequence[int], k, stride, pad, w,
                  bias=None, mask: Optional[np.ndarray] = None, dtype: str = "bf16",
-                 relu: bool = True, residual: bool = False, g=(4, 4), device="cuda"):
+                 relu: bool = True, residual: bool = False, g=(4, 4), device="cuda",
+                 batch: int = 1):
+        """``batch`` is the batch size the layer is planned for (the blob
+        works for any batch; the tile shapes are chosen for this one)."""
         self.dtype = dtype
         self.sparse = mask is not None
-        self.desc = rt3d.make_desc(1, c_in, c_out, tuple(thw), tuple(k), tuple(stride), tuple(pad),
-                                   tuple(g), dtype, relu=relu, residual=residual)
+        self.desc = rt3d.make_desc(batch, c_in, c_out, tuple(thw), tuple(k), tuple(stride),
+                                   tuple(pad), tuple(g), dtype, relu=relu, residual=residual)
         if self.sparse:
             blob, self.info = rt3d.rt3d_kgs_pack(self.desc, w, mask)
         else:
@@ -42,6 +45,7 @@ class Conv3d:
         self.out_thw = rt3d.rt3d_conv3d_out_shape(self.desc)
         self.c_out = c_out
         self.device = device
+        self._ws = {}
 
     def desc_for(self, n: int) -> rt3d.Conv3dDesc:
         d = rt3d.Conv3dDesc.from_buffer_copy(self.desc)
@@ -51,13 +55,23 @@ class Conv3d:
     def out_shape(self, n: int):
         return (n, *self.out_thw, self.c_out)
 
+    def workspace(self, n: int) -> Optional[torch.Tensor]:
+        """Split-K workspace for batch n (allocated once per batch size)."""
+        if n not in self._ws:
+            nbytes = rt3d.rt3d_conv3d_workspace_size(self.desc_for(n), self.info)
+            self._ws[n] = (None if nbytes == 0 else
+                           torch.empty(nbytes // 4, dtype=torch.float32, device=self.device))
+        return self._ws[n]
+
     def __call__(self, x: torch.Tensor, residual: Optional[torch.Tensor] = None,
-                 out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+                 out: Optional[torch.Tensor] = None, stream=None,
+                 use_workspace: bool = True) -> torch.Tensor:
         n = x.shape[0]
         if out is None:
             out = torch.empty(self.out_shape(n), dtype=TORCH_DTYPES[self.dtype], device=x.device)
+        ws = self.workspace(n) if use_workspace and n > 0 else None
         fwd = rt3d.rt3d_kgs_conv3d_fwd if self.sparse else rt3d.rt3d_conv3d_dense_fwd
-        fwd(self.desc_for(n), self.info, self.blob, x, self.bias, residual, out, None, stream)
+        fwd(self.desc_for(n), self.info, self.blob, x, self.bias, residual, out, ws, stream)
         return out
 
 

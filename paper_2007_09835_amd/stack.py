@@ -47,7 +47,7 @@ class Stack:
             self.convs.append(layers.Conv3d(l.c_in, l.c_out, (l.t, l.h, l.w), l.k, l.stride, l.pad,
                                             w, d.bias.astype(np.float32), mask, dtype,
                                             relu=l.relu, residual=l.residual_from is not None,
-                                            device=device))
+                                            device=device, batch=batch))
         # activation buffers (channels-last), allocated once
         self.x = torch.zeros((batch, self.layers[0].t, self.layers[0].h, self.layers[0].w,
                               self.layers[0].c_in), dtype=tdt, device=device)

@@ -143,6 +143,25 @@ def test_vanilla_pruned_group_ignores_its_channels(dtype):
     check_full(case, f"vanilla {dtype}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("sparse", [True, False])
+def test_split_k_matches_unsplit(dtype, sparse):
+    """A small-voxel layer splits its channels across workgroups (fp32
+    partials + ordered reduction); with no workspace it runs unsplit.  Both
+    match the oracle, and the split result is reproducible bit for bit."""
+    mask = masked("split", 128, 256, (3, 3, 3), 9) if sparse else None
+    case = LayerCase("split", 1, 256, 128, (2, 7, 7), (3, 3, 3), (1, 1, 1), (1, 1, 1), dtype, mask,
+                     residual=True)
+    assert case.conv.workspace(1) is not None
+    got, ref = check_full(case, f"split {'kgs' if sparse else 'dense'} {dtype}")
+    x = to_device_ndhwc(case.x_t)
+    r = to_device_ndhwc(case.res_t)
+    again = from_device_ndhwc(case.conv(x, r))
+    assert np.array_equal(got, again)
+    unsplit = from_device_ndhwc(case.conv(x, r, use_workspace=False))
+    assert rel_l2(unsplit, ref) <= TOL[dtype]
+
+
 def test_runs_are_deterministic():
     mask = masked("det", 64, 64, (3, 3, 3), 9)
     case = LayerCase("det", 1, 64, 64, (4, 14, 14), (3, 3, 3), (1, 1, 1), (1, 1, 1), "bf16", mask)
