@@ -41,6 +41,11 @@ def parse():
                    help="fraction of every layer's outputs the oracle computes (1 = full clip)")
     p.add_argument("--layer-reps", type=int, default=20)
     p.add_argument("--report", default=None, help="write per-layer results to this JSON file")
+    p.add_argument("--profile-layer", default=None,
+                   help="only launch this layer's sparse conv --layer-reps times (for rocprofv3)")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="with --profile-layer: also run a plain device copy of MIB MiB, the "
+                        "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE")
     return p.parse_args()
 
 
@@ -75,6 +80,62 @@ def per_layer_ms(torch, stack, reps, stream):
         cur = stack.pool_bufs.get(l.name, stack.bufs[l.name])
         inputs[l.name] = cur
     return out
+
+
+def library_source_hash():
+    """Hash of the HIP library sources (ties a stored traffic measurement to
+    the kernels it was taken on)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("rt3d_kernels.hip", "rt3d_host.cpp", "rt3d_internal.h"):
+        with open(os.path.join(ROOT, "paper_2007_09835_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(layer):
+    """HBM bytes per launch of `layer`'s KGS conv from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summaries, or None when no summary
+    exists for it or the kernels changed since it was taken."""
+    import glob
+    for path in glob.glob(os.path.join(ROOT, "profiles", "*.md")):
+        with open(path) as fh:
+            for line in fh:
+                if line.startswith("traffic-json:"):
+                    d = json.loads(line.split(":", 1)[1])
+                    if d.get("layer") == layer and d.get("source_hash") == library_source_hash():
+                        return d["traffic_bytes_per_launch"]
+    return None
+
+
+def profile_layer(args, torch, stream):
+    """Launch one layer of the sparse stack back to back (and optionally a
+    plain copy of known size) so rocprofv3 sees only these kernels."""
+    from paper_2007_09835_amd.stack import Stack
+    sparse = Stack(args.net, args.batch, args.dtype, args.mode, args.rate)
+    idx = [l.name for l in sparse.layers].index(args.profile_layer)
+    l, conv = sparse.layers[idx], sparse.convs[idx]
+    inp = torch.randn(conv.desc_for(args.batch).n, l.t, l.h, l.w, l.c_in, device="cuda").abs()
+    inp = inp.to(sparse.x.dtype)
+    res = torch.zeros_like(sparse.bufs[l.name]) if l.residual_from else None
+    fn = lambda: conv(inp, res, out=sparse.bufs[l.name])
+    fn()
+    ms = time_region(torch, fn, args.layer_reps, stream)
+    info = conv.info
+    kept = (args.batch * l.voxels_out * info.kept_weights if conv.sparse
+            else l.dense_macs(args.batch))
+    out = {"layer": l.name, "launches": args.layer_reps, "ms_per_launch": ms,
+           "algorithmic_tflops": 2.0 * kept / (ms * 1e-3) / 1e12,
+           "workspace_bytes": 0 if conv.workspace(args.batch) is None
+           else conv.workspace(args.batch).numel() * 4}
+    if args.copy_calibration:
+        n = args.copy_calibration * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        out["copy_bytes_each_way"] = n * 4
+    print(json.dumps(out), flush=True)
 
 
 def cpu_baseline(stack, fraction):
@@ -142,6 +203,10 @@ def main():
     build.build(force=False)
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
+
+    if args.profile_layer:
+        profile_layer(args, torch, stream)
+        return
 
     log("building stacks ...")
     sparse = Stack(args.net, args.batch, args.dtype, args.mode, args.rate)
@@ -220,8 +285,10 @@ def main():
                         if drow["kgs"] else l.dense_macs(args.batch))
     achieved = kept_flops / (drow["ms_sparse"] * 1e-3) / 1e12
     peak = PEAK_TFLOPS[args.dtype]
+    traffic = measured_traffic(l.name) if (drow["kgs"] and args.batch == 1 and args.net == "c3d"
+                                           and args.dtype == "bf16" and args.mode == "kgs") else None
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": None,
+                "frac": round(achieved / peak, 4), "traffic": traffic,
                 "kernel": "%s conv (%s)" % (l.name, "KGS" if drow["kgs"] else "dense"),
                 "flops_per_launch": kept_flops}
 

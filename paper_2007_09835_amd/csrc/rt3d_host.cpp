@@ -581,9 +581,12 @@ Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint64_t ws_cap) {
   const Tiling &tl = p.tiling;
   const long bricks = static_cast<long>(g.n) * ((g.to + tl.bt - 1) / tl.bt) *
                       ((g.ho + tl.bh - 1) / tl.bh) * ((g.wo + tl.bw - 1) / tl.bw);
-  constexpr long kTarget = 1024;  // workgroups: 4 per CU on 256 CUs
   // Four waves per workgroup share one staged brick; parallelism beyond the
-  // bricks and filter tiles comes from channel splits.
+  // bricks and filter tiles comes from channel splits, used until the grid
+  // has about two workgroups per CU (split partials cost memory traffic).
+  long target = 256;
+  if (const char *env = std::getenv("RT3D_SPLIT_TARGET")) target = std::max(1, std::atoi(env));
+  const long kTarget = target;
   Launch L{4, 1, 0};
   const long wgs = bricks * ((p.wave_tiles + L.wpw - 1) / L.wpw);
   int splits = 1;
