@@ -72,6 +72,11 @@ typedef struct {
     int32_t g_m, g_n;         /* kernel-group size (KGS calls; ignored when dense) */
     int32_t dtype;            /* rt3d_dtype of x, W, y, residual */
     uint32_t flags;           /* RT3D_RELU | RT3D_RESIDUAL */
+    int32_t qt, qh, qw;       /* fused max-pool window (= stride) applied after the
+                                 activation, 0 or 1 = none; C3D pools 1x2x2 after conv1
+                                 and 2x2x2 after conv2/3b/4b.  y then has the pooled
+                                 extent floor(to/qt) x floor(ho/qh) x floor(wo/qw);
+                                 the residual keeps the unpooled extent. */
 } rt3d_conv3d_desc;
 
 /* Filled by the pack calls; plain data owned by the caller.  It describes
@@ -111,7 +116,7 @@ const char *rt3d_status_string(rt3d_status status);
  * none).  Valid until the next library call on this thread. */
 const char *rt3d_last_error_detail(void);
 
-/* Output extent of a layer.  Host only. */
+/* Output extent of a layer (after the fused pooling, if any).  Host only. */
 rt3d_status rt3d_conv3d_out_shape(const rt3d_conv3d_desc *desc,
                                   int32_t *to, int32_t *ho, int32_t *wo);
 

@@ -69,6 +69,16 @@ rt3d_status check_desc(const rt3d_conv3d_desc *d, bool need_groups) {
     return fail(RT3D_ERR_UNSUPPORTED, "strides above 2 are not supported");
   if (d->pt >= d->kt || d->ph >= d->kh || d->pw >= d->kw)
     return fail(RT3D_ERR_UNSUPPORTED, "padding must be smaller than the kernel extent");
+  if (d->qt < 0 || d->qh < 0 || d->qw < 0)
+    return fail(RT3D_ERR_INVALID_ARG, "pooling windows must be >= 0");
+  if (d->qt > 8 || d->qh > 8 || d->qw > 8)
+    return fail(RT3D_ERR_UNSUPPORTED, "pooling windows above 8 are not supported");
+  {
+    const int qt = std::max(1, d->qt), qh = std::max(1, d->qh), qw = std::max(1, d->qw);
+    if (out_len(d->t, d->kt, d->st, d->pt) / qt <= 0 || out_len(d->h, d->kh, d->sh, d->ph) / qh <= 0 ||
+        out_len(d->w, d->kw, d->sw, d->pw) / qw <= 0)
+      return fail(RT3D_ERR_INVALID_ARG, "the pooling window does not fit the conv output");
+  }
   if (need_groups) {
     auto okg = [](int g) { return g == 4 || g == 8 || g == 16; };
     if (!okg(d->g_m) || !okg(d->g_n))
@@ -81,8 +91,10 @@ rt3d_status check_desc(const rt3d_conv3d_desc *d, bool need_groups) {
 }
 
 uint64_t desc_hash(const rt3d_conv3d_desc *d) {
-  const int32_t f[] = {d->c_in, d->c_out, d->t,  d->h,  d->w,  d->kt, d->kh, d->kw, d->st,
-                       d->sh,   d->sw,    d->pt, d->ph, d->pw, d->g_m, d->g_n, d->dtype};
+  const int32_t f[] = {d->c_in, d->c_out, d->t,  d->h,  d->w,   d->kt,    d->kh,
+                       d->kw,   d->st,    d->sh, d->sw, d->pt,  d->ph,    d->pw,
+                       d->g_m,  d->g_n,   d->dtype, std::max(1, d->qt), std::max(1, d->qh),
+                       std::max(1, d->qw)};
   uint64_t h = 1469598103934665603ull;
   for (int32_t v : f) {
     for (int b = 0; b < 4; ++b) {
@@ -99,16 +111,24 @@ uint64_t desc_hash(const rt3d_conv3d_desc *d) {
 
 struct Geom {
   int n, c_in, c_out, t, h, w, kt, kh, kw, st, sh, sw, pt, ph, pw, to, ho, wo, ks, es;
+  int qt, qh, qw, pto, pho, pwo;  // fused pooling window and pooled extent
 };
 
 Geom geom_of(const rt3d_conv3d_desc *d) {
   Geom g{d->n,  d->c_in, d->c_out, d->t,  d->h,  d->w,  d->kt, d->kh, d->kw, d->st,
-         d->sh, d->sw,   d->pt,    d->ph, d->pw, 0,     0,     0,     0,     0};
+         d->sh, d->sw,   d->pt,    d->ph, d->pw, 0,     0,     0,     0,     0,
+         1,     1,       1,        0,     0,     0};
   g.to = out_len(d->t, d->kt, d->st, d->pt);
   g.ho = out_len(d->h, d->kh, d->sh, d->ph);
   g.wo = out_len(d->w, d->kw, d->sw, d->pw);
   g.ks = d->kt * d->kh * d->kw;
   g.es = esize_of(d->dtype);
+  g.qt = std::max(1, d->qt);
+  g.qh = std::max(1, d->qh);
+  g.qw = std::max(1, d->qw);
+  g.pto = g.to / g.qt;
+  g.pho = g.ho / g.qh;
+  g.pwo = g.wo / g.qw;
   return g;
 }
 
@@ -130,9 +150,12 @@ Tiling choose_tiling(const Geom &g) {
   // voxels whose halo indices differ modulo 16 fall on 16 distinct banks.
   const int unit = g.es == 2 ? 8 : 16;
   const int row = cc * g.es + unit;
-  for (int bw = 1; bw <= std::min(g.wo, kSlots); ++bw)
-    for (int bh = 1; bh <= std::min(g.ho, kSlots / bw); ++bh)
-      for (int bt = 1; bt <= std::min(g.to, kSlots / (bw * bh)); ++bt) {
+  // Bricks hold whole pooling windows (their origins are then multiples of
+  // the window too), so the fused pooling never crosses workgroups.
+  for (int bw = g.qw; bw <= std::max(g.qw, std::min(g.wo, kSlots)); bw += g.qw)
+    for (int bh = g.qh; bh <= std::max(g.qh, std::min(g.ho, kSlots / bw)); bh += g.qh)
+      for (int bt = g.qt; bt <= std::max(g.qt, std::min(g.to, kSlots / (bw * bh))); bt += g.qt) {
+        if (bt * bh * bw > kSlots) continue;
         const int ht = (bt - 1) * g.st + g.kt;
         const int hh = (bh - 1) * g.sh + g.kh;
         const int hw = (bw - 1) * g.sw + g.kw;
@@ -645,6 +668,10 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   a.c_out4 = (g.c_out + 3) / 4 * 4;
   a.total_vox = static_cast<long>(g.n) * g.to * g.ho * g.wo;
   a.ws = static_cast<float *>(workspace);
+  a.qt = g.qt; a.qh = g.qh; a.qw = g.qw;
+  a.pto = g.pto; a.pho = g.pho; a.pwo = g.pwo;
+  a.c_wg = a.wpw * 16 * p.mfw;
+  a.tile_row = a.c_wg * 4 + 16;  // +16 bytes: slot rows start on different banks
   int e;
   switch (info->variant) {
     case kVarDenseItems16:
@@ -693,9 +720,9 @@ rt3d_status rt3d_conv3d_out_shape(const rt3d_conv3d_desc *d, int32_t *to, int32_
   if (st != RT3D_OK) return st;
   if (!to || !ho || !wo) return fail(RT3D_ERR_INVALID_ARG, "output pointers must be non-NULL");
   const Geom g = geom_of(d);
-  *to = g.to;
-  *ho = g.ho;
-  *wo = g.wo;
+  *to = g.pto;
+  *ho = g.pho;
+  *wo = g.pwo;
   return ok();
 }
 

@@ -71,6 +71,10 @@ struct ConvArgs {
   int32_t pad0;
   long total_vox;     // n * to * ho * wo
   float *ws;          // [splits][total_vox][c_out4] partial sums (splits > 1)
+  int32_t qt, qh, qw; // fused pooling window (1 = none)
+  int32_t pto, pho, pwo;  // pooled output extent
+  int32_t c_wg;       // filters per workgroup (wpw * 16 * mfw)
+  int32_t tile_row;   // LDS bytes per voxel slot of the epilogue tile
 };
 
 // Launch shape chosen at forward time from the batch size.

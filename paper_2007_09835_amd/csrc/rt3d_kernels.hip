@@ -232,67 +232,141 @@ struct Stager {
 template <typename T>
 __device__ __forceinline__ float to_f32(T v) { return static_cast<float>(v); }
 
-template <typename T>
-__device__ __forceinline__ void store4(const ConvArgs &a, long vox, int m0, float v0, float v1,
-                                       float v2, float v3) {
-  if (m0 >= a.c_out) return;
-  float v[4] = {v0, v1, v2, v3};
-  T *y = static_cast<T *>(a.y) + vox * a.c_out + m0;
-  const T *res = a.res ? static_cast<const T *>(a.res) + vox * a.c_out + m0 : nullptr;
-  if ((a.c_out & 3) == 0) {
-    if (a.bias) {
-      const float4 bb = *reinterpret_cast<const float4 *>(a.bias + m0);
-      v[0] += bb.x; v[1] += bb.y; v[2] += bb.z; v[3] += bb.w;
-    }
-    if (res) {
-      if constexpr (sizeof(T) == 4) {
-        const float4 rr = *reinterpret_cast<const float4 *>(res);
-        v[0] += rr.x; v[1] += rr.y; v[2] += rr.z; v[3] += rr.w;
-      } else {
-        union { uint2 u; T e[4]; } rr;
-        rr.u = *reinterpret_cast<const uint2 *>(res);
-        #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] += to_f32(rr.e[r]);
-      }
-    }
-    if (a.relu)
-      #pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = v[r] > 0.f ? v[r] : 0.f;
-    if constexpr (sizeof(T) == 4) {
-      *reinterpret_cast<float4 *>(y) = make_float4(v[0], v[1], v[2], v[3]);
-    } else {
-      union { uint2 u; T e[4]; } out;
-      #pragma unroll
-      for (int r = 0; r < 4; ++r) out.e[r] = static_cast<T>(v[r]);
-      *reinterpret_cast<uint2 *>(y) = out.u;
-    }
-  } else {
-    for (int r = 0; r < 4 && m0 + r < a.c_out; ++r) {
-      float x = v[r];
-      if (a.bias) x += a.bias[m0 + r];
-      if (res) x += to_f32(res[r]);
-      if (a.relu) x = x > 0.f ? x : 0.f;
-      y[r] = static_cast<T>(x);
-    }
-  }
-}
-
-// Final store (one split) or fp32 partial store into the split workspace.
-template <typename T>
-__device__ __forceinline__ void emit4(const ConvArgs &a, long vox, int m0, float v0, float v1,
-                                      float v2, float v3) {
-  if (a.splits == 1) {
-    store4<T>(a, vox, m0, v0, v1, v2, v3);
-  } else if (m0 < a.c_out) {
-    float *dst = a.ws + (static_cast<long>(blockIdx.z) * a.total_vox + vox) * a.c_out4 + m0;
-    *reinterpret_cast<float4 *>(dst) = make_float4(v0, v1, v2, v3);
-  }
-}
-
 // Channel chunks handled by this workgroup's split.
 __device__ __forceinline__ void split_range(const ConvArgs &a, int &ch0, int &ch1) {
   ch0 = static_cast<int>((static_cast<long>(blockIdx.z) * a.nchunks) / a.splits);
   ch1 = static_cast<int>((static_cast<long>(blockIdx.z + 1) * a.nchunks) / a.splits);
+}
+
+// ---------------------------------------------------------------------------
+// Tile epilogue.  After the K loop every wave writes its fp32 accumulators
+// into an LDS tile [voxel slot][filter of the workgroup]; the workgroup then
+// stores it cooperatively, four consecutive filters per thread and item, so
+// each 64-lane store covers whole output rows (channels-last).  On the way it
+// adds bias and residual, applies ReLU, max-pools windows of qt x qh x qw
+// voxels (bricks hold whole windows), rounds to the output dtype -- or, for a
+// split of the channel range, stores the raw fp32 partial sums.
+// ---------------------------------------------------------------------------
+
+// act(acc + bias (+ residual)) for filters m0..m0+3 of unpooled voxel vox.
+template <typename T>
+__device__ __forceinline__ float4 activate4(const ConvArgs &a, long vox, int m0, float4 v) {
+  float r[4] = {v.x, v.y, v.z, v.w};
+  const bool full = (a.c_out & 3) == 0;
+  if (a.bias) {
+    if (full) {
+      const float4 bb = *reinterpret_cast<const float4 *>(a.bias + m0);
+      r[0] += bb.x; r[1] += bb.y; r[2] += bb.z; r[3] += bb.w;
+    } else {
+      for (int q = 0; q < 4; ++q)
+        if (m0 + q < a.c_out) r[q] += a.bias[m0 + q];
+    }
+  }
+  if (a.res) {
+    const T *res = static_cast<const T *>(a.res) + vox * a.c_out + m0;
+    if (full && sizeof(T) == 4) {
+      const float4 rr = *reinterpret_cast<const float4 *>(res);
+      r[0] += rr.x; r[1] += rr.y; r[2] += rr.z; r[3] += rr.w;
+    } else if (full) {
+      union { uint2 u; T e[4]; } rr;
+      rr.u = *reinterpret_cast<const uint2 *>(res);
+      for (int q = 0; q < 4; ++q) r[q] += to_f32(rr.e[q]);
+    } else {
+      for (int q = 0; q < 4; ++q)
+        if (m0 + q < a.c_out) r[q] += to_f32(res[q]);
+    }
+  }
+  if (a.relu)
+    for (int q = 0; q < 4; ++q) r[q] = r[q] > 0.f ? r[q] : 0.f;
+  return make_float4(r[0], r[1], r[2], r[3]);
+}
+
+// Round and store filters m0..m0+3 of output voxel vox (of y's own extent).
+template <typename T>
+__device__ __forceinline__ void put4(const ConvArgs &a, long vox, int m0, float4 v) {
+  T *y = static_cast<T *>(a.y) + vox * a.c_out + m0;
+  const float r[4] = {v.x, v.y, v.z, v.w};
+  if ((a.c_out & 3) == 0) {
+    if constexpr (sizeof(T) == 4) {
+      *reinterpret_cast<float4 *>(y) = v;
+    } else {
+      union { uint2 u; T e[4]; } o;
+      for (int q = 0; q < 4; ++q) o.e[q] = static_cast<T>(r[q]);
+      *reinterpret_cast<uint2 *>(y) = o.u;
+    }
+  } else {
+    for (int q = 0; q < 4 && m0 + q < a.c_out; ++q) y[q] = static_cast<T>(r[q]);
+  }
+}
+
+__device__ __forceinline__ float4 max4(float4 x, float4 y) {
+  return make_float4(x.x > y.x ? x.x : y.x, x.y > y.y ? x.y : y.y, x.z > y.z ? x.z : y.z,
+                     x.w > y.w ? x.w : y.w);
+}
+
+// Walks voxel slots (t, h, w) of a bt x bh x bw box in steps of `step`
+// slots with carries instead of divisions (step is at most 64).
+struct BoxIter {
+  int t, h, w;
+  __device__ __forceinline__ void init(int slot, int bh, int bw) {
+    const int plane = bh * bw;
+    t = slot / plane;
+    h = (slot - t * plane) / bw;
+    w = slot - t * plane - h * bw;
+  }
+  __device__ __forceinline__ void advance(int step, int bh, int bw) {
+    w += step;
+    while (w >= bw) { w -= bw; ++h; }
+    while (h >= bh) { h -= bh; ++t; }
+  }
+};
+
+template <typename T>
+__device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, const uint8_t *lds,
+                                           int m_wg0) {
+  // Thread t owns the 4-filter group t % cg of every voxel slot
+  // t / cg + k * (blockDim / cg); cg divides the block size (16, 32 or 64).
+  const int cg = a.c_wg >> 2;
+  const int step = blockDim.x / cg;
+  const int c4 = threadIdx.x % cg;
+  const int m0 = m_wg0 + 4 * c4;
+  const bool live = m0 < a.c_out;
+  const uint8_t *col = lds + c4 * 16;
+  if (a.splits > 1) {
+    const int nslots = a.bt * a.bh * a.bw;
+    BoxIter it;
+    int slot = threadIdx.x / cg;
+    it.init(slot, a.bh, a.bw);
+    for (; slot < nslots; slot += step, it.advance(step, a.bh, a.bw)) {
+      if (!live || b.ot0 + it.t >= a.to || b.oh0 + it.h >= a.ho || b.ow0 + it.w >= a.wo) continue;
+      const long vox = ((static_cast<long>(b.nb) * a.to + b.ot0 + it.t) * a.ho + b.oh0 + it.h) * a.wo + b.ow0 + it.w;
+      const float4 v = *reinterpret_cast<const float4 *>(col + slot * a.tile_row);
+      *reinterpret_cast<float4 *>(a.ws + (static_cast<long>(blockIdx.z) * a.total_vox + vox) * a.c_out4 + m0) = v;
+    }
+    return;
+  }
+  const int pbt = a.bt / a.qt, pbh = a.bh / a.qh, pbw = a.bw / a.qw;
+  const int npslots = pbt * pbh * pbw;
+  BoxIter it;
+  int ps = threadIdx.x / cg;
+  it.init(ps, pbh, pbw);
+  for (; ps < npslots; ps += step, it.advance(step, pbh, pbw)) {
+    const int gt = b.ot0 / a.qt + it.t, gh = b.oh0 / a.qh + it.h, gw = b.ow0 / a.qw + it.w;
+    if (!live || gt >= a.pto || gh >= a.pho || gw >= a.pwo) continue;
+    float4 best = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int dt = 0; dt < a.qt; ++dt)
+      for (int dh = 0; dh < a.qh; ++dh)
+        for (int dw = 0; dw < a.qw; ++dw) {
+          const int tt = it.t * a.qt + dt, hh = it.h * a.qh + dh, ww = it.w * a.qw + dw;
+          const int slot = (tt * a.bh + hh) * a.bw + ww;
+          const long vox = ((static_cast<long>(b.nb) * a.to + b.ot0 + tt) * a.ho + b.oh0 + hh) * a.wo + b.ow0 + ww;
+          const float4 acc = *reinterpret_cast<const float4 *>(col + slot * a.tile_row);
+          const float4 v = activate4<T>(a, vox, m0, acc);
+          best = (dt | dh | dw) ? max4(best, v) : v;
+        }
+    const long pvox = ((static_cast<long>(b.nb) * a.pto + gt) * a.pho + gh) * a.pwo + gw;
+    put4<T>(a, pvox, m0, best);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -421,17 +495,19 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
       }
     });
   }
-  if (!active) return;
-  #pragma unroll
-  for (int j = 0; j < NF; ++j) {
-    const Slot sl = decode_slot(a, b, 16 * j + (lane & 15));
-    if (!sl.valid) continue;
-    #pragma unroll
-    for (int i = 0; i < MFW; ++i) {
-      const int m0 = wt * 16 * MFW + 16 * i + 4 * g;
-      emit4<T>(a, sl.out, m0, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
-    }
+  const int m_wg0 = static_cast<int>(blockIdx.y) * a.wpw * 16 * MFW;
+  __syncthreads();  // the halo is no longer needed: reuse LDS for the tile
+  if (active) {
+#pragma unroll
+    for (int j = 0; j < NF; ++j)
+#pragma unroll
+      for (int i = 0; i < MFW; ++i) {
+        const int col = wt * 16 * MFW - m_wg0 + 16 * i + 4 * g;
+        *reinterpret_cast<f32x4 *>(lds + (16 * j + (lane & 15)) * a.tile_row + col * 4) = acc[i][j];
+      }
   }
+  __syncthreads();
+  tile_store<T>(a, b, lds, m_wg0);
 }
 
 // ---------------------------------------------------------------------------
@@ -521,17 +597,19 @@ __global__ __launch_bounds__(256) void items_f32_kernel(ConvArgs a) {
       if (s + D < s_end) compute(D);
     });
   }
-  if (!active) return;
-  #pragma unroll
-  for (int j = 0; j < NF; ++j) {
-    const Slot sl = decode_slot(a, b, 16 * j + (lane & 15));
-    if (!sl.valid) continue;
-    #pragma unroll
-    for (int i = 0; i < MFW; ++i) {
-      const int m0 = wt * 16 * MFW + 16 * i + 4 * g;
-      emit4<float>(a, sl.out, m0, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
-    }
+  const int m_wg0 = static_cast<int>(blockIdx.y) * a.wpw * 16 * MFW;
+  __syncthreads();  // the halo is no longer needed: reuse LDS for the tile
+  if (active) {
+#pragma unroll
+    for (int j = 0; j < NF; ++j)
+#pragma unroll
+      for (int i = 0; i < MFW; ++i) {
+        const int col = wt * 16 * MFW - m_wg0 + 16 * i + 4 * g;
+        *reinterpret_cast<f32x4 *>(lds + (16 * j + (lane & 15)) * a.tile_row + col * 4) = acc[i][j];
+      }
   }
+  __syncthreads();
+  tile_store<float>(a, b, lds, m_wg0);
 }
 
 // ---------------------------------------------------------------------------
@@ -608,17 +686,19 @@ __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
       });
     }
   }
-  if (!active) return;
-  #pragma unroll
-  for (int s = 0; s < SUB; ++s) {
-    const Slot sl = decode_slot(a, b, 64 * s + lane);
-    if (!sl.valid) continue;
-    #pragma unroll
-    for (int gi = 0; gi < 4; ++gi) {
-      const int m0 = wt * 16 + 4 * gi;
-      emit4<float>(a, sl.out, m0, acc[gi][s][0], acc[gi][s][1], acc[gi][s][2], acc[gi][s][3]);
-    }
+  const int m_wg0 = static_cast<int>(blockIdx.y) * a.wpw * 16;
+  __syncthreads();  // the halo is no longer needed: reuse LDS for the tile
+  if (active) {
+#pragma unroll
+    for (int s = 0; s < SUB; ++s)
+#pragma unroll
+      for (int gi = 0; gi < 4; ++gi) {
+        const int col = wt * 16 - m_wg0 + 4 * gi;
+        *reinterpret_cast<f32x4 *>(lds + (64 * s + lane) * a.tile_row + col * 4) = acc[gi][s];
+      }
   }
+  __syncthreads();
+  tile_store<float>(a, b, lds, m_wg0);
 }
 
 // ---------------------------------------------------------------------------
@@ -629,17 +709,32 @@ __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
 template <typename T>
 __global__ __launch_bounds__(256) void reduce_splits_kernel(ConvArgs a) {
   const int groups = a.c_out4 >> 2;
-  const long total = a.total_vox * groups;
+  const long pvox_total = static_cast<long>(a.n) * a.pto * a.pho * a.pwo;
+  const long total = pvox_total * groups;
   for (long idx = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
        idx += static_cast<long>(gridDim.x) * blockDim.x) {
-    const long vox = idx / groups;
-    const int m0 = static_cast<int>(idx - vox * groups) * 4;
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int z = 0; z < a.splits; ++z) {
-      const float4 v = *reinterpret_cast<const float4 *>(a.ws + (static_cast<long>(z) * a.total_vox + vox) * a.c_out4 + m0);
-      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-    }
-    store4<T>(a, vox, m0, acc.x, acc.y, acc.z, acc.w);
+    const long pv = idx / groups;
+    const int m0 = static_cast<int>(idx - pv * groups) * 4;
+    const int gw = static_cast<int>(pv % a.pwo);
+    long r = pv / a.pwo;
+    const int gh = static_cast<int>(r % a.pho);
+    r /= a.pho;
+    const int gt = static_cast<int>(r % a.pto);
+    const long nb = r / a.pto;
+    float4 best = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int dt = 0; dt < a.qt; ++dt)
+      for (int dh = 0; dh < a.qh; ++dh)
+        for (int dw = 0; dw < a.qw; ++dw) {
+          const long vox = ((nb * a.to + gt * a.qt + dt) * a.ho + gh * a.qh + dh) * a.wo + gw * a.qw + dw;
+          float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+          for (int z = 0; z < a.splits; ++z) {
+            const float4 v = *reinterpret_cast<const float4 *>(a.ws + (static_cast<long>(z) * a.total_vox + vox) * a.c_out4 + m0);
+            acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+          }
+          const float4 v = activate4<T>(a, vox, m0, acc);
+          best = (dt | dh | dw) ? max4(best, v) : v;
+        }
+    if (m0 < a.c_out) put4<T>(a, pv, m0, best);
   }
 }
 
@@ -682,7 +777,11 @@ __global__ __launch_bounds__(256) void maxpool_kernel(const T *__restrict__ x, T
   }
 }
 
-size_t halo_bytes(const ConvArgs &a) { return static_cast<size_t>(a.ht) * a.hh * a.hw * a.row; }
+size_t halo_bytes(const ConvArgs &a) {
+  const size_t halo = static_cast<size_t>(a.ht) * a.hh * a.hw * a.row;
+  const size_t tile = static_cast<size_t>(128) * a.tile_row;  // epilogue tile: 128 voxel slots
+  return halo > tile ? halo : tile;
+}
 
 template <typename K>
 int launch_conv(K kernel, const ConvArgs &a, void *stream) {
@@ -726,7 +825,7 @@ int launch_items_f32(const ConvArgs &a, int mfw, void *stream) {
 }
 
 int launch_reduce_splits(const ConvArgs &a, int dtype, void *stream) {
-  const long total = a.total_vox * (a.c_out4 / 4);
+  const long total = static_cast<long>(a.n) * a.pto * a.pho * a.pwo * (a.c_out4 / 4);
   if (total == 0) return hipSuccess;
   long blocks = (total + 255) / 256;
   if (blocks > 65536) blocks = 65536;

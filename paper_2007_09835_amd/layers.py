@@ -28,13 +28,15 @@ class Conv3d:
     def __init__(self, c_in: int, c_out: int, thw: Sequence[int], k, stride, pad, w,
                  bias=None, mask: Optional[np.ndarray] = None, dtype: str = "bf16",
                  relu: bool = True, residual: bool = False, g=(4, 4), device="cuda",
-                 batch: int = 1):
+                 batch: int = 1, pool=(1, 1, 1)):
         """``batch`` is the batch size the layer is planned for (the blob
-        works for any batch; the tile shapes are chosen for this one)."""
+        works for any batch; the tile shapes are chosen for this one).
+        ``pool`` fuses a max-pool (window = stride) after the activation."""
         self.dtype = dtype
         self.sparse = mask is not None
         self.desc = rt3d.make_desc(batch, c_in, c_out, tuple(thw), tuple(k), tuple(stride),
-                                   tuple(pad), tuple(g), dtype, relu=relu, residual=residual)
+                                   tuple(pad), tuple(g), dtype, relu=relu, residual=residual,
+                                   pool=tuple(pool))
         if self.sparse:
             blob, self.info = rt3d.rt3d_kgs_pack(self.desc, w, mask)
         else:

@@ -23,8 +23,12 @@ class Stack:
     (every layer on the dense kernel)."""
 
     def __init__(self, net: str, batch: int = 1, dtype: str = "bf16", mode: str = "kgs",
-                 rate: float = 3.0, tag: Optional[str] = None, device: str = "cuda"):
+                 rate: float = 3.0, tag: Optional[str] = None, device: str = "cuda",
+                 fuse_pool: bool = True):
+        """``fuse_pool`` folds each max-pool into the preceding conv's
+        epilogue; otherwise the pools run as separate kernels."""
         self.net, self.batch, self.dtype, self.mode, self.rate = net, batch, dtype, mode, rate
+        self.fuse_pool = fuse_pool
         tag = tag or net
         if net == "c3d":
             self.layers = synth.c3d_stack(rate if mode == "kgs" else 3.0, tag=tag)
@@ -44,10 +48,11 @@ class Stack:
                 mask = d.mask
             self.masks.append(None if l.dense else d.mask)
             w = synth.to_dtype(d.w, dtype)
+            pool = l.pool_after[0] if (fuse_pool and l.pool_after) else (1, 1, 1)
             self.convs.append(layers.Conv3d(l.c_in, l.c_out, (l.t, l.h, l.w), l.k, l.stride, l.pad,
                                             w, d.bias.astype(np.float32), mask, dtype,
                                             relu=l.relu, residual=l.residual_from is not None,
-                                            device=device, batch=batch))
+                                            device=device, batch=batch, pool=pool))
         # activation buffers (channels-last), allocated once
         self.x = torch.zeros((batch, self.layers[0].t, self.layers[0].h, self.layers[0].w,
                               self.layers[0].c_in), dtype=tdt, device=device)
@@ -55,7 +60,7 @@ class Stack:
         self.pool_bufs: Dict[str, torch.Tensor] = {}
         for l, c in zip(self.layers, self.convs):
             self.bufs[l.name] = torch.empty(c.out_shape(batch), dtype=tdt, device=device)
-            if l.pool_after:
+            if l.pool_after and not fuse_pool:
                 k, s = l.pool_after
                 n, t, h, w, ch = c.out_shape(batch)
                 self.pool_bufs[l.name] = torch.empty(
@@ -93,7 +98,7 @@ class Stack:
             if ev:
                 ev[1].record()
             outs[l.name] = y
-            if l.pool_after:
+            if l.pool_after and not self.fuse_pool:
                 k, s = l.pool_after
                 y = layers.maxpool3d(y, k, s, self.dtype, out=self.pool_bufs[l.name])
                 outs[l.name] = y

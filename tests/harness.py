@@ -34,8 +34,9 @@ class LayerCase:
     oracle.  x64 / w64 / res64 are the float64 images of the dtype values."""
 
     def __init__(self, tag, n, c_in, c_out, thw, k, stride, pad, dtype, mask=None, relu=True,
-                 residual=False, w_std=None, x_kind="halfnormal", g=(4, 4), bias=True):
-        self.dtype, self.mask, self.g = dtype, mask, g
+                 residual=False, w_std=None, x_kind="halfnormal", g=(4, 4), bias=True,
+                 pool=(1, 1, 1)):
+        self.dtype, self.mask, self.g, self.pool = dtype, mask, g, tuple(pool)
         self.k, self.stride, self.pad, self.relu = k, stride, pad, relu
         r = synth.rng_for(tag, "w")
         if w_std is None:
@@ -53,7 +54,8 @@ class LayerCase:
             self.res_t, self.res64 = rounded(res, dtype)
         self.conv = layers.Conv3d(c_in, c_out, thw, k, stride, pad, self.w_t,
                                   None if self.b64 is None else self.b64.astype(np.float32),
-                                  mask, dtype, relu=relu, residual=residual, g=g)
+                                  mask, dtype, relu=relu, residual=residual, g=g, batch=n,
+                                  pool=pool)
         # The kernel adds a float32 bias: the oracle sees the same float32 values.
         self.b_oracle = None if self.b64 is None else self.b64.astype(np.float32).astype(np.float64)
 
@@ -66,10 +68,14 @@ class LayerCase:
 
     def oracle_full(self):
         if self.mask is None:
-            return oracle.conv3d_dense(self.x64, self.w64, self.b_oracle, self.res64, self.stride,
-                                       self.pad, self.relu)
-        return oracle.conv3d_kgs(self.x64, self.w64, self.mask, *self.g, self.b_oracle, self.res64,
-                                 self.stride, self.pad, self.relu)
+            y = oracle.conv3d_dense(self.x64, self.w64, self.b_oracle, self.res64, self.stride,
+                                    self.pad, self.relu)
+        else:
+            y = oracle.conv3d_kgs(self.x64, self.w64, self.mask, *self.g, self.b_oracle,
+                                  self.res64, self.stride, self.pad, self.relu)
+        if self.pool != (1, 1, 1):
+            y = oracle.maxpool3d(y, self.pool, self.pool)
+        return y
 
     def oracle_points(self, idx):
         return oracle.conv3d_points(self.x64, self.w64, idx, self.mask, *self.g, self.b_oracle,

@@ -162,6 +162,29 @@ def test_split_k_matches_unsplit(dtype, sparse):
     assert rel_l2(unsplit, ref) <= TOL[dtype]
 
 
+POOLED = [
+    # tag, n, c_in, c_out, thw, pool, dtype, sparse, residual
+    ("pa", 1, 16, 32, (4, 8, 12), (1, 2, 2), "bf16", True, False),
+    ("pb", 2, 32, 48, (6, 9, 11), (2, 2, 2), "bf16", True, False),    # floor: odd extents
+    ("pc", 1, 24, 16, (5, 7, 9), (2, 2, 2), "f32", True, True),
+    ("pd", 1, 64, 64, (4, 8, 8), (2, 2, 2), "f16", False, False),
+    ("pe", 1, 256, 128, (4, 6, 6), (2, 2, 2), "bf16", True, False),   # split-K + pooled reduce
+    ("pf", 1, 256, 128, (4, 6, 6), (2, 2, 2), "f32", False, True),
+    ("pg", 1, 3, 64, (2, 16, 16), (1, 2, 2), "bf16", False, False),   # conv1-like
+]
+
+
+@pytest.mark.parametrize("pi", range(len(POOLED)))
+def test_fused_pool_epilogue(pi):
+    """conv -> act -> max-pool fused in the epilogue equals the oracle's
+    max-pool of its conv output (window = stride, floor extents)."""
+    tag, n, c_in, c_out, thw, pool, dtype, sparse, residual = POOLED[pi]
+    mask = masked(tag, c_out, c_in, (3, 3, 3), 9) if sparse else None
+    case = LayerCase(tag, n, c_in, c_out, thw, (3, 3, 3), (1, 1, 1), (1, 1, 1), dtype, mask,
+                     residual=residual, pool=pool)
+    check_full(case, f"pooled {tag} {dtype} {'kgs' if sparse else 'dense'}")
+
+
 def test_runs_are_deterministic():
     mask = masked("det", 64, 64, (3, 3, 3), 9)
     case = LayerCase("det", 1, 64, 64, (4, 14, 14), (3, 3, 3), (1, 1, 1), (1, 1, 1), "bf16", mask)
