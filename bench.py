@@ -36,6 +36,8 @@ def parse():
     p.add_argument("--rate", type=float, default=3.0, help="whole-stack MAC pruning rate (KGS)")
     p.add_argument("--mode", default="kgs", choices=["kgs", "vanilla"])
     p.add_argument("--no-graph", action="store_true", help="launch eagerly instead of a HIP graph")
+    p.add_argument("--separate-pool", action="store_true",
+                   help="run max-pools as their own kernels instead of in the conv epilogue")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample", type=float, default=1.0,
                    help="fraction of every layer's outputs the oracle computes (1 = full clip)")
@@ -112,7 +114,8 @@ def profile_layer(args, torch, stream):
     """Launch one layer of the sparse stack back to back (and optionally a
     plain copy of known size) so rocprofv3 sees only these kernels."""
     from paper_2007_09835_amd.stack import Stack
-    sparse = Stack(args.net, args.batch, args.dtype, args.mode, args.rate)
+    sparse = Stack(args.net, args.batch, args.dtype, args.mode, args.rate,
+                   fuse_pool=not args.separate_pool)
     idx = [l.name for l in sparse.layers].index(args.profile_layer)
     l, conv = sparse.layers[idx], sparse.convs[idx]
     inp = torch.randn(conv.desc_for(args.batch).n, l.t, l.h, l.w, l.c_in, device="cuda").abs()
@@ -209,8 +212,9 @@ def main():
         return
 
     log("building stacks ...")
-    sparse = Stack(args.net, args.batch, args.dtype, args.mode, args.rate)
-    dense = Stack(args.net, args.batch, args.dtype, "dense")
+    fuse = not args.separate_pool
+    sparse = Stack(args.net, args.batch, args.dtype, args.mode, args.rate, fuse_pool=fuse)
+    dense = Stack(args.net, args.batch, args.dtype, "dense", fuse_pool=fuse)
     l0 = sparse.layers[0]
     clip = synth.clip_input("bench-clip", args.batch, "uniform01", l0.c_in, l0.t, l0.h, l0.w)
     x = synth.to_dtype(clip, args.dtype).permute(0, 2, 3, 4, 1).contiguous().cuda()

@@ -145,11 +145,12 @@ Tiling choose_tiling(const Geom &g) {
   const int epp = 16 / g.es;
   int cc = epp;  // smallest power-of-two multiple of a piece covering c_in, capped
   while (cc < g.c_in && cc < (g.es == 2 ? 32 : 16)) cc *= 2;
-  // LDS row pitch: an odd number of bank-width units (8 bytes for the 16-bit
-  // kernels, which read 8-byte item slices; 16 bytes for fp32) so that 16
-  // voxels whose halo indices differ modulo 16 fall on 16 distinct banks.
-  const int unit = g.es == 2 ? 8 : 16;
-  const int row = cc * g.es + unit;
+  // LDS row pitch: an odd multiple of 16 bytes (4 banks), so that 16 voxels
+  // whose halo indices differ modulo 16 start on 16 distinct bank quads and
+  // two 8-byte item reads in one pass are conflict-free when their channel
+  // blocks differ in parity (see pair_items).
+  int row = (cc * g.es + 15) / 16 * 16;
+  if ((row / 16) % 2 == 0) row += 16;
   // Bricks hold whole pooling windows (their origins are then multiples of
   // the window too), so the fused pooling never crosses workgroups.
   for (int bw = g.qw; bw <= std::max(g.qw, std::min(g.wo, kSlots)); bw += g.qw)
@@ -285,10 +286,11 @@ struct Item {
   uint32_t keep;
 };
 
-// Items of one chunk for one 16-filter tile: every (block, position) that
-// any of the tile's four 4x4 blocks keeps (all of them when dense), in
-// position-major order.
-std::vector<Item> chunk_items(const Geom &g, const Mask4 *m4, int cc, int ch, int p4_first) {
+// Items of one chunk for one wave tile of 4*nb4 filters: every (block,
+// position) that any of the tile's nb4 4x4 blocks keeps (all of them when
+// dense), in position-major order.
+std::vector<Item> chunk_items(const Geom &g, const Mask4 *m4, int cc, int ch, int p4_first,
+                              int nb4 = 4) {
   std::vector<Item> out;
   const int blocks = cc / 4;
   const int q4_count = (g.c_in + 3) / 4;
@@ -298,13 +300,106 @@ std::vector<Item> chunk_items(const Geom &g, const Mask4 *m4, int cc, int ch, in
       const int q4 = ch * blocks + ql;
       if (q4 >= q4_count) continue;
       uint32_t keep = 0;
-      for (int gi = 0; gi < 4; ++gi) {
+      for (int gi = 0; gi < nb4; ++gi) {
         const int p4 = p4_first + gi;
         if (p4 < p4_count && (!m4 || m4->kept(p4, q4, pos))) keep |= 1u << gi;
       }
       if (keep) out.push_back(Item{ql, pos, keep});
     }
   return out;
+}
+
+// LDS bank model of gfx950 (measured with a read-pattern probe): 64 banks of
+// 4 bytes; a wave's ds_read_b64 is served in two passes of 32 lanes, and a
+// pass takes as many cycles as its most loaded bank has distinct addresses.
+// In the 16-bit item kernel a pass carries lane groups g and g+1, which read
+// two different items for the same 16 voxel slots, so the planner pairs the
+// items of each pass to avoid conflicts.
+class PassCost {
+ public:
+  PassCost(const Geom &g, const Tiling &tl) : row_dw_(tl.row / 4) {
+    for (int f = 0; f < tl.slots / 16; ++f)
+      for (int n = 0; n < 16; ++n) {
+        const int sl = 16 * f + n;
+        const int tt = sl / (tl.bh * tl.bw), hh = (sl / tl.bw) % tl.bh, ww = sl % tl.bw;
+        const int v = tt < tl.bt ? ((tt * g.st) * tl.hh + hh * g.sh) * tl.hw + ww * g.sw : 0;
+        rows_.push_back(v);
+      }
+    span_ = tl.ht * tl.hh * tl.hw * row_dw_;
+    memo_.assign(2 * static_cast<size_t>(span_) + 1, -1);
+  }
+  // Cycles of one pass whose two lane groups read byte offsets o1 and o2.
+  int operator()(uint32_t o1, uint32_t o2) {
+    const long d = (static_cast<long>(o2) - static_cast<long>(o1)) / 4;
+    if (d < -span_ || d > span_) return eval(d);
+    int8_t &m = memo_[static_cast<size_t>(d + span_)];
+    if (m < 0) m = static_cast<int8_t>(eval(d));
+    return m;
+  }
+
+ private:
+  int eval(long d) const {
+    int worst = 1;
+    for (size_t f = 0; f < rows_.size(); f += 16) {
+      long addr[64];
+      int k = 0;
+      for (int grp = 0; grp < 2; ++grp)
+        for (int n = 0; n < 16; ++n)
+          for (int e = 0; e < 2; ++e)
+            addr[k++] = static_cast<long>(rows_[f + n]) * row_dw_ + (grp ? d : 0) + e;
+      std::sort(addr, addr + 64);
+      int per_bank[64] = {0};
+      for (int i = 0; i < 64; ++i)
+        if (i == 0 || addr[i] != addr[i - 1]) {
+          const int b = static_cast<int>(((addr[i] % 64) + 64) % 64);
+          worst = std::max(worst, ++per_bank[b]);
+        }
+    }
+    return worst;
+  }
+  long row_dw_, span_;
+  std::vector<int> rows_;
+  std::vector<int8_t> memo_;
+};
+
+// Reorders a step-padded item list so that items 2k and 2k+1 share an LDS
+// pass with as few bank conflicts as possible (greedy over a window), then
+// lays the pairs out in K-step order: pass pairs (0,2) (4,6) (1,3) (5,7).
+void pair_items(std::vector<Item> &its, const Geom &g, const Tiling &tl, PassCost &cost) {
+  const size_t n = its.size();
+  auto off = [&](const Item &it) { return it.ql < 0 ? 0u : item_offset(g, tl, it.ql, it.pos); };
+  std::vector<char> used(n, 0);
+  std::vector<Item> paired;
+  paired.reserve(n);
+  constexpr size_t kWindow = 48;
+  for (size_t i = 0; i < n; ++i) {
+    if (used[i]) continue;
+    used[i] = 1;
+    const uint32_t oi = off(its[i]);
+    size_t best = n;
+    int best_cost = 1 << 30;
+    for (size_t j = i + 1, looked = 0; j < n && looked < kWindow; ++j) {
+      if (used[j]) continue;
+      ++looked;
+      const int c = cost(oi, off(its[j]));
+      if (c < best_cost) {
+        best_cost = c;
+        best = j;
+        if (c == 1) break;
+      }
+    }
+    paired.push_back(its[i]);
+    if (best < n) {
+      used[best] = 1;
+      paired.push_back(its[best]);
+    }
+  }
+  // n is a multiple of 8, so every item found a partner.
+  for (size_t s = 0; s + 8 <= n; s += 8) {
+    const Item *p = &paired[s];
+    const Item step[8] = {p[0], p[2], p[1], p[3], p[4], p[6], p[5], p[7]};
+    std::copy(step, step + 8, its.begin() + static_cast<long>(s));
+  }
 }
 
 // 16-bit MFMA item layout (variants kVarDenseItems16, kVarKgsUnion16) and
@@ -333,6 +428,9 @@ void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
       const int v = std::atoi(env);
       if (v == 1 || v == 2 || v == 4) mfw = v;
     }
+  } else if (const char *env = std::getenv("RT3D_KGS_MFW")) {
+    const int v = std::atoi(env);
+    if (v == 1 || v == 2 || v == 4) mfw = v;
   }
   const int wt_count = (g.c_out + 16 * mfw - 1) / (16 * mfw);
   L.variant = dense ? (f32 ? kVarDenseItemsF32 : kVarDenseItems16) : kVarKgsUnion16;
@@ -343,10 +441,17 @@ void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
   L.item_ptr.assign(wt_count, 0);
   WeightSource src{w, g, m4};
 
+  PassCost cost(g, tl);
+  auto prepare = [&](std::vector<Item> its) {
+    while (its.size() % ips) its.push_back(Item{-1, 0, 0});  // zero-weight filler
+    if (!f32) pair_items(its, g, tl, cost);
+    return its;
+  };
   // Dense: one item list shared by every wave tile.
   std::vector<std::vector<Item>> shared;
   if (dense)
-    for (int ch = 0; ch < tl.nchunks; ++ch) shared.push_back(chunk_items(g, nullptr, tl.cc, ch, 0));
+    for (int ch = 0; ch < tl.nchunks; ++ch)
+      shared.push_back(prepare(chunk_items(g, nullptr, tl.cc, ch, 0)));
 
   uint32_t step = 0;
   for (int wt = 0; wt < wt_count; ++wt) {
@@ -355,8 +460,8 @@ void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
     L.item_ptr[wt] = dense ? 0 : first_step;
     for (int ch = 0; ch < tl.nchunks; ++ch) {
       L.step_ptr[static_cast<size_t>(wt) * (tl.nchunks + 1) + ch] = step;
-      std::vector<Item> its = dense ? shared[ch] : chunk_items(g, m4, tl.cc, ch, wt * 4);
-      while (its.size() % ips) its.push_back(Item{-1, 0, 0});  // zero-weight filler
+      const std::vector<Item> its =
+          dense ? shared[ch] : prepare(chunk_items(g, m4, tl.cc, ch, wt * 4 * mfw, 4 * mfw));
       const int nsteps = static_cast<int>(its.size()) / ips;
       for (int s = 0; s < nsteps; ++s) {
         const Item *si = &its[static_cast<size_t>(s) * ips];
@@ -599,26 +704,85 @@ rt3d_status check_info(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, bo
 // Launch shape for a batch: waves per workgroup and channel-chunk splits so
 // that the grid covers the GPU several times over, limited by the workspace
 // the caller provides (ws_cap bytes; UINT64_MAX when sizing).
-Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint64_t ws_cap) {
+// Bytes the eight XCDs pull into their L2s when the logical workgroup ids
+// (brick, filter tile group, split) are laid out with `order` and each XCD
+// runs one contiguous run of them: a workgroup reads the weight rows of its
+// (split, tile group) and the halo of its (split, brick).
+double xcd_fill_bytes(long nb, long nt, long ns, int order, double a_unit, double x_unit) {
+  const long nw = nb * nt * ns;
+  const long q = nw / 8, r = nw % 8;
+  const long inner = order == 0 ? nb : nt;          // fastest-varying index
+  const long per_split = nb * nt;
+  const double outer_unit = order == 0 ? a_unit : x_unit;  // pairs (split, slower index)
+  const double inner_unit = order == 0 ? x_unit : a_unit;  // pairs (split, inner index)
+  double total = 0;
+  long lo = 0;
+  for (int x = 0; x < 8; ++x) {
+    const long cnt = q + (x < r ? 1 : 0);
+    if (cnt == 0) continue;
+    const long hi = lo + cnt;
+    total += static_cast<double>((hi - 1) / inner - lo / inner + 1) * outer_unit;
+    for (long sp = lo / per_split; sp <= (hi - 1) / per_split; ++sp) {
+      const long a0 = std::max(lo, sp * per_split), a1 = std::min(hi, (sp + 1) * per_split);
+      total += static_cast<double>(std::min(inner, a1 - a0)) * inner_unit;
+    }
+    lo = hi;
+  }
+  return total;
+}
+
+// Compute units of the current device (256 when no device answers).
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  return cus;
+}
+
+Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint32_t variant, uint64_t ws_cap,
+                   uint64_t a_bytes) {
   const Geom g = geom_of(d);
   const Tiling &tl = p.tiling;
   const long bricks = static_cast<long>(g.n) * ((g.to + tl.bt - 1) / tl.bt) *
                       ((g.ho + tl.bh - 1) / tl.bh) * ((g.wo + tl.bw - 1) / tl.bw);
-  // Four waves per workgroup share one staged brick; parallelism beyond the
-  // bricks and filter tiles comes from channel splits, used until the grid
-  // has about two workgroups per CU (split partials cost memory traffic).
-  long target = 256;
-  if (const char *env = std::getenv("RT3D_SPLIT_TARGET")) target = std::max(1, std::atoi(env));
-  const long kTarget = target;
-  Launch L{4, 1, 0};
-  const long wgs = bricks * ((p.wave_tiles + L.wpw - 1) / L.wpw);
+  Launch L{4, 1, 0, 0};
+  const long ntg = (p.wave_tiles + L.wpw - 1) / L.wpw;
+  const long wgs = bricks * ntg;
+  // Channel splits add workgroups until the GPU holds one resident round:
+  // CUs x workgroups per CU (registers and LDS of the split-K kernel, whose
+  // LDS is just the halo).  A second partial round would double the time,
+  // so the count is rounded down, then lowered to the fewest splits that
+  // give the same number of chunks per workgroup (balanced splits).
+  const size_t halo = static_cast<size_t>(tl.ht) * tl.hh * tl.hw * tl.row;
+  int per_cu = conv_resident(static_cast<int>(variant), d->dtype, p.mfw, halo);
+  if (per_cu <= 0) {
+    (void)hipGetLastError();
+    per_cu = 2;
+  }
+  long cap = static_cast<long>(device_cus()) * per_cu;
+  if (const char *env = std::getenv("RT3D_SPLIT_TARGET")) cap = std::max(1, std::atoi(env));
   int splits = 1;
-  if (wgs < kTarget) splits = static_cast<int>(std::min<long>(tl.nchunks, (kTarget + wgs - 1) / wgs));
+  if (wgs < cap) {
+    splits = static_cast<int>(std::min<long>(tl.nchunks, std::max<long>(1, cap / wgs)));
+    const int per = (tl.nchunks + splits - 1) / splits;
+    splits = (tl.nchunks + per - 1) / per;
+  }
   const long total_vox = static_cast<long>(g.n) * g.to * g.ho * g.wo;
   const uint64_t per_split = static_cast<uint64_t>(total_vox) * ((g.c_out + 3) / 4 * 4) * 4;
   while (splits > 1 && per_split * splits > ws_cap) --splits;
   L.splits = splits;
   L.ws_bytes = splits > 1 ? per_split * splits : 0;
+  const double a_unit = static_cast<double>(a_bytes) / (static_cast<double>(ntg) * splits);
+  const double x_unit = static_cast<double>(tl.ht) * tl.hh * tl.hw * tl.cc * g.es * tl.nchunks / splits;
+  L.order = xcd_fill_bytes(bricks, ntg, splits, 1, a_unit, x_unit) <
+                    xcd_fill_bytes(bricks, ntg, splits, 0, a_unit, x_unit)
+                ? 1
+                : 0;
+  if (const char *env = std::getenv("RT3D_WG_ORDER")) L.order = std::atoi(env) ? 1 : 0;
   return L;
 }
 
@@ -639,7 +803,7 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
     return fail(RT3D_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
   Plan p;
   std::memcpy(&p, info->plan, sizeof(p));
-  const Launch launch = plan_launch(d, p, workspace ? ws_bytes : 0);
+  const Launch launch = plan_launch(d, p, info->variant, workspace ? ws_bytes : 0, info->packed_bytes - p.a_off);
   const Geom g = geom_of(d);
   const Tiling &tl = p.tiling;
   const uint8_t *b = static_cast<const uint8_t *>(blob);
@@ -672,6 +836,12 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   a.pto = g.pto; a.pho = g.pho; a.pwo = g.pwo;
   a.c_wg = a.wpw * 16 * p.mfw;
   a.tile_row = a.c_wg * 4 + 16;  // +16 bytes: slot rows start on different banks
+  a.order = launch.order;
+  a.nbricks = static_cast<int32_t>(static_cast<long>(a.n) * a.nbt * a.nbh * a.nbw);
+  a.ntg = (a.wave_tiles + a.wpw - 1) / a.wpw;
+  // The kernels divide workgroup ids with a 24-bit reciprocal method.
+  if (static_cast<long>(a.n) * a.nbt * a.nbh * a.nbw * a.ntg * a.splits >= (1L << 24))
+    return fail(RT3D_ERR_UNSUPPORTED, "layer needs 2^24 or more workgroups");
   int e;
   switch (info->variant) {
     case kVarDenseItems16:
@@ -807,7 +977,7 @@ rt3d_status rt3d_conv3d_workspace_size(const rt3d_conv3d_desc *d, const rt3d_pac
     return fail(RT3D_ERR_BLOB_MISMATCH, "info does not belong to this layer description");
   Plan p;
   std::memcpy(&p, info->plan, sizeof(p));
-  *bytes = plan_launch(d, p, UINT64_MAX).ws_bytes;
+  *bytes = plan_launch(d, p, info->variant, UINT64_MAX, info->packed_bytes - p.a_off).ws_bytes;
   return ok();
 }
 

@@ -68,13 +68,15 @@ struct ConvArgs {
   int32_t wpw;        // waves (wave tiles) per workgroup
   int32_t splits;     // channel-chunk splits (grid.z); > 1 writes fp32 partials to ws
   int32_t c_out4;     // c_out rounded up to 4 (partial row pitch)
-  int32_t pad0;
+  int32_t order;      // logical workgroup order: 0 = bricks fastest, 1 = filter tiles fastest
   long total_vox;     // n * to * ho * wo
   float *ws;          // [splits][total_vox][c_out4] partial sums (splits > 1)
   int32_t qt, qh, qw; // fused pooling window (1 = none)
   int32_t pto, pho, pwo;  // pooled output extent
   int32_t c_wg;       // filters per workgroup (wpw * 16 * mfw)
   int32_t tile_row;   // LDS bytes per voxel slot of the epilogue tile
+  int32_t nbricks;    // n * nbt * nbh * nbw
+  int32_t ntg;        // workgroups along the filters: ceil(wave_tiles / wpw)
 };
 
 // Launch shape chosen at forward time from the batch size.
@@ -82,9 +84,13 @@ struct Launch {
   int wpw;
   int splits;
   uint64_t ws_bytes;
+  int order;  // ConvArgs::order
 };
 
 // Kernel launchers (rt3d_kernels.hip).  Return hipSuccess or the launch error.
+// Workgroups of the conv kernel for (variant, dtype, mfw) that fit on one CU
+// with `lds` bytes of dynamic LDS each; 0 when the runtime cannot say.
+int conv_resident(int variant, int dtype, int mfw, size_t lds);
 int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream);
 int launch_items_f32(const ConvArgs &a, int mfw, void *stream);
 int launch_kgs_exact_f32(const ConvArgs &a, void *stream);

@@ -17,6 +17,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+
 #include <type_traits>
 #include <utility>
 
@@ -43,6 +45,27 @@ __device__ __forceinline__ uint32_t uniform(uint32_t v) {
   return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(v)));
 }
 
+// n / d and n % d for 0 <= n < 2^24 and 1 <= d < 2^24.  The fp32 reciprocal
+// estimate has relative error below 2^-22, so for quotients below 2^21 the
+// truncated product is off by at most one, which one step corrects.  (The
+// host keeps every index divided here below 2^24.)
+struct DivMod {
+  int q, r;
+};
+
+__device__ __forceinline__ DivMod divmod(int n, int d) {
+  int q = static_cast<int>(static_cast<float>(n) * __builtin_amdgcn_rcpf(static_cast<float>(d)));
+  int r = n - q * d;
+  if (r < 0) {
+    --q;
+    r += d;
+  } else if (r >= d) {
+    ++q;
+    r -= d;
+  }
+  return {q, r};
+}
+
 // ---------------------------------------------------------------------------
 // Brick geometry
 // ---------------------------------------------------------------------------
@@ -53,15 +76,44 @@ struct Brick {
   int zt0, zh0, zw0;    // input coordinate of halo voxel (0, 0, 0)
 };
 
-__device__ __forceinline__ Brick decode_brick(const ConvArgs &a) {
+// Workgroup coordinates.  The hardware hands consecutive workgroup ids to
+// the eight XCDs in turn (id mod 8); remapping so that each XCD receives one
+// contiguous run of logical ids keeps the workgroups that share weight rows
+// (order 0: bricks fastest) or halo bricks (order 1: filter tiles fastest) in
+// one XCD's L2.  The remap is a bijection for any grid size.
+struct Wg {
+  int brick, tg, split;
+};
+
+__device__ __forceinline__ Wg decode_wg(const ConvArgs &a) {
+  const int nw = a.nbricks * a.ntg * a.splits;
+  const int id = static_cast<int>(blockIdx.x);
+  const int q = nw >> 3, r = nw & 7;
+  const int xcd = id & 7, local = id >> 3;
+  const int lid = xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
+  Wg g;
+  if (a.order == 0) {
+    const DivMod x = divmod(lid, a.nbricks), y = divmod(x.q, a.ntg);
+    g.brick = x.r;
+    g.tg = y.r;
+    g.split = y.q;
+  } else {
+    const DivMod x = divmod(lid, a.ntg), y = divmod(x.q, a.nbricks);
+    g.tg = x.r;
+    g.brick = y.r;
+    g.split = y.q;
+  }
+  g.brick = uniform(g.brick);
+  g.tg = uniform(g.tg);
+  g.split = uniform(g.split);
+  return g;
+}
+
+__device__ __forceinline__ Brick decode_brick(const ConvArgs &a, int brick) {
   Brick b;
-  int id = blockIdx.x;
-  const int bwi = id % a.nbw;
-  id /= a.nbw;
-  const int bhi = id % a.nbh;
-  id /= a.nbh;
-  const int bti = id % a.nbt;
-  b.nb = id / a.nbt;
+  const DivMod x = divmod(brick, a.nbw), y = divmod(x.q, a.nbh), z = divmod(y.q, a.nbt);
+  const int bwi = x.r, bhi = y.r, bti = z.r;
+  b.nb = z.q;
   b.ot0 = bti * a.bt;
   b.oh0 = bhi * a.bh;
   b.ow0 = bwi * a.bw;
@@ -80,11 +132,8 @@ struct Slot {
 };
 
 __device__ __forceinline__ Slot decode_slot(const ConvArgs &a, const Brick &b, int s) {
-  const int plane = a.bh * a.bw;
-  int tt = s / plane;
-  const int r = s - tt * plane;
-  int hh = r / a.bw;
-  int ww = r - hh * a.bw;
+  const DivMod x = divmod(s, a.bh * a.bw), y = divmod(x.r, a.bw);
+  int tt = x.q, hh = y.q, ww = y.r;
   Slot o;
   o.valid = tt < a.bt && b.ot0 + tt < a.to && b.oh0 + hh < a.ho && b.ow0 + ww < a.wo;
   if (!o.valid) tt = hh = ww = 0;
@@ -105,12 +154,9 @@ __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, cons
   const bool vec = (a.c_in % EPP) == 0;
   const uint8_t *xb = static_cast<const uint8_t *>(a.x);
   for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
-    const int hv = idx / ppr;
-    const int piece = idx - hv * ppr;
-    const int xw = hv % a.hw;
-    const int rest = hv / a.hw;
-    const int xh = rest % a.hh;
-    const int xt = rest / a.hh;
+    const DivMod p = divmod(idx, ppr), x = divmod(p.q, a.hw), y = divmod(x.q, a.hh);
+    const int hv = p.q, piece = p.r;
+    const int xw = x.r, xh = y.r, xt = y.q;
     const int zt = b.zt0 + xt, zh = b.zh0 + xh, zw = b.zw0 + xw;
     const int c = c0 + piece * EPP;
     uint4 v = make_uint4(0, 0, 0, 0);
@@ -135,9 +181,7 @@ __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, cons
         v = make_uint4(w[0], w[1], w[2], w[3]);
       }
     }
-    uint2 *dst = reinterpret_cast<uint2 *>(lds + hv * a.row + piece * 16);
-    dst[0] = make_uint2(v.x, v.y);  // rows are 8-byte aligned (odd pitch in
-    dst[1] = make_uint2(v.z, v.w);  // 8-byte units keeps reads conflict-free)
+    *reinterpret_cast<uint4 *>(lds + hv * a.row + piece * 16) = v;  // rows are 16-byte multiples
   }
 }
 
@@ -167,10 +211,8 @@ struct Stager {
       int v = -2;
       if (idx < total) {
         const int hv = idx >> shift;
-        const int xw = hv % a.hw;
-        const int rest = hv / a.hw;
-        const int xh = rest % a.hh;
-        const int xt = rest / a.hh;
+        const DivMod x = divmod(hv, a.hw), y = divmod(x.q, a.hh);
+        const int xw = x.r, xh = y.r, xt = y.q;
         const int zt = b.zt0 + xt, zh = b.zh0 + xh, zw = b.zw0 + xw;
         v = (zt >= 0 && zt < a.t && zh >= 0 && zh < a.h && zw >= 0 && zw < a.w)
                 ? ((b.nb * a.t + zt) * a.h + zh) * a.w + zw
@@ -216,9 +258,7 @@ struct Stager {
     for (int k = 0; k < MAXI; ++k) {
       const int idx = threadIdx.x + k * blockDim.x;
       if (vox[k] != -2) {
-        uint2 *dst = reinterpret_cast<uint2 *>(lds + (idx >> shift) * a.row + (idx & (ppr - 1)) * 16);
-        dst[0] = make_uint2(d[k].x, d[k].y);
-        dst[1] = make_uint2(d[k].z, d[k].w);
+        *reinterpret_cast<uint4 *>(lds + (idx >> shift) * a.row + (idx & (ppr - 1)) * 16) = d[k];
       }
     }
   }
@@ -233,9 +273,9 @@ template <typename T>
 __device__ __forceinline__ float to_f32(T v) { return static_cast<float>(v); }
 
 // Channel chunks handled by this workgroup's split.
-__device__ __forceinline__ void split_range(const ConvArgs &a, int &ch0, int &ch1) {
-  ch0 = static_cast<int>((static_cast<long>(blockIdx.z) * a.nchunks) / a.splits);
-  ch1 = static_cast<int>((static_cast<long>(blockIdx.z + 1) * a.nchunks) / a.splits);
+__device__ __forceinline__ void split_range(const ConvArgs &a, int split, int &ch0, int &ch1) {
+  ch0 = static_cast<int>((static_cast<long>(split) * a.nchunks) / a.splits);
+  ch1 = static_cast<int>((static_cast<long>(split + 1) * a.nchunks) / a.splits);
 }
 
 // ---------------------------------------------------------------------------
@@ -309,10 +349,10 @@ __device__ __forceinline__ float4 max4(float4 x, float4 y) {
 struct BoxIter {
   int t, h, w;
   __device__ __forceinline__ void init(int slot, int bh, int bw) {
-    const int plane = bh * bw;
-    t = slot / plane;
-    h = (slot - t * plane) / bw;
-    w = slot - t * plane - h * bw;
+    const DivMod x = divmod(slot, bh * bw), y = divmod(x.r, bw);
+    t = x.q;
+    h = y.q;
+    w = y.r;
   }
   __device__ __forceinline__ void advance(int step, int bh, int bw) {
     w += step;
@@ -320,6 +360,16 @@ struct BoxIter {
     while (h >= bh) { h -= bh; ++t; }
   }
 };
+
+// Split-K partial of four consecutive filters of one voxel slot, stored
+// straight from the accumulator registers (the reduction pass applies the
+// epilogue, so no LDS tile is needed).
+__device__ __forceinline__ void put_partial(const ConvArgs &a, const Brick &b, int slot, int m0,
+                                            int split, const f32x4 &v) {
+  const Slot sl = decode_slot(a, b, slot);
+  if (!sl.valid || m0 >= a.c_out) return;
+  *reinterpret_cast<f32x4 *>(a.ws + (static_cast<long>(split) * a.total_vox + sl.out) * a.c_out4 + m0) = v;
+}
 
 template <typename T>
 __device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, const uint8_t *lds,
@@ -332,19 +382,6 @@ __device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, co
   const int m0 = m_wg0 + 4 * c4;
   const bool live = m0 < a.c_out;
   const uint8_t *col = lds + c4 * 16;
-  if (a.splits > 1) {
-    const int nslots = a.bt * a.bh * a.bw;
-    BoxIter it;
-    int slot = threadIdx.x / cg;
-    it.init(slot, a.bh, a.bw);
-    for (; slot < nslots; slot += step, it.advance(step, a.bh, a.bw)) {
-      if (!live || b.ot0 + it.t >= a.to || b.oh0 + it.h >= a.ho || b.ow0 + it.w >= a.wo) continue;
-      const long vox = ((static_cast<long>(b.nb) * a.to + b.ot0 + it.t) * a.ho + b.oh0 + it.h) * a.wo + b.ow0 + it.w;
-      const float4 v = *reinterpret_cast<const float4 *>(col + slot * a.tile_row);
-      *reinterpret_cast<float4 *>(a.ws + (static_cast<long>(blockIdx.z) * a.total_vox + vox) * a.c_out4 + m0) = v;
-    }
-    return;
-  }
   const int pbt = a.bt / a.qt, pbh = a.bh / a.qh, pbw = a.bw / a.qw;
   const int npslots = pbt * pbh * pbw;
   BoxIter it;
@@ -379,9 +416,9 @@ __device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, co
 // for its voxel n, and the A stream is stored in exactly that lane order.
 //
 // The waves of a workgroup share one brick; wave w computes wave tile
-// blockIdx.y*wpw + w: 16*MFW filters x 16*NF voxel slots.  blockIdx.z
-// selects a range of channel chunks (split-K) when the layer alone cannot
-// fill the GPU.  Dense layers give every wave tile the
+// tg*wpw + w: 16*MFW filters x 16*NF voxel slots.  The split index selects
+// a range of channel chunks (split-K) when the layer alone cannot fill the
+// GPU.  Dense layers give every wave tile the
 // full item list (and MFW > 1 shares each B fragment across filter rows);
 // KGS layers give each 16-filter tile the union of the items its four kernel
 // groups keep, with the pruned entries of that union stored as zero weights.
@@ -397,9 +434,10 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
   extern __shared__ __align__(16) uint8_t lds[];
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
-  const int wt = uniform(static_cast<int>(blockIdx.y) * a.wpw + (static_cast<int>(threadIdx.x) >> 6));
+  const Wg wg = decode_wg(a);
+  const int wt = uniform(wg.tg * a.wpw + (static_cast<int>(threadIdx.x) >> 6));
   const bool active = wt < a.wave_tiles;
-  const Brick b = decode_brick(a);
+  const Brick b = decode_brick(a, wg.brick);
 
   int vb[NF];
   #pragma unroll
@@ -448,7 +486,7 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
   };
 
   int ch0, ch1;
-  split_range(a, ch0, ch1);
+  split_range(a, wg.split, ch0, ch1);
   Stager<2, 8> st;
   st.init(a, b);
   if (st.ok && ch0 < ch1) st.issue(a, ch0 * a.cc);
@@ -495,7 +533,16 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
       }
     });
   }
-  const int m_wg0 = static_cast<int>(blockIdx.y) * a.wpw * 16 * MFW;
+  if (a.splits > 1) {
+    if (active)
+#pragma unroll
+      for (int j = 0; j < NF; ++j)
+#pragma unroll
+        for (int i = 0; i < MFW; ++i)
+          put_partial(a, b, 16 * j + (lane & 15), wt * 16 * MFW + 16 * i + 4 * g, wg.split, acc[i][j]);
+    return;
+  }
+  const int m_wg0 = wg.tg * a.wpw * 16 * MFW;
   __syncthreads();  // the halo is no longer needed: reuse LDS for the tile
   if (active) {
 #pragma unroll
@@ -523,9 +570,10 @@ __global__ __launch_bounds__(256) void items_f32_kernel(ConvArgs a) {
   extern __shared__ __align__(16) uint8_t lds[];
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
-  const int wt = uniform(static_cast<int>(blockIdx.y) * a.wpw + (static_cast<int>(threadIdx.x) >> 6));
+  const Wg wg = decode_wg(a);
+  const int wt = uniform(wg.tg * a.wpw + (static_cast<int>(threadIdx.x) >> 6));
   const bool active = wt < a.wave_tiles;
-  const Brick b = decode_brick(a);
+  const Brick b = decode_brick(a, wg.brick);
 
   int vb[NF];
   #pragma unroll
@@ -567,7 +615,7 @@ __global__ __launch_bounds__(256) void items_f32_kernel(ConvArgs a) {
   };
 
   int ch0, ch1;
-  split_range(a, ch0, ch1);
+  split_range(a, wg.split, ch0, ch1);
   Stager<4, 8> st;
   st.init(a, b);
   if (st.ok && ch0 < ch1) st.issue(a, ch0 * a.cc);
@@ -597,7 +645,16 @@ __global__ __launch_bounds__(256) void items_f32_kernel(ConvArgs a) {
       if (s + D < s_end) compute(D);
     });
   }
-  const int m_wg0 = static_cast<int>(blockIdx.y) * a.wpw * 16 * MFW;
+  if (a.splits > 1) {
+    if (active)
+#pragma unroll
+      for (int j = 0; j < NF; ++j)
+#pragma unroll
+        for (int i = 0; i < MFW; ++i)
+          put_partial(a, b, 16 * j + (lane & 15), wt * 16 * MFW + 16 * i + 4 * g, wg.split, acc[i][j]);
+    return;
+  }
+  const int m_wg0 = wg.tg * a.wpw * 16 * MFW;
   __syncthreads();  // the halo is no longer needed: reuse LDS for the tile
   if (active) {
 #pragma unroll
@@ -635,9 +692,10 @@ template <int SUB>
 __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
   extern __shared__ __align__(16) uint8_t lds[];
   const int lane = threadIdx.x & 63;
-  const int wt = uniform(static_cast<int>(blockIdx.y) * a.wpw + (static_cast<int>(threadIdx.x) >> 6));
+  const Wg wg = decode_wg(a);
+  const int wt = uniform(wg.tg * a.wpw + (static_cast<int>(threadIdx.x) >> 6));
   const bool active = wt < a.wave_tiles;
-  const Brick b = decode_brick(a);
+  const Brick b = decode_brick(a, wg.brick);
 
   int vb[SUB];
   #pragma unroll
@@ -653,7 +711,7 @@ __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
   const float *A = static_cast<const float *>(a.a);
 
   int ch0, ch1;
-  split_range(a, ch0, ch1);
+  split_range(a, wg.split, ch0, ch1);
   Stager<4, 8> st;
   st.init(a, b);
   if (st.ok && ch0 < ch1) st.issue(a, ch0 * a.cc);
@@ -686,7 +744,16 @@ __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
       });
     }
   }
-  const int m_wg0 = static_cast<int>(blockIdx.y) * a.wpw * 16;
+  if (a.splits > 1) {
+    if (active)
+#pragma unroll
+      for (int sb = 0; sb < SUB; ++sb)
+#pragma unroll
+        for (int gi = 0; gi < 4; ++gi)
+          put_partial(a, b, 64 * sb + lane, wt * 16 + 4 * gi, wg.split, acc[gi][sb]);
+    return;
+  }
+  const int m_wg0 = wg.tg * a.wpw * 16;
   __syncthreads();  // the halo is no longer needed: reuse LDS for the tile
   if (active) {
 #pragma unroll
@@ -706,35 +773,82 @@ __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
 // (+ residual)).  Fixed summation order keeps results run-to-run identical.
 // ---------------------------------------------------------------------------
 
+// Sum of the split partials of one voxel and four filters, added in split
+// order (so the result does not depend on scheduling); four loads are in
+// flight at a time.
+__device__ __forceinline__ float4 sum_splits(const ConvArgs &a, long vox, int m0) {
+  const float *p = a.ws + vox * a.c_out4 + m0;
+  const long zstride = a.total_vox * a.c_out4;
+  float4 acc = *reinterpret_cast<const float4 *>(p);
+  for (int z = 1; z < a.splits; z += 4) {
+    float4 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      v[k] = z + k < a.splits ? *reinterpret_cast<const float4 *>(p + (z + k) * zstride)
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (z + k < a.splits) {
+        acc.x += v[k].x; acc.y += v[k].y; acc.z += v[k].z; acc.w += v[k].w;
+      }
+  }
+  return acc;
+}
+
+// Split reduction + epilogue (+ fused max-pool).  When the pool window has
+// win = 2, 4, 8, ... elements, the win voxels of a window go to win adjacent
+// lanes and the max is taken across lanes; any other window is walked by one
+// thread.
 template <typename T>
 __global__ __launch_bounds__(256) void reduce_splits_kernel(ConvArgs a) {
   const int groups = a.c_out4 >> 2;
   const long pvox_total = static_cast<long>(a.n) * a.pto * a.pho * a.pwo;
-  const long total = pvox_total * groups;
-  for (long idx = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
-       idx += static_cast<long>(gridDim.x) * blockDim.x) {
-    const long pv = idx / groups;
-    const int m0 = static_cast<int>(idx - pv * groups) * 4;
+  const int win = a.qt * a.qh * a.qw;
+  const bool lanes = win > 1 && win <= 64 && (win & (win - 1)) == 0;
+  const int wl = lanes ? win : 1;                 // lanes per output
+  const long total = pvox_total * groups * wl;     // a multiple of wl: no window straddles waves
+  const long stride = static_cast<long>(gridDim.x) * blockDim.x;
+  for (long base = static_cast<long>(blockIdx.x) * blockDim.x; base < total; base += stride) {
+    const long idx = base + threadIdx.x;
+    const bool live = idx < total;
+    const long o = live ? idx / wl : 0;
+    const int e = static_cast<int>(idx - (idx / wl) * wl);
+    const long pv = o / groups;
+    const int m0 = static_cast<int>(o - pv * groups) * 4;
     const int gw = static_cast<int>(pv % a.pwo);
     long r = pv / a.pwo;
     const int gh = static_cast<int>(r % a.pho);
     r /= a.pho;
     const int gt = static_cast<int>(r % a.pto);
     const long nb = r / a.pto;
-    float4 best = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int dt = 0; dt < a.qt; ++dt)
-      for (int dh = 0; dh < a.qh; ++dh)
-        for (int dw = 0; dw < a.qw; ++dw) {
-          const long vox = ((nb * a.to + gt * a.qt + dt) * a.ho + gh * a.qh + dh) * a.wo + gw * a.qw + dw;
-          float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-          for (int z = 0; z < a.splits; ++z) {
-            const float4 v = *reinterpret_cast<const float4 *>(a.ws + (static_cast<long>(z) * a.total_vox + vox) * a.c_out4 + m0);
-            acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-          }
-          const float4 v = activate4<T>(a, vox, m0, acc);
-          best = (dt | dh | dw) ? max4(best, v) : v;
-        }
-    if (m0 < a.c_out) put4<T>(a, pv, m0, best);
+    auto voxel = [&](int dt, int dh, int dw) {
+      return ((nb * a.to + gt * a.qt + dt) * a.ho + gh * a.qh + dh) * a.wo + gw * a.qw + dw;
+    };
+    float4 best;
+    if (lanes) {
+      const int dw = e % a.qw, dh = (e / a.qw) % a.qh, dt = e / (a.qw * a.qh);
+      const long vox = voxel(dt, dh, dw);
+      best = live ? activate4<T>(a, vox, m0, sum_splits(a, vox, m0)) : make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int off = 1; off < wl; off <<= 1) {
+        float4 oth;
+        oth.x = __shfl_xor(best.x, off);
+        oth.y = __shfl_xor(best.y, off);
+        oth.z = __shfl_xor(best.z, off);
+        oth.w = __shfl_xor(best.w, off);
+        best = max4(best, oth);
+      }
+    } else {
+      best = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (live)
+        for (int dt = 0; dt < a.qt; ++dt)
+          for (int dh = 0; dh < a.qh; ++dh)
+            for (int dw = 0; dw < a.qw; ++dw) {
+              const long vox = voxel(dt, dh, dw);
+              const float4 v = activate4<T>(a, vox, m0, sum_splits(a, vox, m0));
+              best = (dt | dh | dw) ? max4(best, v) : v;
+            }
+    }
+    if (live && e == 0 && m0 < a.c_out) put4<T>(a, pv, m0, best);
   }
 }
 
@@ -779,30 +893,72 @@ __global__ __launch_bounds__(256) void maxpool_kernel(const T *__restrict__ x, T
 
 size_t halo_bytes(const ConvArgs &a) {
   const size_t halo = static_cast<size_t>(a.ht) * a.hh * a.hw * a.row;
+  if (a.splits > 1) return halo;  // partials are stored from registers
   const size_t tile = static_cast<size_t>(128) * a.tile_row;  // epilogue tile: 128 voxel slots
   return halo > tile ? halo : tile;
+}
+
+// Raise the kernel's dynamic LDS limit to the whole 160 KB once.
+template <typename K>
+hipError_t prepare(K kernel) {
+  static std::atomic<bool> done{false};
+  if (done.load(std::memory_order_acquire)) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  if (e == hipSuccess) done.store(true, std::memory_order_release);
+  return e;
 }
 
 template <typename K>
 int launch_conv(K kernel, const ConvArgs &a, void *stream) {
   const size_t lds = halo_bytes(a);
-  static bool attr_done = false;
-  if (!attr_done) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return e;
-    attr_done = true;
-  }
-  const long blocks_x = static_cast<long>(a.n) * a.nbt * a.nbh * a.nbw;
-  const int blocks_y = (a.wave_tiles + a.wpw - 1) / a.wpw;
-  if (blocks_x == 0 || blocks_y == 0) return hipSuccess;
-  dim3 grid(static_cast<unsigned>(blocks_x), static_cast<unsigned>(blocks_y),
-            static_cast<unsigned>(a.splits));
+  const hipError_t e = prepare(kernel);
+  if (e != hipSuccess) return e;
+  const long blocks = static_cast<long>(a.nbricks) * a.ntg * a.splits;
+  if (blocks == 0) return hipSuccess;
+  dim3 grid(static_cast<unsigned>(blocks));
   hipLaunchKernelGGL(kernel, grid, dim3(64 * a.wpw), lds, static_cast<hipStream_t>(stream), a);
   return hipGetLastError();
 }
 
+// Resident workgroups per CU for a kernel at an LDS size (0 when unknown).
+template <typename K>
+int resident(K kernel, size_t lds) {
+  if (prepare(kernel) != hipSuccess) return 0;
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void *>(kernel), 256,
+                                                   lds) != hipSuccess)
+    return 0;
+  return n;
+}
+
 }  // namespace
+
+int conv_resident(int variant, int dtype, int mfw, size_t lds) {
+  switch (variant) {
+    case kVarDenseItems16:
+    case kVarKgsUnion16:
+      if (dtype == RT3D_BF16) {
+        if (mfw == 1) return resident(items16_kernel<__bf16, 1, 8>, lds);
+        if (mfw == 2) return resident(items16_kernel<__bf16, 2, 8>, lds);
+        if (mfw == 4) return resident(items16_kernel<__bf16, 4, 8>, lds);
+      } else {
+        if (mfw == 1) return resident(items16_kernel<_Float16, 1, 8>, lds);
+        if (mfw == 2) return resident(items16_kernel<_Float16, 2, 8>, lds);
+        if (mfw == 4) return resident(items16_kernel<_Float16, 4, 8>, lds);
+      }
+      return 0;
+    case kVarDenseItemsF32:
+      if (mfw == 1) return resident(items_f32_kernel<1, 8>, lds);
+      if (mfw == 2) return resident(items_f32_kernel<2, 8>, lds);
+      if (mfw == 4) return resident(items_f32_kernel<4, 8>, lds);
+      return 0;
+    case kVarKgsExactF32:
+      return resident(kgs_exact_f32_kernel<2>, lds);
+    default:
+      return 0;
+  }
+}
 
 int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream) {
   if (dtype == RT3D_BF16) {
@@ -825,7 +981,9 @@ int launch_items_f32(const ConvArgs &a, int mfw, void *stream) {
 }
 
 int launch_reduce_splits(const ConvArgs &a, int dtype, void *stream) {
-  const long total = static_cast<long>(a.n) * a.pto * a.pho * a.pwo * (a.c_out4 / 4);
+  const int win = a.qt * a.qh * a.qw;
+  const int wl = win > 1 && win <= 64 && (win & (win - 1)) == 0 ? win : 1;  // as in the kernel
+  const long total = static_cast<long>(a.n) * a.pto * a.pho * a.pwo * (a.c_out4 / 4) * wl;
   if (total == 0) return hipSuccess;
   long blocks = (total + 255) / 256;
   if (blocks > 65536) blocks = 65536;

@@ -171,6 +171,8 @@ POOLED = [
     ("pe", 1, 256, 128, (4, 6, 6), (2, 2, 2), "bf16", True, False),   # split-K + pooled reduce
     ("pf", 1, 256, 128, (4, 6, 6), (2, 2, 2), "f32", False, True),
     ("pg", 1, 3, 64, (2, 16, 16), (1, 2, 2), "bf16", False, False),   # conv1-like
+    ("ph", 1, 128, 64, (3, 9, 9), (1, 3, 3), "bf16", True, False),    # 9-voxel window, split-K
+    ("pi", 1, 96, 40, (6, 5, 5), (3, 1, 1), "f16", True, True),       # 3-voxel window, residual
 ]
 
 
