@@ -55,15 +55,10 @@ struct DivMod {
 
 __device__ __forceinline__ DivMod divmod(int n, int d) {
   int q = static_cast<int>(static_cast<float>(n) * __builtin_amdgcn_rcpf(static_cast<float>(d)));
-  int r = n - q * d;
-  if (r < 0) {
-    --q;
-    r += d;
-  } else if (r >= d) {
-    ++q;
-    r -= d;
-  }
-  return {q, r};
+  const int r0 = n - q * d;
+  const int fix = (r0 >= d ? 1 : 0) - (r0 < 0 ? 1 : 0);  // selects, no branches
+  q += fix;
+  return {q, r0 - fix * d};
 }
 
 // ---------------------------------------------------------------------------
@@ -289,19 +284,27 @@ __device__ __forceinline__ void split_range(const ConvArgs &a, int split, int &c
 // ---------------------------------------------------------------------------
 
 // act(acc + bias (+ residual)) for filters m0..m0+3 of unpooled voxel vox.
-template <typename T>
-__device__ __forceinline__ float4 activate4(const ConvArgs &a, long vox, int m0, float4 v) {
-  float r[4] = {v.x, v.y, v.z, v.w};
-  const bool full = (a.c_out & 3) == 0;
-  if (a.bias) {
-    if (full) {
+// Bias of filters m0..m0+3 (zero where absent).  Loaded once per thread and
+// output column, outside the voxel loops.
+__device__ __forceinline__ float4 load_bias4(const ConvArgs &a, int m0) {
+  float r[4] = {0.f, 0.f, 0.f, 0.f};
+  if (a.bias && m0 < a.c_out) {
+    if ((a.c_out & 3) == 0) {
       const float4 bb = *reinterpret_cast<const float4 *>(a.bias + m0);
-      r[0] += bb.x; r[1] += bb.y; r[2] += bb.z; r[3] += bb.w;
+      r[0] = bb.x; r[1] = bb.y; r[2] = bb.z; r[3] = bb.w;
     } else {
       for (int q = 0; q < 4; ++q)
-        if (m0 + q < a.c_out) r[q] += a.bias[m0 + q];
+        if (m0 + q < a.c_out) r[q] = a.bias[m0 + q];
     }
   }
+  return make_float4(r[0], r[1], r[2], r[3]);
+}
+
+template <typename T>
+__device__ __forceinline__ float4 activate4(const ConvArgs &a, long vox, int m0, float4 v,
+                                            float4 bb) {
+  float r[4] = {v.x + bb.x, v.y + bb.y, v.z + bb.z, v.w + bb.w};
+  const bool full = (a.c_out & 3) == 0;
   if (a.res) {
     const T *res = static_cast<const T *>(a.res) + vox * a.c_out + m0;
     if (full && sizeof(T) == 4) {
@@ -381,6 +384,7 @@ __device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, co
   const int c4 = threadIdx.x % cg;
   const int m0 = m_wg0 + 4 * c4;
   const bool live = m0 < a.c_out;
+  const float4 bb = load_bias4(a, m0);
   const uint8_t *col = lds + c4 * 16;
   const int pbt = a.bt / a.qt, pbh = a.bh / a.qh, pbw = a.bw / a.qw;
   const int npslots = pbt * pbh * pbw;
@@ -398,7 +402,7 @@ __device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, co
           const int slot = (tt * a.bh + hh) * a.bw + ww;
           const long vox = ((static_cast<long>(b.nb) * a.to + b.ot0 + tt) * a.ho + b.oh0 + hh) * a.wo + b.ow0 + ww;
           const float4 acc = *reinterpret_cast<const float4 *>(col + slot * a.tile_row);
-          const float4 v = activate4<T>(a, vox, m0, acc);
+          const float4 v = activate4<T>(a, vox, m0, acc, bb);
           best = (dt | dh | dw) ? max4(best, v) : v;
         }
     const long pvox = ((static_cast<long>(b.nb) * a.pto + gt) * a.pho + gh) * a.pwo + gw;
@@ -487,26 +491,34 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
 
   int ch0, ch1;
   split_range(a, wg.split, ch0, ch1);
+  // The wave's steps over all chunks of its split form one stream
+  // [S0, S1): item offsets and A are prefetched along it straight across
+  // chunk boundaries (indices clamped to the last step: a harmless re-read,
+  // so the loop body stays straight-line and the wait counters exact).
+  // Only the B fragments wait for a new chunk to reach LDS.
+  const uint32_t S0 = uniform(sp[ch0]), S1 = uniform(sp[ch1]);
+  const bool work = active && S1 > S0;
+  const uint32_t LAST = work ? S1 - 1 : S0;
   Stager<2, 8> st;
   st.init(a, b);
   if (st.ok && ch0 < ch1) st.issue(a, ch0 * a.cc);
+  if (work) {
+#pragma unroll
+    for (int d = 0; d < 4; ++d) fetch_off(d, min(S0 + d, LAST));
+#pragma unroll
+    for (int d = 0; d < 2; ++d) fetch_a(d, min(S0 + d, LAST));
+  }
   for (int ch = ch0; ch < ch1; ++ch) {
     __syncthreads();  // every wave is done with the previous chunk
     if (st.ok) st.commit(lds, a);
     else stage_halo<2>(lds, a, b, ch * a.cc);
     __syncthreads();
     if (st.ok && ch + 1 < ch1) st.issue(a, (ch + 1) * a.cc);  // overlaps this chunk's MFMAs
-    if (!active) continue;
+    if (!work) continue;
     const uint32_t s_beg = uniform(sp[ch]), s_end = uniform(sp[ch + 1]);
     if (s_beg == s_end) continue;
-    const uint32_t last = s_end - 1;
-    // Every fetch is unconditional (indices clamped to the last step: a
-    // harmless re-read) so the loop body is straight-line and the memory
-    // wait counters stay exact.
-    #pragma unroll
-    for (int d = 0; d < 4; ++d) fetch_off(d, min(s_beg + d, last));
-    #pragma unroll
-    for (int d = 0; d < 2; ++d) fetch_a(d, min(s_beg + d, last));
+    // Ring slots are relative to the chunk's first step: offsets slot i&3,
+    // A slot i&1, B slot i&1 for local step i.
     load_b(0, roff[0]);
     uint32_t s = s_beg;
     for (; s + 4 <= s_end; s += 4) {
@@ -514,24 +526,41 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
         constexpr int D = decltype(dc)::value;
         load_b((D + 1) & 1, roff[(D + 1) & 3]);
         mma(D & 1);
-        fetch_a(D & 1, min(s + D + 2, last));
-        fetch_off(D, min(s + D + 4, last));
+        fetch_a(D & 1, min(s + D + 2, LAST));
+        fetch_off(D, min(s + D + 4, LAST));
         // Keep the stages in place: without this fence the scheduler sinks
         // the prefetches next to their uses two steps later.
         __builtin_amdgcn_sched_barrier(0);
       });
     }
-    // Tail: 0..3 steps.  Step s+D uses A slot D&1 (refilled two steps
-    // ahead as in the main loop), B slot D&1 and offset slot D.
-    const uint32_t rem = s_end - s;
+    const uint32_t rem = s_end - s;  // tail: 0..3 steps
     static_for<3>([&](auto dc) {
       constexpr int D = decltype(dc)::value;
       if (D < rem) {
         if (D + 1 < rem) load_b((D + 1) & 1, roff[(D + 1) & 3]);
         mma(D & 1);
-        if (D + 2 < rem) fetch_a(D & 1, s + D + 2);
+        fetch_a(D & 1, min(s + D + 2, LAST));
+        fetch_off(D, min(s + D + 4, LAST));
       }
     });
+    // The rings now hold steps s_end.. at slots (n + k) & 3 and (n + k) & 1
+    // (n = steps of this chunk): rotate them to slot 0 for the next chunk.
+    const uint32_t n = s_end - s_beg;
+    const uint2 o0 = roff[0], o1 = roff[1], o2 = roff[2], o3 = roff[3];
+    switch (n & 3) {
+      case 1: roff[0] = o1; roff[1] = o2; roff[2] = o3; roff[3] = o0; break;
+      case 2: roff[0] = o2; roff[1] = o3; roff[2] = o0; roff[3] = o1; break;
+      case 3: roff[0] = o3; roff[1] = o0; roff[2] = o1; roff[3] = o2; break;
+      default: break;
+    }
+    if (n & 1) {
+#pragma unroll
+      for (int i = 0; i < MFW; ++i) {
+        const V8 t = ra[0][i];
+        ra[0][i] = ra[1][i];
+        ra[1][i] = t;
+      }
+    }
   }
   if (a.splits > 1) {
     if (active)
@@ -828,7 +857,8 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(ConvArgs a) {
     if (lanes) {
       const int dw = e % a.qw, dh = (e / a.qw) % a.qh, dt = e / (a.qw * a.qh);
       const long vox = voxel(dt, dh, dw);
-      best = live ? activate4<T>(a, vox, m0, sum_splits(a, vox, m0)) : make_float4(0.f, 0.f, 0.f, 0.f);
+      best = live ? activate4<T>(a, vox, m0, sum_splits(a, vox, m0), load_bias4(a, m0))
+                  : make_float4(0.f, 0.f, 0.f, 0.f);
       for (int off = 1; off < wl; off <<= 1) {
         float4 oth;
         oth.x = __shfl_xor(best.x, off);
@@ -839,12 +869,13 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(ConvArgs a) {
       }
     } else {
       best = make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 bb = live ? load_bias4(a, m0) : best;
       if (live)
         for (int dt = 0; dt < a.qt; ++dt)
           for (int dh = 0; dh < a.qh; ++dh)
             for (int dw = 0; dw < a.qw; ++dw) {
               const long vox = voxel(dt, dh, dw);
-              const float4 v = activate4<T>(a, vox, m0, sum_splits(a, vox, m0));
+              const float4 v = activate4<T>(a, vox, m0, sum_splits(a, vox, m0), bb);
               best = (dt | dh | dw) ? max4(best, v) : v;
             }
     }
