@@ -839,7 +839,11 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   a.order = launch.order;
   a.nbricks = static_cast<int32_t>(static_cast<long>(a.n) * a.nbt * a.nbh * a.nbw);
   a.ntg = (a.wave_tiles + a.wpw - 1) / a.wpw;
-  // The kernels divide workgroup ids with a 24-bit reciprocal method.
+  a.grid = 0;  // one workgroup per tile
+  // The kernels divide workgroup ids and (pooled) voxel indices with a
+  // 24-bit reciprocal method.
+  if (a.total_vox >= (1L << 24))
+    return fail(RT3D_ERR_UNSUPPORTED, "2^24 or more output voxels per launch");
   if (static_cast<long>(a.n) * a.nbt * a.nbh * a.nbw * a.ntg * a.splits >= (1L << 24))
     return fail(RT3D_ERR_UNSUPPORTED, "layer needs 2^24 or more workgroups");
   int e;

@@ -77,6 +77,8 @@ struct ConvArgs {
   int32_t tile_row;   // LDS bytes per voxel slot of the epilogue tile
   int32_t nbricks;    // n * nbt * nbh * nbw
   int32_t ntg;        // workgroups along the filters: ceil(wave_tiles / wpw)
+  int32_t grid;       // workgroups launched (0: one per tile); fewer loop over tiles
+  int32_t pad1;
 };
 
 // Launch shape chosen at forward time from the batch size.

@@ -80,12 +80,8 @@ struct Wg {
   int brick, tg, split;
 };
 
-__device__ __forceinline__ Wg decode_wg(const ConvArgs &a) {
-  const int nw = a.nbricks * a.ntg * a.splits;
-  const int id = static_cast<int>(blockIdx.x);
-  const int q = nw >> 3, r = nw & 7;
-  const int xcd = id & 7, local = id >> 3;
-  const int lid = xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
+// Logical tile id -> (brick, filter tile group, split).
+__device__ __forceinline__ Wg decode_tile(const ConvArgs &a, int lid) {
   Wg g;
   if (a.order == 0) {
     const DivMod x = divmod(lid, a.nbricks), y = divmod(x.q, a.ntg);
@@ -102,6 +98,18 @@ __device__ __forceinline__ Wg decode_wg(const ConvArgs &a) {
   g.tg = uniform(g.tg);
   g.split = uniform(g.split);
   return g;
+}
+
+// Logical id of this workgroup's tile in a one-tile-per-workgroup grid.
+__device__ __forceinline__ int xcd_remap(int nw) {
+  const int id = static_cast<int>(blockIdx.x);
+  const int q = nw >> 3, r = nw & 7;
+  const int xcd = id & 7, local = id >> 3;
+  return xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
+}
+
+__device__ __forceinline__ Wg decode_wg(const ConvArgs &a) {
+  return decode_tile(a, xcd_remap(a.nbricks * a.ntg * a.splits));
 }
 
 __device__ __forceinline__ Brick decode_brick(const ConvArgs &a, int brick) {
@@ -126,9 +134,7 @@ struct Slot {
   bool valid;
 };
 
-__device__ __forceinline__ Slot decode_slot(const ConvArgs &a, const Brick &b, int s) {
-  const DivMod x = divmod(s, a.bh * a.bw), y = divmod(x.r, a.bw);
-  int tt = x.q, hh = y.q, ww = y.r;
+__device__ __forceinline__ Slot slot_at(const ConvArgs &a, const Brick &b, int tt, int hh, int ww) {
   Slot o;
   o.valid = tt < a.bt && b.ot0 + tt < a.to && b.oh0 + hh < a.ho && b.ow0 + ww < a.wo;
   if (!o.valid) tt = hh = ww = 0;
@@ -136,6 +142,33 @@ __device__ __forceinline__ Slot decode_slot(const ConvArgs &a, const Brick &b, i
   o.out = ((static_cast<long>(b.nb) * a.to + b.ot0 + tt) * a.ho + b.oh0 + hh) * a.wo + b.ow0 + ww;
   return o;
 }
+
+// (t, h, w) of voxel slots s, s + stride, s + 2*stride, ... of the brick:
+// one divmod pair to start, then carries only (VALU time in the prologue
+// and epilogue is otherwise dominated by divisions).
+struct SlotWalk {
+  int t, h, w, dt, dh, dw;
+  __device__ __forceinline__ void init(const ConvArgs &a, int s, int stride) {
+    const int plane = a.bh * a.bw;
+    const DivMod x = divmod(s, plane), y = divmod(x.r, a.bw);
+    t = x.q;
+    h = y.q;
+    w = y.r;
+    const DivMod p = divmod(stride, plane), q = divmod(p.r, a.bw);
+    dt = p.q;
+    dh = q.q;
+    dw = q.r;
+  }
+  __device__ __forceinline__ void next(const ConvArgs &a) {
+    w += dw;
+    const int cw = w >= a.bw ? 1 : 0;
+    w -= cw * a.bw;
+    h += dh + cw;
+    const int chh = h >= a.bh ? 1 : 0;
+    h -= chh * a.bh;
+    t += dt + chh;
+  }
+};
 
 // Stage channels [c0, c0 + cc) of the input brick plus halo into LDS.
 // Row r of the halo (one input voxel) holds cc channels, zero where the
@@ -200,20 +233,30 @@ struct Stager {
     shift = ppr == 4 ? 2 : (ppr == 2 ? 1 : 0);
     total = a.ht * a.hh * a.hw * ppr;
     ok = total <= MAXI * static_cast<int>(blockDim.x);
+    // Halo row of piece k: (threadIdx.x + k * blockDim.x) >> shift, walked
+    // with carries from one divmod pair (blockDim is a multiple of ppr).
+    const DivMod x = divmod(static_cast<int>(threadIdx.x) >> shift, a.hw), y = divmod(x.q, a.hh);
+    int xw = x.r, xh = y.r, xt = y.q;
+    const int rstep = static_cast<int>(blockDim.x) >> shift;
+    const DivMod sx = divmod(rstep, a.hw), sy = divmod(sx.q, a.hh);
 #pragma unroll
     for (int k = 0; k < MAXI; ++k) {
       const int idx = threadIdx.x + k * blockDim.x;
       int v = -2;
       if (idx < total) {
-        const int hv = idx >> shift;
-        const DivMod x = divmod(hv, a.hw), y = divmod(x.q, a.hh);
-        const int xw = x.r, xh = y.r, xt = y.q;
         const int zt = b.zt0 + xt, zh = b.zh0 + xh, zw = b.zw0 + xw;
         v = (zt >= 0 && zt < a.t && zh >= 0 && zh < a.h && zw >= 0 && zw < a.w)
                 ? ((b.nb * a.t + zt) * a.h + zh) * a.w + zw
                 : -1;
       }
       vox[k] = v;
+      xw += sx.r;
+      const int cw = xw >= a.hw ? 1 : 0;
+      xw -= cw * a.hw;
+      xh += sy.r + cw;
+      const int chh = xh >= a.hh ? 1 : 0;
+      xh -= chh * a.hh;
+      xt += sy.q + chh;
     }
   }
 
@@ -367,9 +410,8 @@ struct BoxIter {
 // Split-K partial of four consecutive filters of one voxel slot, stored
 // straight from the accumulator registers (the reduction pass applies the
 // epilogue, so no LDS tile is needed).
-__device__ __forceinline__ void put_partial(const ConvArgs &a, const Brick &b, int slot, int m0,
-                                            int split, const f32x4 &v) {
-  const Slot sl = decode_slot(a, b, slot);
+__device__ __forceinline__ void put_partial(const ConvArgs &a, const Slot &sl, int m0, int split,
+                                            const f32x4 &v) {
   if (!sl.valid || m0 >= a.c_out) return;
   *reinterpret_cast<f32x4 *>(a.ws + (static_cast<long>(split) * a.total_vox + sl.out) * a.c_out4 + m0) = v;
 }
@@ -444,8 +486,15 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
   const Brick b = decode_brick(a, wg.brick);
 
   int vb[NF];
-  #pragma unroll
-  for (int j = 0; j < NF; ++j) vb[j] = decode_slot(a, b, 16 * j + (lane & 15)).lds;
+  {
+    SlotWalk sw;
+    sw.init(a, lane & 15, 16);
+#pragma unroll
+    for (int j = 0; j < NF; ++j) {
+      vb[j] = slot_at(a, b, sw.t, sw.h, sw.w).lds;
+      sw.next(a);
+    }
+  }
 
   f32x4 acc[MFW][NF];
   #pragma unroll
@@ -563,12 +612,18 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
     }
   }
   if (a.splits > 1) {
-    if (active)
+    if (active) {
+      SlotWalk sw;
+      sw.init(a, lane & 15, 16);
 #pragma unroll
-      for (int j = 0; j < NF; ++j)
+      for (int j = 0; j < NF; ++j) {
+        const Slot sl = slot_at(a, b, sw.t, sw.h, sw.w);
+        sw.next(a);
 #pragma unroll
         for (int i = 0; i < MFW; ++i)
-          put_partial(a, b, 16 * j + (lane & 15), wt * 16 * MFW + 16 * i + 4 * g, wg.split, acc[i][j]);
+          put_partial(a, sl, wt * 16 * MFW + 16 * i + 4 * g, wg.split, acc[i][j]);
+      }
+    }
     return;
   }
   const int m_wg0 = wg.tg * a.wpw * 16 * MFW;
@@ -605,8 +660,15 @@ __global__ __launch_bounds__(256) void items_f32_kernel(ConvArgs a) {
   const Brick b = decode_brick(a, wg.brick);
 
   int vb[NF];
-  #pragma unroll
-  for (int j = 0; j < NF; ++j) vb[j] = decode_slot(a, b, 16 * j + (lane & 15)).lds;
+  {
+    SlotWalk sw;
+    sw.init(a, lane & 15, 16);
+#pragma unroll
+    for (int j = 0; j < NF; ++j) {
+      vb[j] = slot_at(a, b, sw.t, sw.h, sw.w).lds;
+      sw.next(a);
+    }
+  }
 
   f32x4 acc[MFW][NF];
   #pragma unroll
@@ -675,12 +737,18 @@ __global__ __launch_bounds__(256) void items_f32_kernel(ConvArgs a) {
     });
   }
   if (a.splits > 1) {
-    if (active)
+    if (active) {
+      SlotWalk sw;
+      sw.init(a, lane & 15, 16);
 #pragma unroll
-      for (int j = 0; j < NF; ++j)
+      for (int j = 0; j < NF; ++j) {
+        const Slot sl = slot_at(a, b, sw.t, sw.h, sw.w);
+        sw.next(a);
 #pragma unroll
         for (int i = 0; i < MFW; ++i)
-          put_partial(a, b, 16 * j + (lane & 15), wt * 16 * MFW + 16 * i + 4 * g, wg.split, acc[i][j]);
+          put_partial(a, sl, wt * 16 * MFW + 16 * i + 4 * g, wg.split, acc[i][j]);
+      }
+    }
     return;
   }
   const int m_wg0 = wg.tg * a.wpw * 16 * MFW;
@@ -727,8 +795,15 @@ __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
   const Brick b = decode_brick(a, wg.brick);
 
   int vb[SUB];
-  #pragma unroll
-  for (int s = 0; s < SUB; ++s) vb[s] = decode_slot(a, b, 64 * s + lane).lds;
+  {
+    SlotWalk sw;
+    sw.init(a, lane, 64);
+#pragma unroll
+    for (int s = 0; s < SUB; ++s) {
+      vb[s] = slot_at(a, b, sw.t, sw.h, sw.w).lds;
+      sw.next(a);
+    }
+  }
 
   f32x4 acc[4][SUB];
   #pragma unroll
@@ -774,12 +849,17 @@ __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
     }
   }
   if (a.splits > 1) {
-    if (active)
+    if (active) {
+      SlotWalk sw;
+      sw.init(a, lane, 64);
 #pragma unroll
-      for (int sb = 0; sb < SUB; ++sb)
+      for (int sb = 0; sb < SUB; ++sb) {
+        const Slot sl = slot_at(a, b, sw.t, sw.h, sw.w);
+        sw.next(a);
 #pragma unroll
-        for (int gi = 0; gi < 4; ++gi)
-          put_partial(a, b, 64 * sb + lane, wt * 16 + 4 * gi, wg.split, acc[gi][sb]);
+        for (int gi = 0; gi < 4; ++gi) put_partial(a, sl, wt * 16 + 4 * gi, wg.split, acc[gi][sb]);
+      }
+    }
     return;
   }
   const int m_wg0 = wg.tg * a.wpw * 16;
@@ -802,85 +882,101 @@ __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
 // (+ residual)).  Fixed summation order keeps results run-to-run identical.
 // ---------------------------------------------------------------------------
 
-// Sum of the split partials of one voxel and four filters, added in split
-// order (so the result does not depend on scheduling); four loads are in
-// flight at a time.
-__device__ __forceinline__ float4 sum_splits(const ConvArgs &a, long vox, int m0) {
-  const float *p = a.ws + vox * a.c_out4 + m0;
-  const long zstride = a.total_vox * a.c_out4;
-  float4 acc = *reinterpret_cast<const float4 *>(p);
-  for (int z = 1; z < a.splits; z += 4) {
-    float4 v[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      v[k] = z + k < a.splits ? *reinterpret_cast<const float4 *>(p + (z + k) * zstride)
-                              : make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      if (z + k < a.splits) {
-        acc.x += v[k].x; acc.y += v[k].y; acc.z += v[k].z; acc.w += v[k].w;
-      }
-  }
-  return acc;
+// Split reduction + epilogue (+ fused max-pool).  Each output (pooled voxel,
+// four filters) gets wl x zl adjacent lanes: wl = window voxels (when the
+// window has 2, 4, ... voxels; any other window is walked by one lane) and
+// zl = lanes sharing the splits (split z goes to lane z mod zl, at most four
+// per lane, all loads in flight together).  Lanes add their splits in
+// increasing order, combine across the zl lanes by an xor butterfly (a fixed
+// order, so every run gives the same bits), apply the epilogue per window
+// voxel, and take the max across the wl lanes.  A block covers vpb pooled
+// voxels x cpb filter quads; blockIdx.y picks the filter-quad range.
+__device__ __forceinline__ float4 add4(float4 x, float4 y) {
+  return make_float4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
 }
 
-// Split reduction + epilogue (+ fused max-pool).  When the pool window has
-// win = 2, 4, 8, ... elements, the win voxels of a window go to win adjacent
-// lanes and the max is taken across lanes; any other window is walked by one
-// thread.
+__device__ __forceinline__ float4 shfl_xor4(float4 v, int m) {
+  return make_float4(__shfl_xor(v.x, m), __shfl_xor(v.y, m), __shfl_xor(v.z, m),
+                     __shfl_xor(v.w, m));
+}
+
+struct ReduceShape {
+  int wl, zl, lpo, cpb, vpb, groups;
+};
+
+__host__ __device__ inline ReduceShape reduce_shape(const ConvArgs &a) {
+  ReduceShape r;
+  const int win = a.qt * a.qh * a.qw;
+  r.wl = win > 1 && win <= 16 && (win & (win - 1)) == 0 ? win : 1;
+  r.zl = 1;
+  while (r.zl * 4 < a.splits && r.zl * 2 * r.wl <= 16) r.zl *= 2;
+  r.lpo = r.wl * r.zl;  // divides 64
+  r.groups = a.c_out4 >> 2;
+  r.cpb = r.groups < 256 / r.lpo ? r.groups : 256 / r.lpo;
+  r.vpb = 256 / (r.cpb * r.lpo);
+  return r;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void reduce_splits_kernel(ConvArgs a) {
-  const int groups = a.c_out4 >> 2;
-  const long pvox_total = static_cast<long>(a.n) * a.pto * a.pho * a.pwo;
-  const int win = a.qt * a.qh * a.qw;
-  const bool lanes = win > 1 && win <= 64 && (win & (win - 1)) == 0;
-  const int wl = lanes ? win : 1;                 // lanes per output
-  const long total = pvox_total * groups * wl;     // a multiple of wl: no window straddles waves
-  const long stride = static_cast<long>(gridDim.x) * blockDim.x;
-  for (long base = static_cast<long>(blockIdx.x) * blockDim.x; base < total; base += stride) {
-    const long idx = base + threadIdx.x;
-    const bool live = idx < total;
-    const long o = live ? idx / wl : 0;
-    const int e = static_cast<int>(idx - (idx / wl) * wl);
-    const long pv = o / groups;
-    const int m0 = static_cast<int>(o - pv * groups) * 4;
-    const int gw = static_cast<int>(pv % a.pwo);
-    long r = pv / a.pwo;
-    const int gh = static_cast<int>(r % a.pho);
-    r /= a.pho;
-    const int gt = static_cast<int>(r % a.pto);
-    const long nb = r / a.pto;
-    auto voxel = [&](int dt, int dh, int dw) {
-      return ((nb * a.to + gt * a.qt + dt) * a.ho + gh * a.qh + dh) * a.wo + gw * a.qw + dw;
-    };
-    float4 best;
-    if (lanes) {
-      const int dw = e % a.qw, dh = (e / a.qw) % a.qh, dt = e / (a.qw * a.qh);
-      const long vox = voxel(dt, dh, dw);
-      best = live ? activate4<T>(a, vox, m0, sum_splits(a, vox, m0), load_bias4(a, m0))
-                  : make_float4(0.f, 0.f, 0.f, 0.f);
-      for (int off = 1; off < wl; off <<= 1) {
-        float4 oth;
-        oth.x = __shfl_xor(best.x, off);
-        oth.y = __shfl_xor(best.y, off);
-        oth.z = __shfl_xor(best.z, off);
-        oth.w = __shfl_xor(best.w, off);
-        best = max4(best, oth);
-      }
-    } else {
-      best = make_float4(0.f, 0.f, 0.f, 0.f);
-      const float4 bb = live ? load_bias4(a, m0) : best;
-      if (live)
-        for (int dt = 0; dt < a.qt; ++dt)
-          for (int dh = 0; dh < a.qh; ++dh)
-            for (int dw = 0; dw < a.qw; ++dw) {
-              const long vox = voxel(dt, dh, dw);
-              const float4 v = activate4<T>(a, vox, m0, sum_splits(a, vox, m0), bb);
-              best = (dt | dh | dw) ? max4(best, v) : v;
-            }
+  const ReduceShape rs = reduce_shape(a);
+  const int t = threadIdx.x;
+  const DivMod u = divmod(t, rs.lpo), w = divmod(u.q, rs.cpb);
+  const int z0 = u.r % rs.zl, e = u.r / rs.zl;
+  const int c4 = static_cast<int>(blockIdx.y) * rs.cpb + w.r;
+  const int pv = static_cast<int>(blockIdx.x) * rs.vpb + w.q;
+  const int pvox_total = a.n * a.pto * a.pho * a.pwo;
+  const bool live = w.q < rs.vpb && pv < pvox_total && c4 < rs.groups;
+  const int m0 = 4 * c4;
+  const DivMod x = divmod(live ? pv : 0, a.pwo), y = divmod(x.q, a.pho), z = divmod(y.q, a.pto);
+  const int gw = x.r, gh = y.r, gt = z.r, nb = z.q;
+  const long zstride = a.total_vox * a.c_out4;
+  auto voxel = [&](int dt, int dh, int dw) {
+    return ((static_cast<long>(nb) * a.to + gt * a.qt + dt) * a.ho + gh * a.qh + dh) * a.wo +
+           gw * a.qw + dw;
+  };
+  // This lane's share of the split sum of voxel vox: splits z0, z0 + zl, ...
+  auto partial = [&](long vox) {
+    const float *p = a.ws + vox * a.c_out4 + m0;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int zz = z0; zz < a.splits; zz += 4 * rs.zl) {
+      float4 v[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        v[k] = zz + k * rs.zl < a.splits
+                   ? *reinterpret_cast<const float4 *>(p + (zz + k * rs.zl) * zstride)
+                   : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (zz + k * rs.zl < a.splits) acc = add4(acc, v[k]);
     }
-    if (live && e == 0 && m0 < a.c_out) put4<T>(a, pv, m0, best);
+    return acc;
+  };
+  auto across_splits = [&](float4 v) {
+    for (int m = 1; m < rs.zl; m <<= 1) v = add4(v, shfl_xor4(v, m));
+    return v;
+  };
+  const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+  const float4 bb = live ? load_bias4(a, m0) : zero;
+  float4 best;
+  if (rs.wl > 1) {
+    const int dw = e % a.qw, dh = (e / a.qw) % a.qh, dt = e / (a.qw * a.qh);
+    const long vox = voxel(dt, dh, dw);
+    const float4 sum = across_splits(live ? partial(vox) : zero);
+    best = live ? activate4<T>(a, vox, m0, sum, bb) : zero;
+    for (int m = rs.zl; m < rs.lpo; m <<= 1) best = max4(best, shfl_xor4(best, m));
+  } else {
+    best = zero;
+    for (int dt = 0; dt < a.qt; ++dt)  // uniform trip counts: shuffles stay converged
+      for (int dh = 0; dh < a.qh; ++dh)
+        for (int dw = 0; dw < a.qw; ++dw) {
+          const long vox = voxel(dt, dh, dw);
+          const float4 sum = across_splits(live ? partial(vox) : zero);
+          const float4 v = live ? activate4<T>(a, vox, m0, sum, bb) : zero;
+          best = (dt | dh | dw) ? max4(best, v) : v;
+        }
   }
+  if (live && u.r == 0 && m0 < a.c_out) put4<T>(a, pv, m0, best);
 }
 
 // ---------------------------------------------------------------------------
@@ -945,7 +1041,7 @@ int launch_conv(K kernel, const ConvArgs &a, void *stream) {
   const size_t lds = halo_bytes(a);
   const hipError_t e = prepare(kernel);
   if (e != hipSuccess) return e;
-  const long blocks = static_cast<long>(a.nbricks) * a.ntg * a.splits;
+  const long blocks = a.grid > 0 ? a.grid : static_cast<long>(a.nbricks) * a.ntg * a.splits;
   if (blocks == 0) return hipSuccess;
   dim3 grid(static_cast<unsigned>(blocks));
   hipLaunchKernelGGL(kernel, grid, dim3(64 * a.wpw), lds, static_cast<hipStream_t>(stream), a);
@@ -1012,19 +1108,18 @@ int launch_items_f32(const ConvArgs &a, int mfw, void *stream) {
 }
 
 int launch_reduce_splits(const ConvArgs &a, int dtype, void *stream) {
-  const int win = a.qt * a.qh * a.qw;
-  const int wl = win > 1 && win <= 64 && (win & (win - 1)) == 0 ? win : 1;  // as in the kernel
-  const long total = static_cast<long>(a.n) * a.pto * a.pho * a.pwo * (a.c_out4 / 4) * wl;
-  if (total == 0) return hipSuccess;
-  long blocks = (total + 255) / 256;
-  if (blocks > 65536) blocks = 65536;
+  const ReduceShape rs = reduce_shape(a);
+  const long pvox = static_cast<long>(a.n) * a.pto * a.pho * a.pwo;
+  if (pvox == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>((pvox + rs.vpb - 1) / rs.vpb),
+                  static_cast<unsigned>((rs.groups + rs.cpb - 1) / rs.cpb));
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == RT3D_F32)
-    hipLaunchKernelGGL(reduce_splits_kernel<float>, dim3(blocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(reduce_splits_kernel<float>, grid, dim3(256), 0, s, a);
   else if (dtype == RT3D_BF16)
-    hipLaunchKernelGGL(reduce_splits_kernel<__bf16>, dim3(blocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(reduce_splits_kernel<__bf16>, grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(reduce_splits_kernel<_Float16>, dim3(blocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(reduce_splits_kernel<_Float16>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

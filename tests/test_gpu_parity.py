@@ -275,3 +275,4 @@ def test_c3d_batch32_layers(variant, li):
     case = LayerCase(f"b32-{variant}-{l.name}", 32, l.c_in, l.c_out, (l.t, l.h, l.w), l.k,
                      l.stride, l.pad, "bf16", mask)
     check_sampled(case, f"b32 {variant} {l.name}", count=2000)
+
