@@ -35,6 +35,7 @@ def parse():
     p.add_argument("--dtype", default="bf16", choices=["bf16", "f16", "f32"])
     p.add_argument("--rate", type=float, default=3.0, help="whole-stack MAC pruning rate (KGS)")
     p.add_argument("--mode", default="kgs", choices=["kgs", "vanilla"])
+    p.add_argument("--group", default="4x4", help="kernel group size g_MxG_N of the masks")
     p.add_argument("--no-graph", action="store_true", help="launch eagerly instead of a HIP graph")
     p.add_argument("--separate-pool", action="store_true",
                    help="run max-pools as their own kernels instead of in the conv epilogue")
@@ -49,6 +50,11 @@ def parse():
                    help="with --profile-layer: also run a plain device copy of MIB MiB, the "
                         "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE")
     return p.parse_args()
+
+
+def group_of(args):
+    gm, gn = (int(v) for v in args.group.lower().split("x"))
+    return gm, gn
 
 
 def log(*a):
@@ -115,7 +121,7 @@ def profile_layer(args, torch, stream):
     plain copy of known size) so rocprofv3 sees only these kernels."""
     from paper_2007_09835_amd.stack import Stack
     sparse = Stack(args.net, args.batch, args.dtype, args.mode, args.rate,
-                   fuse_pool=not args.separate_pool)
+                   fuse_pool=not args.separate_pool, group=group_of(args))
     idx = [l.name for l in sparse.layers].index(args.profile_layer)
     l, conv = sparse.layers[idx], sparse.convs[idx]
     inp = torch.randn(conv.desc_for(args.batch).n, l.t, l.h, l.w, l.c_in, device="cuda").abs()
@@ -213,7 +219,8 @@ def main():
 
     log("building stacks ...")
     fuse = not args.separate_pool
-    sparse = Stack(args.net, args.batch, args.dtype, args.mode, args.rate, fuse_pool=fuse)
+    sparse = Stack(args.net, args.batch, args.dtype, args.mode, args.rate, fuse_pool=fuse,
+                   group=group_of(args))
     dense = Stack(args.net, args.batch, args.dtype, "dense", fuse_pool=fuse)
     l0 = sparse.layers[0]
     clip = synth.clip_input("bench-clip", args.batch, "uniform01", l0.c_in, l0.t, l0.h, l0.w)
@@ -289,8 +296,9 @@ def main():
                         if drow["kgs"] else l.dense_macs(args.batch))
     achieved = kept_flops / (drow["ms_sparse"] * 1e-3) / 1e12
     peak = PEAK_TFLOPS[args.dtype]
-    traffic = measured_traffic(l.name) if (drow["kgs"] and args.batch == 1 and args.net == "c3d"
-                                           and args.dtype == "bf16" and args.mode == "kgs") else None
+    traffic = measured_traffic(l.name) if (args.batch == 1 and args.net == "c3d"
+                                           and args.dtype == "bf16" and args.mode == "kgs"
+                                           and group_of(args) == (4, 4)) else None
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": traffic,
                 "kernel": "%s conv (%s)" % (l.name, "KGS" if drow["kgs"] else "dense"),
@@ -312,9 +320,10 @@ def main():
         "dtype": args.dtype,
         "data": "synthetic (seeded clip and Kaiming-normal weights; no dataset or trained model)",
         "config": {
-            "workload": "%s conv stack, %d x 16x112x112 clip, %s %s masks g=4x4, whole-stack "
+            "workload": "%s conv stack, %d x 16x112x112 clip, %s %s masks g=%s, whole-stack "
                         "pruning rate %.2fx (conv1 dense)%s"
-                        % (args.net.upper(), args.batch, args.dtype, args.mode.upper(), rate,
+                        % (args.net.upper(), args.batch, args.dtype, args.mode.upper(),
+                           args.group.lower(), rate,
                            ", HIP graph" if not args.no_graph else ", eager launches"),
             "batch": args.batch, "clip": [16, 112, 112], "pruning_rate": round(rate, 4),
         },

@@ -186,6 +186,24 @@ Tiling choose_tiling(const Geom &g) {
           best = Tiling{bt, bh, bw, ht, hh, hw, cc, row, kSlots, (g.c_in + cc - 1) / cc};
         }
       }
+  // 16-bit layers with a small halo (few kernel taps) take wider channel
+  // chunks: each chunk then carries more K-steps per halo load, barrier and
+  // pipeline restart.  Limits: the register stager's 8 pieces of 16 bytes
+  // per thread (2048 per workgroup) and the LDS budget.
+  if (best_cost >= 0 && g.es == 2) {
+    int wide = best.cc;
+    while (wide < 128 && wide < g.c_in) {
+      const int next = wide * 2;
+      int nrow = (next * g.es + 15) / 16 * 16;
+      if ((nrow / 16) % 2 == 0) nrow += 16;
+      const long rows = static_cast<long>(best.ht) * best.hh * best.hw;
+      if (rows * (next / 8) > 2048 || rows * nrow > kMaxHalo) break;
+      wide = next;
+      best.row = nrow;
+    }
+    best.cc = wide;
+    best.nchunks = (g.c_in + wide - 1) / wide;
+  }
   return best;
 }
 
@@ -493,6 +511,7 @@ void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
       }
     }
     L.step_ptr[static_cast<size_t>(wt) * (tl.nchunks + 1) + tl.nchunks] = step;
+    L.plan.tile_steps = std::max<int32_t>(L.plan.tile_steps, static_cast<int32_t>(step - first_step));
   }
 }
 
@@ -532,6 +551,8 @@ void build_exact_f32_layout(const Geom &g, const Tiling &tl, const uint8_t *w, c
       }
     }
     L.step_ptr[static_cast<size_t>(wt) * (tl.nchunks + 1) + tl.nchunks] = item;
+    L.plan.tile_steps = std::max<int32_t>(L.plan.tile_steps,
+                                          static_cast<int32_t>(item - L.item_ptr[wt]));
   }
 }
 
@@ -752,25 +773,46 @@ Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint32_t variant, u
   Launch L{4, 1, 0, 0};
   const long ntg = (p.wave_tiles + L.wpw - 1) / L.wpw;
   const long wgs = bricks * ntg;
-  // Channel splits add workgroups until the GPU holds one resident round:
-  // CUs x workgroups per CU (registers and LDS of the split-K kernel, whose
-  // LDS is just the halo).  A second partial round would double the time,
-  // so the count is rounded down, then lowered to the fewest splits that
-  // give the same number of chunks per workgroup (balanced splits).
+  // Channel splits trade per-workgroup fixed cost (prologue, first halo
+  // load, epilogue) and a reduction pass against parallelism.  The split
+  // count minimises a time model in cycles:
+  //   rounds * kFixed + chunks per workgroup * steps per chunk * step cycles
+  //   * (1 + kShare * (workgroups per CU - 1)) + [s > 1] (kReduce + partial
+  //   bytes written and read back / kPartialBytesPerCycle),
+  // with constants fitted to per-wave timestamps and per-layer traces of the
+  // C3D and R(2+1)D layers on MI355X.
   const size_t halo = static_cast<size_t>(tl.ht) * tl.hh * tl.hw * tl.row;
   int per_cu = conv_resident(static_cast<int>(variant), d->dtype, p.mfw, halo);
   if (per_cu <= 0) {
     (void)hipGetLastError();
     per_cu = 2;
   }
-  long cap = static_cast<long>(device_cus()) * per_cu;
-  if (const char *env = std::getenv("RT3D_SPLIT_TARGET")) cap = std::max(1, std::atoi(env));
+  const long cus = device_cus();
+  const long total_vox_ = static_cast<long>(g.n) * g.to * g.ho * g.wo;
+  const double partial_bytes = 2.0 * static_cast<double>(total_vox_) * ((g.c_out + 3) / 4 * 4) * 4;
+  constexpr double kFixed = 12000, kReduce = 9600, kShare = 0.2, kPartialBytesPerCycle = 4200;
+  const double step_cycles = p.mfw == 1 ? 380.0 : (p.mfw == 2 ? 555.0 : 815.0);
+  const double chunk_steps = p.tile_steps > 0 ? static_cast<double>(p.tile_steps) / tl.nchunks : 24.0;
+  // A chunk costs its K-steps, but no less than the exposed latency of its
+  // halo load, plus the barriers and LDS commit around it.
+  constexpr double kChunkLatency = 5000, kChunkFixed = 2000;
+  const double chunk_cycles = std::max(chunk_steps * step_cycles, kChunkLatency) + kChunkFixed;
   int splits = 1;
-  if (wgs < cap) {
-    splits = static_cast<int>(std::min<long>(tl.nchunks, std::max<long>(1, cap / wgs)));
-    const int per = (tl.nchunks + splits - 1) / splits;
-    splits = (tl.nchunks + per - 1) / per;
+  double best = -1;
+  for (int s = 1; s <= tl.nchunks; ++s) {
+    if (s > 1 && (tl.nchunks + s - 1) / s == (tl.nchunks + s - 2) / (s - 1)) continue;  // same chunks per WG
+    const long n = wgs * s;
+    const long per = std::min<long>((n + cus - 1) / cus, per_cu);          // workgroups per CU at once
+    const long rounds = (n + cus * per - 1) / (cus * per);
+    const double t = rounds * (kFixed + ((tl.nchunks + s - 1) / s) * chunk_cycles *
+                                            (1.0 + kShare * static_cast<double>(per - 1))) +
+                     (s > 1 ? kReduce + s * partial_bytes / kPartialBytesPerCycle : 0.0);
+    if (best < 0 || t < best) {
+      best = t;
+      splits = s;
+    }
   }
+  if (const char *env = std::getenv("RT3D_SPLITS")) splits = std::max(1, std::min(tl.nchunks, std::atoi(env)));
   const long total_vox = static_cast<long>(g.n) * g.to * g.ho * g.wo;
   const uint64_t per_split = static_cast<uint64_t>(total_vox) * ((g.c_out + 3) / 4 * 4) * 4;
   while (splits > 1 && per_split * splits > ws_cap) --splits;

@@ -40,7 +40,7 @@ struct Plan {
   int32_t mfw;             // 16-filter MFMA rows per wave tile
   int32_t wave_tiles;      // number of wave tiles
   int32_t items_per_step;  // items consumed per K-step
-  int32_t pad0;
+  int32_t tile_steps;      // most K-steps of one wave tile over all chunks
   uint64_t step_ptr_off;   // u32 [wave_tiles][nchunks + 1]
   uint64_t item_ptr_off;   // u32 [wave_tiles]
   uint64_t items_off;      // u32 [...] LDS byte offset of each item

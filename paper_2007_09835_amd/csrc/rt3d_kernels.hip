@@ -229,8 +229,8 @@ struct Stager {
   bool ok;
 
   __device__ __forceinline__ void init(const ConvArgs &a, const Brick &b) {
-    ppr = a.cc / EPP;  // 1, 2 or 4
-    shift = ppr == 4 ? 2 : (ppr == 2 ? 1 : 0);
+    ppr = a.cc / EPP;  // a power of two
+    shift = __builtin_ctz(static_cast<unsigned>(ppr));
     total = a.ht * a.hh * a.hw * ppr;
     ok = total <= MAXI * static_cast<int>(blockDim.x);
     // Halo row of piece k: (threadIdx.x + k * blockDim.x) >> shift, walked

@@ -24,16 +24,18 @@ class Stack:
 
     def __init__(self, net: str, batch: int = 1, dtype: str = "bf16", mode: str = "kgs",
                  rate: float = 3.0, tag: Optional[str] = None, device: str = "cuda",
-                 fuse_pool: bool = True):
+                 fuse_pool: bool = True, group=(4, 4)):
         """``fuse_pool`` folds each max-pool into the preceding conv's
-        epilogue; otherwise the pools run as separate kernels."""
+        epilogue; otherwise the pools run as separate kernels.  ``group`` is
+        the kernel group size (g_M, g_N) of the KGS masks."""
         self.net, self.batch, self.dtype, self.mode, self.rate = net, batch, dtype, mode, rate
         self.fuse_pool = fuse_pool
+        self.group = tuple(group)
         tag = tag or net
         if net == "c3d":
-            self.layers = synth.c3d_stack(rate if mode == "kgs" else 3.0, tag=tag)
+            self.layers = synth.c3d_stack(rate if mode == "kgs" else 3.0, tag=tag, g=self.group)
         elif net == "r2plus1d":
-            self.layers = synth.r2plus1d_stack(tag=tag)
+            self.layers = synth.r2plus1d_stack(tag=tag, g=self.group)
         else:
             raise ValueError(net)
         tdt = layers.TORCH_DTYPES[dtype]
@@ -52,7 +54,7 @@ class Stack:
             self.convs.append(layers.Conv3d(l.c_in, l.c_out, (l.t, l.h, l.w), l.k, l.stride, l.pad,
                                             w, d.bias.astype(np.float32), mask, dtype,
                                             relu=l.relu, residual=l.residual_from is not None,
-                                            device=device, batch=batch, pool=pool))
+                                            g=l.g, device=device, batch=batch, pool=pool))
         # activation buffers (channels-last), allocated once
         self.x = torch.zeros((batch, self.layers[0].t, self.layers[0].h, self.layers[0].w,
                               self.layers[0].c_in), dtype=tdt, device=device)

@@ -54,6 +54,7 @@ class ConvLayer:
     input_from: Optional[str] = None     # name of the tensor this layer reads (None: previous)
     pool_after: Optional[Tuple[Tuple[int, int, int], Tuple[int, int, int]]] = None
     keep: Optional[int] = None         # kept positions per group (KGS layers)
+    g: Tuple[int, int] = (GROUP, GROUP)  # kernel group size (g_M filters, g_N channels)
 
     @property
     def ks(self) -> int:
@@ -71,7 +72,7 @@ class ConvLayer:
 
     @property
     def groups(self) -> Tuple[int, int]:
-        return -(-self.c_out // GROUP), -(-self.c_in // GROUP)
+        return -(-self.c_out // self.g[0]), -(-self.c_in // self.g[1])
 
     def dense_macs(self, batch: int = 1) -> int:
         """Multiply-accumulates of the dense layer (the paper's "FLOPs")."""
@@ -251,10 +252,10 @@ def stack_rate(layers: Sequence[ConvLayer], masks: Sequence[Optional[np.ndarray]
 def kept_weights(l: ConvLayer, mask: np.ndarray) -> int:
     """Number of weights kept by a mask: sum over groups of g_m_eff*g_n_eff*k."""
     p_groups, q_groups = l.groups
-    gm = np.full(p_groups, GROUP)
-    gm[-1] = l.c_out - GROUP * (p_groups - 1)
-    gn = np.full(q_groups, GROUP)
-    gn[-1] = l.c_in - GROUP * (q_groups - 1)
+    gm = np.full(p_groups, l.g[0])
+    gm[-1] = l.c_out - l.g[0] * (p_groups - 1)
+    gn = np.full(q_groups, l.g[1])
+    gn[-1] = l.c_in - l.g[1] * (q_groups - 1)
     k = mask.sum(axis=2, dtype=np.int64)
     return int((gm[:, None] * gn[None, :] * k).sum())
 
@@ -339,21 +340,24 @@ def single_layer_conv3b() -> Tuple[ConvLayer, dict]:
     return l, dict(tag="conv3b256", w_std=None, x_kind="halfnormal")
 
 
-def c3d_stack(rate: float = 3.0, tag: str = "c3d") -> List[ConvLayer]:
+def c3d_stack(rate: float = 3.0, tag: str = "c3d", g: Tuple[int, int] = (GROUP, GROUP)
+              ) -> List[ConvLayer]:
     """C3D stack with per-layer keep counts for a whole-stack rate (conv1
-    dense)."""
+    dense), kernel groups of g = (g_M, g_N)."""
     layers = c3d_layers()
     for l, k in zip(layers, stack_keep_counts(layers, rate, tag)):
         l.keep = k
+        l.g = tuple(g)
     return layers
 
 
-def r2plus1d_stack(tag: str = "r2plus1d") -> List[ConvLayer]:
+def r2plus1d_stack(tag: str = "r2plus1d", g: Tuple[int, int] = (GROUP, GROUP)) -> List[ConvLayer]:
     """R(2+1)D-18 stack: spatial KGS convs keep 3 or 4 of 9 positions,
     temporal ones 1 or 2 of 3, drawn per layer; stem and shortcuts dense."""
     layers = r2plus1d_layers()
     r = rng_for(tag, "keep")
     for l in layers:
+        l.g = tuple(g)
         if l.dense:
             continue
         l.keep = int(r.integers(3, 5)) if l.ks == 9 else int(r.integers(1, 3))

@@ -91,6 +91,37 @@ def test_dense_small_shapes(si, dtype):
     check_full(case, f"dense {tag} {dtype}")
 
 
+# Kernel groups wider than 4x4 (g_M, g_N in {4, 8, 16}): the planner expands
+# each group mask to its 4x4 blocks, so a 16-filter tile of a g_M = 16 layer
+# walks exactly its group's kept items.
+GROUPED = [
+    # tag, n, c_in, c_out, thw, k, stride, pad, g, keep
+    ("g1", 1, 32, 48, (4, 7, 9), (3, 3, 3), (1, 1, 1), (1, 1, 1), (16, 4), 9),
+    ("g2", 2, 24, 40, (3, 8, 6), (3, 3, 3), (1, 1, 1), (1, 1, 1), (8, 4), 10),
+    ("g3", 1, 36, 33, (4, 6, 6), (1, 3, 3), (1, 2, 2), (0, 1, 1), (16, 8), 4),   # partial groups
+    ("g4", 1, 20, 16, (5, 5, 5), (3, 1, 1), (1, 1, 1), (1, 0, 0), (4, 8), 2),
+    ("g5", 1, 64, 64, (3, 6, 6), (3, 3, 3), (1, 1, 1), (1, 1, 1), (16, 16), 8),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("gi", range(len(GROUPED)))
+def test_kgs_group_sizes(gi, dtype):
+    tag, n, c_in, c_out, thw, k, stride, pad, g, keep = GROUPED[gi]
+    mask = masked(tag, c_out, c_in, k, keep, g)
+    case = LayerCase(tag, n, c_in, c_out, thw, k, stride, pad, dtype, mask, g=g)
+    check_full(case, f"kgs {tag} g={g} {dtype}")
+
+
+def test_conv3b_shape_with_16x4_groups():
+    """C3D conv3b-shaped layer with g = 16x4 (MFMA-width groups) at full size,
+    sampled outputs."""
+    mask = masked("g16conv3b", 256, 256, (3, 3, 3), 9, (16, 4))
+    case = LayerCase("g16conv3b", 1, 256, 256, (8, 28, 28), (3, 3, 3), (1, 1, 1), (1, 1, 1),
+                     "bf16", mask, x_kind="halfnormal", g=(16, 4))
+    check_sampled(case, "conv3b g=16x4 bf16")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_residual_epilogue(dtype):
     mask = masked("res", 24, 16, (3, 1, 1), 2)
