@@ -46,6 +46,10 @@ def parse():
     p.add_argument("--report", default=None, help="write per-layer results to this JSON file")
     p.add_argument("--profile-layer", default=None,
                    help="only launch this layer's sparse conv --layer-reps times (for rocprofv3)")
+    p.add_argument("--suite", default=None, metavar="PATH",
+                   help="instead of the headline line, run the per-config measurement suite "
+                        "(single layers, R(2+1)D, batch-32 rate sweep, warm/cold latency, oracle "
+                        "timing) and write a markdown report to PATH (+ PATH.json)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="with --profile-layer: also run a plain device copy of MIB MiB, the "
                         "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE")
@@ -171,13 +175,13 @@ def cpu_baseline(stack, fraction):
             if l.dense:
                 oracle.conv3d_dense(x64, w64, b64, None, l.stride, l.pad, l.relu)
             else:
-                oracle.conv3d_kgs(x64, w64, mask, 4, 4, b64, None, l.stride, l.pad, l.relu)
+                oracle.conv3d_kgs(x64, w64, mask, *l.g, b64, None, l.stride, l.pad, l.relu)
             elapsed += time.perf_counter() - t0
         else:
             k = max(1, int(n_out * fraction))
             idx = np.sort(synth.rng_for("cpu-sample", l.name).choice(n_out, size=k, replace=False))
             t0 = time.perf_counter()
-            oracle.conv3d_points(x64, w64, idx, None if l.dense else mask, 4, 4, b64, None,
+            oracle.conv3d_points(x64, w64, idx, None if l.dense else mask, *l.g, b64, None,
                                  l.stride, l.pad, l.relu)
             elapsed += time.perf_counter() - t0
         flops += 2.0 * k * l.c_in * l.ks
@@ -193,6 +197,217 @@ def cpu_baseline(stack, fraction):
                       "seeded %.0f%% of every conv layer's outputs" % (100 * fraction),
                       total_outputs, elapsed)),
     }
+
+
+# ---------------------------------------------------------------------------
+# Measurement suite (the per-config report; not the headline line)
+# ---------------------------------------------------------------------------
+
+def pct(xs, q):
+    import numpy as np
+    return float(np.percentile(np.asarray(xs), q))
+
+
+def latency(torch, fn, iters, stream, flush=None):
+    """Per-launch latency (ms) over `iters` launches, each bracketed by its
+    own events; with `flush`, 1 GiB is written before every launch (outside
+    the events) so L2 and the 256 MB MALL start cold."""
+    times = []
+    fn()
+    torch.cuda.synchronize()
+    for _ in range(iters):
+        if flush is not None:
+            flush()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+    return {"p10": pct(times, 10), "p50": pct(times, 50), "p90": pct(times, 90)}
+
+
+def suite(args, torch, stream):
+    import numpy as np
+
+    import oracle
+    from paper_2007_09835_amd import layers as L
+    from paper_2007_09835_amd import synth
+    from paper_2007_09835_amd.stack import Stack
+
+    scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")   # 1 GiB
+    flush = lambda: scratch.fill_(1.0)
+    iters = max(args.steps, 50)
+    out = {"configs": {}}
+    md = ["# Measurement suite (MI355X, one GPU)", "",
+          "Latencies are per launch from HIP events (p10 / p50 / p90 over %d launches); warm = "
+          "back-to-back launches, cold = 1 GiB written before each launch. Dense-equivalent "
+          "TFLOP/s = 2 x dense MACs / time; executed = 2 x kept MACs / time." % iters, "",
+          "Command: `python bench.py --suite <path>`", ""]
+    cores_all = oracle.num_threads()
+
+    def one_layer(tag, l, cfg, dtype, sparse, g=(4, 4)):
+        d = synth.layer_params(cfg["tag"], l, w_std=cfg.get("w_std"))
+        mask = d.mask if sparse else None
+        w_t = synth.to_dtype(d.w, dtype)
+        conv = L.Conv3d(l.c_in, l.c_out, (l.t, l.h, l.w), l.k, l.stride, l.pad, w_t,
+                        d.bias.astype(np.float32), mask, dtype, g=g)
+        x64 = synth.clip_input(cfg["tag"], 1, cfg["x_kind"], l.c_in, l.t, l.h, l.w)
+        x_t = synth.to_dtype(x64, dtype)
+        x = x_t.permute(0, 2, 3, 4, 1).contiguous().cuda()
+        y = torch.empty(conv.out_shape(1), dtype=L.TORCH_DTYPES[dtype], device="cuda")
+        fn = lambda: conv(x, out=y)
+        warm = latency(torch, fn, iters, stream)
+        cold = latency(torch, fn, iters, stream, flush)
+        fn()
+        torch.cuda.synchronize()
+        got = y.permute(0, 4, 1, 2, 3).double().cpu().numpy()
+        return conv, d, x_t, got, warm, cold
+
+    def rel(a, b):
+        return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30))
+
+    # Configs 1 and 2: single layers, every variant checked against the oracle.
+    rows = []
+    for cname, (l, cfg), dtypes, full in (("1", synth.single_layer_small(), ("f32",), True),
+                                          ("2", synth.single_layer_conv3b(), ("f32", "bf16"), False)):
+        for dtype in dtypes:
+            for sparse in (True, False):
+                conv, d, x_t, got, warm, cold = one_layer(cname, l, cfg, dtype, sparse)
+                w_ref = synth.to_dtype(d.w, dtype).double().numpy()
+                x_ref = x_t.double().numpy()
+                b_ref = d.bias.astype(np.float32).astype(np.float64)
+                mask = d.mask if sparse else None
+                if full:
+                    t0 = time.perf_counter()
+                    ref = (oracle.conv3d_kgs(x_ref, w_ref, mask, 4, 4, b_ref, None, l.stride, l.pad, True)
+                           if sparse else oracle.conv3d_dense(x_ref, w_ref, b_ref, None, l.stride, l.pad, True))
+                    t_all = time.perf_counter() - t0
+                    err = rel(got, ref)
+                    n_or = got.size
+                else:
+                    idx = np.sort(synth.rng_for("suite", cname, dtype).choice(got.size, 4000, replace=False))
+                    t0 = time.perf_counter()
+                    ref = oracle.conv3d_points(x_ref, w_ref, idx, mask, 4, 4, b_ref, None, l.stride, l.pad, True)
+                    t_all = time.perf_counter() - t0
+                    err = rel(got.ravel()[idx], ref)
+                    n_or = len(idx)
+                # one-thread oracle timing on a bounded sample
+                idx1 = np.sort(synth.rng_for("suite1", cname, dtype).choice(got.size, min(got.size, 2000), replace=False))
+                oracle.set_threads(1)
+                t0 = time.perf_counter()
+                oracle.conv3d_points(x_ref, w_ref, idx1, mask, 4, 4, b_ref, None, l.stride, l.pad, True)
+                t_one = time.perf_counter() - t0
+                oracle.set_threads(cores_all)
+                dense_macs = l.dense_macs()
+                kept = l.voxels_out * conv.info.kept_weights if sparse else dense_macs
+                rows.append({"config": cname, "dtype": dtype, "variant": "KGS" if sparse else "dense",
+                             "warm": warm, "cold": cold, "relL2": err, "oracle_outputs": n_or,
+                             "dense_eq_tflops": 2 * dense_macs / warm["p50"] / 1e9,
+                             "executed_tflops": 2 * kept / warm["p50"] / 1e9,
+                             "rate": dense_macs / kept,
+                             "oracle_s_all_threads_per_output": t_all / n_or,
+                             "oracle_s_one_thread_per_output": t_one / len(idx1)})
+                log("cfg%s %s %s warm p50 %.4f ms cold p50 %.4f ms relL2 %.2e" %
+                    (cname, dtype, rows[-1]["variant"], warm["p50"], cold["p50"], err))
+    out["configs"]["1-2"] = rows
+    md += ["## Configs 1 and 2: single layers", "",
+           "| cfg | dtype | variant | R | warm p10/p50/p90 ms | cold p50 ms | dense-eq TF | executed TF | relL2 vs oracle | oracle us/output (%d thr / 1 thr) |" % cores_all,
+           "|---|---|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        md.append("| %s | %s | %s | %.2f | %.4f / %.4f / %.4f | %.4f | %.1f | %.1f | %.2e (%d outputs) | %.2f / %.2f |" % (
+            r["config"], r["dtype"], r["variant"], r["rate"], r["warm"]["p10"], r["warm"]["p50"],
+            r["warm"]["p90"], r["cold"]["p50"], r["dense_eq_tflops"], r["executed_tflops"], r["relL2"],
+            r["oracle_outputs"], 1e6 * r["oracle_s_all_threads_per_output"],
+            1e6 * r["oracle_s_one_thread_per_output"]))
+    md.append("")
+
+    # Configs 3-5: stacks (whole pass in one HIP graph), per-layer warm latency.
+    def stack_pair(net, batch, mode, rate, group=(4, 4)):
+        sp = Stack(net, batch, "bf16", mode, rate, group=group)
+        dn = Stack(net, batch, "bf16", "dense", group=group)
+        l0 = sp.layers[0]
+        x = synth.to_dtype(synth.clip_input("bench-clip", batch, "uniform01", l0.c_in, l0.t, l0.h,
+                                            l0.w), "bf16").permute(0, 2, 3, 4, 1).contiguous().cuda()
+        sp.x.copy_(x)
+        dn.x.copy_(x)
+        res = {}
+        for name, st in (("kgs", sp), ("dense", dn)):
+            for _ in range(2):
+                st.forward()
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                st.forward()
+            res[name] = {"warm": latency(torch, g.replay, iters, stream),
+                         "cold": latency(torch, g.replay, max(iters // 5, 10), stream, flush),
+                         "layers": per_layer_ms(torch, st, 20, stream)}
+        return sp, res
+
+    md += ["## Configs 3-5: stacks (bf16, HIP graph per pass)", "",
+           "| workload | R | KGS ms/clip warm p50 (p10-p90) | cold p50 | dense ms/clip warm p50 | speedup | speedup / R | dense-eq TFLOP/s |",
+           "|---|---|---|---|---|---|---|---|"]
+    sweep = [("C3D batch 1 (cfg 3)", "c3d", 1, "kgs", 3.0, (4, 4)),
+             ("C3D batch 1, g=16x4 (NEXT #1)", "c3d", 1, "kgs", 3.0, (16, 4)),
+             ("R(2+1)D-18 batch 1 (cfg 4)", "r2plus1d", 1, "kgs", 3.0, (4, 4))]
+    sweep += [("C3D batch 32, KGS %gx (cfg 5)" % r, "c3d", 32, "kgs", r, (4, 4)) for r in (2.0, 3.0, 4.0, 5.0)]
+    sweep += [("C3D batch 32, vanilla 3x (cfg 5)", "c3d", 32, "vanilla", 3.0, (4, 4))]
+    stacks = []
+    for label, net, batch, mode, rate, group in sweep:
+        sp, res = stack_pair(net, batch, mode, rate, group)
+        R = sp.kept_rate()
+        kw, dw = res["kgs"]["warm"]["p50"], res["dense"]["warm"]["p50"]
+        entry = {"label": label, "rate": R, "kgs": res["kgs"], "dense": res["dense"],
+                 "layers": [l.name for l in sp.layers],
+                 "layer_rates": [l.dense_macs(batch) / (batch * l.voxels_out * c.info.kept_weights)
+                                 if m is not None else 1.0 for l, c, m in zip(sp.layers, sp.convs, sp.masks)]}
+        stacks.append(entry)
+        md.append("| %s | %.2f | %.4f (%.4f-%.4f) | %.4f | %.4f | %.2f | %.2f | %.0f |" % (
+            label, R, kw / batch, res["kgs"]["warm"]["p10"] / batch, res["kgs"]["warm"]["p90"] / batch,
+            res["kgs"]["cold"]["p50"] / batch, dw / batch, dw / kw, dw / kw / R,
+            2 * sp.dense_macs() / (kw * 1e-3) / 1e12))
+        log("%s: kgs %.4f ms dense %.4f ms (R %.2f)" % (label, kw, dw, R))
+        del sp
+        torch.cuda.empty_cache()
+    md.append("")
+    for e in stacks:
+        if "batch 32" not in e["label"] and "R(2+1)D" not in e["label"]:
+            continue
+        md += ["### %s: per layer (ms per launch, warm)" % e["label"], "",
+               "| layer | R | KGS | dense | speedup | speedup / R |", "|---|---|---|---|---|---|"]
+        for name, r, ks, ds in zip(e["layers"], e["layer_rates"], e["kgs"]["layers"], e["dense"]["layers"]):
+            md.append("| %s | %.2f | %.4f | %.4f | %.2f | %.2f |" % (name, r, ks, ds, ds / ks, ds / ks / r))
+        md.append("")
+    out["configs"]["stacks"] = stacks
+
+    # Context: MIOpen dense conv3d (torch) per C3D layer, batch 1, bf16 channels-last.
+    md += ["## Context: torch conv3d (MIOpen), C3D layers, batch 1, bf16 (warm p50 ms)", "",
+           "| layer | MIOpen | our dense | our KGS (4x4) |", "|---|---|---|---|"]
+    try:
+        c3d = next(e for e in stacks if e["label"].startswith("C3D batch 1 (cfg 3)"))
+        ctx = []
+        for i, l in enumerate(synth.c3d_stack(3.0)):
+            x = torch.randn(1, l.c_in, l.t, l.h, l.w, device="cuda", dtype=torch.bfloat16).to(
+                memory_format=torch.channels_last_3d)
+            w = torch.randn(l.c_out, l.c_in, *l.k, device="cuda", dtype=torch.bfloat16).to(
+                memory_format=torch.channels_last_3d)
+            b = torch.zeros(l.c_out, device="cuda", dtype=torch.bfloat16)
+            fn = lambda: torch.nn.functional.conv3d(x, w, b, l.stride, l.pad)
+            for _ in range(3):
+                fn()
+            t = latency(torch, fn, 20, stream)["p50"]
+            ctx.append(t)
+            md.append("| %s | %.4f | %.4f | %.4f |" % (l.name, t, c3d["dense"]["layers"][i], c3d["kgs"]["layers"][i]))
+        out["miopen_c3d_b1_ms"] = ctx
+    except Exception as exc:  # MIOpen unavailable or failing: report, do not abort the suite
+        md.append("| (torch conv3d failed: %s) | | | |" % str(exc).splitlines()[0][:80])
+    md.append("")
+    with open(args.suite, "w") as f:
+        f.write("\n".join(md) + "\n")
+    with open(args.suite + ".json", "w") as f:
+        json.dump(out, f, indent=1)
+    log("suite written to %s" % args.suite)
 
 
 def main():
@@ -215,6 +430,9 @@ def main():
 
     if args.profile_layer:
         profile_layer(args, torch, stream)
+        return
+    if args.suite:
+        suite(args, torch, stream)
         return
 
     log("building stacks ...")

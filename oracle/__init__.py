@@ -34,6 +34,8 @@ def _load():
         lib.oracle_conv3d_points.argtypes = ([i] * 17 + [dp, dp, ctypes.c_void_p, dp, dp, i,
                                               ctypes.c_long, ctypes.c_void_p, dp])
         lib.oracle_num_threads.argtypes = []
+        lib.oracle_set_threads.argtypes = [i]
+        lib.oracle_set_threads.restype = None
         for f in (lib.oracle_conv3d_dense, lib.oracle_conv3d_kgs, lib.oracle_kgs_pack,
                   lib.oracle_maxpool3d, lib.oracle_conv3d_points, lib.oracle_num_threads):
             f.restype = ctypes.c_int
@@ -44,6 +46,11 @@ def _load():
 def num_threads() -> int:
     """Threads the oracle's OpenMP loops use."""
     return int(_load().oracle_num_threads())
+
+
+def set_threads(n: int) -> None:
+    """Set the thread count of the oracle's OpenMP loops (for timing)."""
+    _load().oracle_set_threads(int(n))
 
 
 def _f64(a):

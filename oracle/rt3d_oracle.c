@@ -333,3 +333,13 @@ int oracle_num_threads(void)
     return 1;
 #endif
 }
+
+/* Thread count for the loops above (timing runs on one core); n < 1 is ignored. */
+void oracle_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
