@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <numeric>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -262,6 +263,35 @@ rt3d_status canon_index(const rt3d_conv3d_desc *d, const uint8_t *mask, Canon &c
   return ok();
 }
 
+// Small-input-channel path (kVarSmall*16): 16-bit, c_in <= 4 (one channel
+// block), kernels up to 3x3x3 with stride 1 (at most 4 K-steps of 8 items and
+// 12 halo lines of <= 192 elements per brick, the kernel's register budget),
+// and no pooling or the 1x2x2 window (pooled in registers).  Disable with
+// RT3D_SMALL_KERNEL=0.
+bool small_ok(const Geom &g) {
+  if (const char *env = std::getenv("RT3D_SMALL_KERNEL"))
+    if (std::atoi(env) == 0) return false;
+  const bool pool_ok = (g.qt == 1 && g.qh == 1 && g.qw == 1) || (g.qt == 1 && g.qh == 2 && g.qw == 2);
+  return g.es == 2 && g.c_in <= 4 && g.kt <= 3 && g.kh <= 3 && g.kw <= 3 && g.st == 1 &&
+         g.sh == 1 && g.sw == 1 && pool_ok;
+}
+
+// Bricks of 1 x 2 x 32 output voxels; halo rows of 4 channels (8 bytes).
+Tiling small_tiling(const Geom &g) {
+  Tiling t{};
+  t.bt = 1;
+  t.bh = 2;
+  t.bw = 32;
+  t.ht = g.kt;
+  t.hh = 1 + g.kh;
+  t.hw = 31 + g.kw;
+  t.cc = 4;
+  t.row = 8;
+  t.slots = 64;
+  t.nchunks = 1;
+  return t;
+}
+
 // mask of the 4x4 kernel block (p4, q4) at position pos (groups of 8 or 16
 // are unions of 4x4 blocks that share their group's mask row).
 struct Mask4 {
@@ -423,7 +453,7 @@ void pair_items(std::vector<Item> &its, const Geom &g, const Tiling &tl, PassCos
 // 16-bit MFMA item layout (variants kVarDenseItems16, kVarKgsUnion16) and
 // the f32 16x16x4 dense layout (kVarDenseItemsF32).
 void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const Mask4 *m4,
-                        Layout &L) {
+                        Layout &L, bool small = false) {
   const bool f32 = g.es == 4;
   const int ips = f32 ? 4 : 8;           // items per K-step
   const int epl = f32 ? 4 : 8;           // operand elements per lane
@@ -450,8 +480,18 @@ void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
     const int v = std::atoi(env);
     if (v == 1 || v == 2 || v == 4) mfw = v;
   }
+  if (small) {
+    // Up to 32 filters per wave: wider tiles hold 4x the weights in
+    // registers and drop residency to one wave per SIMD.
+    mfw = g.c_out > 16 ? 2 : 1;
+    if (const char *env = std::getenv("RT3D_SMALL_MFW")) {
+      const int v = std::atoi(env);
+      if (v == 1 || v == 2 || v == 4) mfw = v;
+    }
+  }
   const int wt_count = (g.c_out + 16 * mfw - 1) / (16 * mfw);
-  L.variant = dense ? (f32 ? kVarDenseItemsF32 : kVarDenseItems16) : kVarKgsUnion16;
+  L.variant = small ? (dense ? kVarSmallDense16 : kVarSmallKgs16)
+                    : (dense ? (f32 ? kVarDenseItemsF32 : kVarDenseItems16) : kVarKgsUnion16);
   L.plan.mfw = mfw;
   L.plan.wave_tiles = wt_count;
   L.plan.items_per_step = ips;
@@ -674,7 +714,8 @@ rt3d_status plan_kgs(const rt3d_conv3d_desc *d, const uint8_t *mask, const uint8
     }
   }
   const Geom g = geom_of(d);
-  tl = choose_tiling(g);
+  const bool small = small_ok(g);
+  tl = small ? small_tiling(g) : choose_tiling(g);
   if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
   Mask4 m4{mask, c.Q, ks, d->g_m / 4, d->g_n / 4};
   static const uint8_t zero = 0;
@@ -695,9 +736,9 @@ rt3d_status plan_kgs(const rt3d_conv3d_desc *d, const uint8_t *mask, const uint8
   } else {
     if (!w) {
       std::vector<uint8_t> scratch(static_cast<size_t>(g.c_out) * g.c_in * ks * g.es, 0);
-      build_items_layout(g, tl, scratch.data(), &m4, L);
+      build_items_layout(g, tl, scratch.data(), &m4, L, small);
     } else {
-      build_items_layout(g, tl, wsrc, &m4, L);
+      build_items_layout(g, tl, wsrc, &m4, L, small);
     }
   }
   return ok();
@@ -715,7 +756,8 @@ rt3d_status check_info(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, bo
     return fail(RT3D_ERR_BLOB_MISMATCH, "info was not written by this library version");
   if (info->desc_hash != desc_hash(d))
     return fail(RT3D_ERR_BLOB_MISMATCH, "blob was packed for a different layer description");
-  const bool is_sparse = info->variant == kVarKgsUnion16 || info->variant == kVarKgsExactF32;
+  const bool is_sparse = info->variant == kVarKgsUnion16 || info->variant == kVarKgsExactF32 ||
+                         info->variant == kVarSmallKgs16;
   if (is_sparse != sparse)
     return fail(RT3D_ERR_BLOB_MISMATCH, sparse ? "dense blob passed to the KGS forward"
                                                : "KGS blob passed to the dense forward");
@@ -771,6 +813,7 @@ Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint32_t variant, u
   const long bricks = static_cast<long>(g.n) * ((g.to + tl.bt - 1) / tl.bt) *
                       ((g.ho + tl.bh - 1) / tl.bh) * ((g.wo + tl.bw - 1) / tl.bw);
   Launch L{4, 1, 0, 0};
+  if (variant == kVarSmallDense16 || variant == kVarSmallKgs16) return L;  // one chunk, no split
   const long ntg = (p.wave_tiles + L.wpw - 1) / L.wpw;
   const long wgs = bricks * ntg;
   // Channel splits trade per-workgroup fixed cost (prologue, first halo
@@ -894,6 +937,23 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
     case kVarKgsUnion16:
       e = launch_items16(a, d->dtype, p.mfw, stream);
       break;
+    case kVarSmallDense16:
+    case kVarSmallKgs16: {
+      // Waves walk (wave tile, brick) pairs: as many workgroups as fit
+      // resident, with a wave count that is a multiple of the wave tiles.
+      const long waves = static_cast<long>(a.nbricks) * a.wave_tiles;
+      int per_cu = small_resident(a, d->dtype, p.mfw);
+      if (per_cu <= 0) {
+        (void)hipGetLastError();
+        per_cu = 1;
+      }
+      long grid = std::min<long>((waves + 3) / 4, static_cast<long>(device_cus()) * per_cu);
+      const long unit = a.wave_tiles / std::gcd(a.wave_tiles, 4);
+      grid = std::max<long>(unit, grid / unit * unit);
+      a.grid = static_cast<int32_t>(grid);
+      e = launch_small16(a, d->dtype, p.mfw, stream);
+      break;
+    }
     case kVarDenseItemsF32:
       e = launch_items_f32(a, p.mfw, stream);
       break;
@@ -1039,11 +1099,12 @@ rt3d_status rt3d_dense_pack_size(const rt3d_conv3d_desc *d, uint64_t *bytes) {
   if (st != RT3D_OK) return st;
   if (!bytes) return fail(RT3D_ERR_INVALID_ARG, "bytes must be non-NULL");
   const Geom g = geom_of(d);
-  const Tiling tl = choose_tiling(g);
+  const bool small = small_ok(g);
+  const Tiling tl = small ? small_tiling(g) : choose_tiling(g);
   if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
   std::vector<uint8_t> scratch(static_cast<size_t>(g.c_out) * g.c_in * g.ks * g.es, 0);
   Layout L;
-  build_items_layout(g, tl, scratch.data(), nullptr, L);
+  build_items_layout(g, tl, scratch.data(), nullptr, L, small);
   *bytes = section_offsets(nullptr, g.es, L).total;
   return ok();
 }
@@ -1055,10 +1116,11 @@ rt3d_status rt3d_dense_pack(const rt3d_conv3d_desc *d, const void *w_dense, void
   if (!w_dense || !blob || !info)
     return fail(RT3D_ERR_INVALID_ARG, "w_dense, blob and info must be non-NULL");
   const Geom g = geom_of(d);
-  const Tiling tl = choose_tiling(g);
+  const bool small = small_ok(g);
+  const Tiling tl = small ? small_tiling(g) : choose_tiling(g);
   if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
   Layout L;
-  build_items_layout(g, tl, static_cast<const uint8_t *>(w_dense), nullptr, L);
+  build_items_layout(g, tl, static_cast<const uint8_t *>(w_dense), nullptr, L, small);
   const Sections s = section_offsets(nullptr, g.es, L);
   if (blob_bytes < s.total)
     return fail(RT3D_ERR_BUFFER_TOO_SMALL, "blob needs %llu bytes, got %llu",

@@ -18,6 +18,8 @@ enum Variant : uint32_t {
   kVarDenseItemsF32 = 2, // dense, 16x16x4 f32 MFMA
   kVarKgsUnion16 = 3,    // KGS, 16x16x32 MFMA over the union of a 16-filter tile's items
   kVarKgsExactF32 = 4,   // KGS, 4x4x1 f32 MFMA, exact per 4x4 kernel block
+  kVarSmallDense16 = 5,  // dense, c_in <= 4: wave-private bricks, weights in registers
+  kVarSmallKgs16 = 6,    // KGS, c_in <= 4: as above over the union of the wave tile's items
 };
 
 // Voxel tiling shared by every conv kernel: a workgroup computes a brick of
@@ -94,6 +96,9 @@ struct Launch {
 // with `lds` bytes of dynamic LDS each; 0 when the runtime cannot say.
 int conv_resident(int variant, int dtype, int mfw, size_t lds);
 int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream);
+int launch_small16(const ConvArgs &a, int dtype, int mfw, void *stream);
+size_t small_lds_bytes(const ConvArgs &a);
+int small_resident(const ConvArgs &a, int dtype, int mfw);
 int launch_items_f32(const ConvArgs &a, int mfw, void *stream);
 int launch_kgs_exact_f32(const ConvArgs &a, void *stream);
 int launch_reduce_splits(const ConvArgs &a, int dtype, void *stream);

@@ -390,6 +390,16 @@ __device__ __forceinline__ float4 max4(float4 x, float4 y) {
                      x.w > y.w ? x.w : y.w);
 }
 
+__device__ __forceinline__ float4 add4(float4 x, float4 y) {
+  return make_float4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
+}
+
+__device__ __forceinline__ float4 shfl_xor4(float4 v, int m) {
+  return make_float4(__shfl_xor(v.x, m), __shfl_xor(v.y, m), __shfl_xor(v.z, m),
+                     __shfl_xor(v.w, m));
+}
+
+
 // Walks voxel slots (t, h, w) of a bt x bh x bw box in steps of `step`
 // slots with carries instead of divisions (step is at most 64).
 struct BoxIter {
@@ -642,6 +652,214 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Small-input-channel kernel (c_in <= 4, at most 4 K-steps: a first layer on
+// RGB clips).  Here the per-workgroup fixed cost of the item kernel (halo
+// staging latency, barriers, the LDS output tile) dwarfs the 4 K-steps, so
+// each wave works alone: it keeps its whole weight tile (16*MFW filters x all
+// steps) in registers, owns a double-buffered halo in LDS, and walks bricks
+// of 1 x 2 x 32 output voxels (64 slots, 4 fragments) with the next brick's
+// input loads in flight while it computes and stores the current one.  Max
+// pooling with a 1x2x2 window is done in registers (the h pair is two
+// fragments of the same lane, the w pair two adjacent lanes).
+// Halo rows hold 4 channels (8 bytes); channels >= c_in stay zero.
+// ---------------------------------------------------------------------------
+
+constexpr int kSmallLines = 12;      // halo lines (t, h) per brick: kt * (kh + 1) <= 12
+
+// LL = halo-line elements per lane (hw * c_in <= 64 * LL).
+template <typename T, int MFW, int LL>
+__global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
+  constexpr int kSmallLineLoads = LL;
+  using V8 = std::conditional_t<std::is_same_v<T, __bf16>, bf16x8, f16x8>;
+  constexpr int NF = 4, STEPS = 4;
+  extern __shared__ __align__(16) uint8_t lds[];
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4;
+  const int wave = static_cast<int>(threadIdx.x) >> 6;
+  const int rows = a.ht * a.hh * a.hw;
+  const int buf_bytes = ((rows * 8 + 15) & ~15) + 16;  // + a 16-byte sink for unused lanes
+  uint8_t *mine = lds + wave * 2 * buf_bytes;
+  for (int i = lane; i < 2 * buf_bytes / 16; i += 64)
+    reinterpret_cast<uint4 *>(mine)[i] = make_uint4(0, 0, 0, 0);
+
+  // Work split: wave gw handles wave tile gw % wave_tiles and bricks
+  // gw / wave_tiles + k * (waves / wave_tiles); the host makes the wave
+  // count a multiple of wave_tiles.
+  const int gw = static_cast<int>(blockIdx.x) * 4 + wave;
+  const int nwaves = static_cast<int>(gridDim.x) * 4;
+  const int wt = uniform(gw % a.wave_tiles);
+  const int bstride = uniform(nwaves / a.wave_tiles);
+  int brick = uniform(gw / a.wave_tiles);
+
+  // Weights and item offsets of the whole K loop, in registers.
+  const uint32_t *sp = a.step_ptr + static_cast<long>(wt) * (a.nchunks + 1);
+  const uint32_t s0 = uniform(sp[0]);
+  const int steps = uniform(static_cast<int>(sp[1] - s0));
+  const uint32_t row0 = uniform(a.item_ptr[wt]);
+  const V8 *A = static_cast<const V8 *>(a.a) + lane;
+  const uint2 *IT = reinterpret_cast<const uint2 *>(a.items) + g;
+  V8 ra[STEPS][MFW];
+  uint2 off[STEPS];
+#pragma unroll
+  for (int s = 0; s < STEPS; ++s) {
+    const uint32_t st = s0 + static_cast<uint32_t>(s < steps ? s : 0);
+#pragma unroll
+    for (int i = 0; i < MFW; ++i) ra[s][i] = A[(static_cast<long>(st) * MFW + i) * 64];
+    off[s] = IT[(static_cast<long>(row0) + (st - s0)) * 4];
+  }
+
+  // Let the weight loads land before the brick loop: otherwise the wait
+  // counters at the loop head cannot tell them from the staging loads in
+  // flight and the MFMAs would wait for those.
+  __syncthreads();
+
+  // LDS row of each fragment's voxel slot (slot 16j + n of the 1x2x32 brick).
+  int vb[NF];
+#pragma unroll
+  for (int j = 0; j < NF; ++j) {
+    const int hh = j >> 1, ww = 16 * (j & 1) + (lane & 15);
+    vb[j] = (hh * a.sh * a.hw + ww * a.sw) * 8;
+  }
+
+  // Halo staging: line L = (xt, xh) holds hw voxels x c_in channels that are
+  // contiguous in the channels-last input; lane takes elements lane + 64k.
+  int ex[kSmallLineLoads], ec[kSmallLineLoads];
+  const int line_len = a.hw * a.c_in;
+#pragma unroll
+  for (int k = 0; k < kSmallLineLoads; ++k) {
+    const DivMod d = divmod(lane + 64 * k, a.c_in);
+    ex[k] = d.q;
+    ec[k] = d.r;
+  }
+  const int nlines = a.ht * a.hh;
+  uint16_t sv[kSmallLines][kSmallLineLoads];
+  unsigned long long okbits = 0;  // element (L, k) is inside the input (else it stages a zero)
+  static_assert(kSmallLines * 3 <= 64, "ok bits");
+  const uint16_t *xin = static_cast<const uint16_t *>(a.x);
+  // Staging is branch-free: every lane loads from a clamped in-range address
+  // and selects zero where the element is padding, and writes go to a sink
+  // past the halo rows where the lane has no element, so all loads issue
+  // back to back and the LDS writes wait once.
+  auto issue = [&](int br) {
+    const Brick b = decode_brick(a, br);
+#pragma unroll
+    for (int L = 0; L < kSmallLines; ++L) {
+      const DivMod lt = divmod(L, a.hh);
+      const int zt = b.zt0 + lt.q, zh = b.zh0 + lt.r;
+      const bool line_ok = L < nlines && zt >= 0 && zt < a.t && zh >= 0 && zh < a.h;
+      const int ztc = min(max(zt, 0), a.t - 1), zhc = min(max(zh, 0), a.h - 1);
+      const long base = ((static_cast<long>(b.nb) * a.t + ztc) * a.h + zhc) * a.w;
+#pragma unroll
+      for (int k = 0; k < kSmallLineLoads; ++k) {
+        const int zw = b.zw0 + ex[k];
+        const bool ok = line_ok && lane + 64 * k < line_len && zw >= 0 && zw < a.w;
+        const int zwc = min(max(zw, 0), a.w - 1);
+        sv[L][k] = xin[(base + zwc) * a.c_in + ec[k]];  // selected at commit, after the wait
+        okbits = (okbits & ~(1ull << (L * kSmallLineLoads + k))) |
+                 (static_cast<unsigned long long>(ok) << (L * kSmallLineLoads + k));
+      }
+    }
+  };
+  auto commit = [&](uint8_t *buf) {
+#pragma unroll
+    for (int L = 0; L < kSmallLines; ++L)
+#pragma unroll
+      for (int k = 0; k < kSmallLineLoads; ++k) {
+        const bool mine_el = L < nlines && lane + 64 * k < line_len;
+        const int off = mine_el ? (L * a.hw + ex[k]) * 8 + ec[k] * 2 : buf_bytes - 16;
+        const bool ok = (okbits >> (L * kSmallLineLoads + k)) & 1ull;
+        *reinterpret_cast<uint16_t *>(buf + off) = ok ? sv[L][k] : uint16_t{0};
+      }
+  };
+  auto wave_sync = [] {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+
+  // Bias of this lane's filters.
+  float4 bb[MFW];
+#pragma unroll
+  for (int i = 0; i < MFW; ++i) bb[i] = load_bias4(a, wt * 16 * MFW + 16 * i + 4 * g);
+
+  int cur = 0;
+  if (brick < a.nbricks) {
+    issue(brick);
+    wave_sync();  // zero fill done before the first commit
+    commit(mine);
+  }
+  for (; brick < a.nbricks; brick += bstride) {
+    const int next = brick + bstride;
+    if (next < a.nbricks) issue(next);  // in flight during this brick
+    wave_sync();
+    const uint8_t *buf = mine + cur * buf_bytes;
+    f32x4 acc[MFW][NF];
+#pragma unroll
+    for (int i = 0; i < MFW; ++i)
+#pragma unroll
+      for (int j = 0; j < NF; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+      if (s < steps) {
+#pragma unroll
+        for (int j = 0; j < NF; ++j) {
+          const uint2 lo = *reinterpret_cast<const uint2 *>(buf + vb[j] + off[s].x);
+          const uint2 hi = *reinterpret_cast<const uint2 *>(buf + vb[j] + off[s].y);
+          const V8 bv = __builtin_bit_cast(V8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+#pragma unroll
+          for (int i = 0; i < MFW; ++i) {
+            if constexpr (std::is_same_v<T, __bf16>)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ra[s][i], bv, acc[i][j], 0, 0, 0);
+            else
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ra[s][i], bv, acc[i][j], 0, 0, 0);
+          }
+        }
+      }
+    }
+    // Epilogue: activation per voxel, optional 1x2x2 max, store.
+    const Brick b = decode_brick(a, brick);
+    const int n = lane & 15;
+#pragma unroll
+    for (int i = 0; i < MFW; ++i) {
+      const int m0 = wt * 16 * MFW + 16 * i + 4 * g;
+      if (m0 >= a.c_out) continue;
+      float4 v[NF];
+      bool ok[NF];
+      auto voxel = [&](int j) {
+        return ((static_cast<long>(b.nb) * a.to + b.ot0) * a.ho + b.oh0 + (j >> 1)) * a.wo +
+               b.ow0 + 16 * (j & 1) + n;
+      };
+#pragma unroll
+      for (int j = 0; j < NF; ++j) {
+        const int oh = b.oh0 + (j >> 1), ow = b.ow0 + 16 * (j & 1) + n;
+        ok[j] = b.ot0 < a.to && oh < a.ho && ow < a.wo;
+        const float4 raw = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+        v[j] = ok[j] ? activate4<T>(a, voxel(j), m0, raw, bb[i]) : raw;
+      }
+      if (a.qh == 2) {  // window 1x2x2 (bricks hold whole windows)
+#pragma unroll
+        for (int jw = 0; jw < 2; ++jw) {
+          float4 m = max4(v[jw], v[jw + 2]);
+          m = max4(m, shfl_xor4(m, 1));
+          const int ow = b.ow0 + 16 * jw + n;
+          const int ph = b.oh0 >> 1, pw = ow >> 1;
+          if ((n & 1) == 0 && b.ot0 < a.pto && ph < a.pho && pw < a.pwo)
+            put4<T>(a, ((static_cast<long>(b.nb) * a.pto + b.ot0) * a.pho + ph) * a.pwo + pw, m0, m);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < NF; ++j)
+          if (ok[j]) put4<T>(a, voxel(j), m0, v[j]);
+      }
+    }
+    if (next < a.nbricks) {
+      cur ^= 1;
+      commit(mine + cur * buf_bytes);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // f32 dense item kernel: v_mfma_f32_16x16x4_f32 (full fp32, no reduced
 // precision).  A K-step is 4 items = 16 reduction slots issued as four
 // MFMAs; in MFMA s lane group g supplies channel s of item g, so one
@@ -891,15 +1109,6 @@ __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
 // order, so every run gives the same bits), apply the epilogue per window
 // voxel, and take the max across the wl lanes.  A block covers vpb pooled
 // voxels x cpb filter quads; blockIdx.y picks the filter-quad range.
-__device__ __forceinline__ float4 add4(float4 x, float4 y) {
-  return make_float4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
-}
-
-__device__ __forceinline__ float4 shfl_xor4(float4 v, int m) {
-  return make_float4(__shfl_xor(v.x, m), __shfl_xor(v.y, m), __shfl_xor(v.z, m),
-                     __shfl_xor(v.w, m));
-}
-
 struct ReduceShape {
   int wl, zl, lpo, cpb, vpb, groups;
 };
@@ -1085,6 +1294,56 @@ int conv_resident(int variant, int dtype, int mfw, size_t lds) {
     default:
       return 0;
   }
+}
+
+size_t small_lds_bytes(const ConvArgs &a) {
+  const size_t buf =
+      ((static_cast<size_t>(a.ht) * a.hh * a.hw * 8 + 15) & ~static_cast<size_t>(15)) + 16;
+  return 4 * 2 * buf;  // four waves, two halo buffers each (rows + a 16-byte sink)
+}
+
+template <typename K>
+int launch_small(K kernel, const ConvArgs &a, void *stream) {
+  const hipError_t e = prepare(kernel);
+  if (e != hipSuccess) return e;
+  if (a.grid <= 0) return hipSuccess;
+  hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(a.grid)), dim3(256), small_lds_bytes(a),
+                     static_cast<hipStream_t>(stream), a);
+  return hipGetLastError();
+}
+
+int small_line_loads(const ConvArgs &a) { return a.hw * a.c_in <= 128 ? 2 : 3; }
+
+#define RT3D_SMALL_DISPATCH(FN, ...)                                                     \
+  do {                                                                                   \
+    const int ll = small_line_loads(a);                                                  \
+    if (dtype == RT3D_BF16) {                                                            \
+      if (mfw == 1) return ll == 2 ? FN(small_kernel<__bf16, 1, 2>, __VA_ARGS__)         \
+                                   : FN(small_kernel<__bf16, 1, 3>, __VA_ARGS__);        \
+      if (mfw == 2) return ll == 2 ? FN(small_kernel<__bf16, 2, 2>, __VA_ARGS__)         \
+                                   : FN(small_kernel<__bf16, 2, 3>, __VA_ARGS__);        \
+      if (mfw == 4) return ll == 2 ? FN(small_kernel<__bf16, 4, 2>, __VA_ARGS__)         \
+                                   : FN(small_kernel<__bf16, 4, 3>, __VA_ARGS__);        \
+    } else {                                                                             \
+      if (mfw == 1) return ll == 2 ? FN(small_kernel<_Float16, 1, 2>, __VA_ARGS__)       \
+                                   : FN(small_kernel<_Float16, 1, 3>, __VA_ARGS__);      \
+      if (mfw == 2) return ll == 2 ? FN(small_kernel<_Float16, 2, 2>, __VA_ARGS__)       \
+                                   : FN(small_kernel<_Float16, 2, 3>, __VA_ARGS__);      \
+      if (mfw == 4) return ll == 2 ? FN(small_kernel<_Float16, 4, 2>, __VA_ARGS__)       \
+                                   : FN(small_kernel<_Float16, 4, 3>, __VA_ARGS__);      \
+    }                                                                                    \
+  } while (0)
+
+int launch_small16(const ConvArgs &a, int dtype, int mfw, void *stream) {
+  if (dtype != RT3D_BF16 && dtype != RT3D_F16) return hipErrorInvalidValue;
+  RT3D_SMALL_DISPATCH(launch_small, a, stream);
+  return hipErrorInvalidValue;
+}
+
+int small_resident(const ConvArgs &a, int dtype, int mfw) {
+  const size_t lds = small_lds_bytes(a);
+  RT3D_SMALL_DISPATCH(resident, lds);
+  return 0;
 }
 
 int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream) {

@@ -91,6 +91,29 @@ def test_dense_small_shapes(si, dtype):
     check_full(case, f"dense {tag} {dtype}")
 
 
+# First-layer shapes (c_in <= 4, kernels up to 3x3x3, stride 1) run on the
+# small-input-channel kernel: wave-private bricks of 1x2x32 voxels, weights in
+# registers, optional 1x2x2 pooling in registers.
+SMALL_CIN = [
+    # tag, n, c_in, c_out, thw, k, pad, pool, dtype, sparse, residual
+    ("c1", 1, 3, 64, (4, 10, 70), (3, 3, 3), (1, 1, 1), (1, 2, 2), "bf16", False, False),
+    ("c2", 2, 3, 40, (3, 7, 45), (3, 3, 3), (1, 1, 1), (1, 1, 1), "f16", True, False),
+    ("c3", 1, 4, 20, (2, 6, 33), (1, 3, 3), (0, 1, 1), (1, 1, 1), "bf16", False, True),
+    ("c4", 1, 1, 16, (5, 5, 9), (3, 3, 3), (0, 1, 1), (1, 2, 2), "bf16", True, False),
+    ("c5", 3, 2, 64, (3, 9, 40), (3, 1, 3), (1, 0, 1), (1, 2, 2), "f16", False, True),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(SMALL_CIN)))
+def test_small_input_channel_layers(ci):
+    tag, n, c_in, c_out, thw, k, pad, pool, dtype, sparse, residual = SMALL_CIN[ci]
+    mask = masked(tag, c_out, c_in, k, max(1, (k[0] * k[1] * k[2]) // 3)) if sparse else None
+    case = LayerCase(tag, n, c_in, c_out, thw, k, (1, 1, 1), pad, dtype, mask, residual=residual,
+                     pool=pool)
+    assert case.conv.info.variant in (5, 6), case.conv.info.variant
+    check_full(case, f"small c_in {tag} {dtype} {'kgs' if sparse else 'dense'}")
+
+
 # Kernel groups wider than 4x4 (g_M, g_N in {4, 8, 16}): the planner expands
 # each group mask to its 4x4 blocks, so a 16-filter tile of a g_M = 16 layer
 # walks exactly its group's kept items.
