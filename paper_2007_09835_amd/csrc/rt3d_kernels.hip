@@ -30,6 +30,7 @@ namespace {
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(4 * sizeof(unsigned)))) unsigned u32x4;
 
 template <int... Is, typename F>
 __device__ __forceinline__ void static_for_impl(std::integer_sequence<int, Is...>, F &&f) {
@@ -329,6 +330,18 @@ __device__ __forceinline__ void split_range(const ConvArgs &a, int split, int &c
 // act(acc + bias (+ residual)) for filters m0..m0+3 of unpooled voxel vox.
 // Bias of filters m0..m0+3 (zero where absent).  Loaded once per thread and
 // output column, outside the voxel loops.
+// Completes, at this point, every load that writes v: an empty asm statement
+// that reads a register makes the wait-count insertion wait for it here.
+template <typename V>
+__device__ __forceinline__ void settle(const V &v) {
+  if constexpr (sizeof(V) == 16) {
+    asm volatile("" ::"v"(__builtin_bit_cast(u32x4, v)));
+  } else {
+    static_assert(sizeof(V) == 8, "settle: 8 or 16 bytes");
+    asm volatile("" ::"v"(__builtin_bit_cast(unsigned long long, v)));
+  }
+}
+
 __device__ __forceinline__ float4 load_bias4(const ConvArgs &a, int m0) {
   float r[4] = {0.f, 0.f, 0.f, 0.f};
   if (a.bias && m0 < a.c_out) {
@@ -708,10 +721,22 @@ __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
     off[s] = IT[(static_cast<long>(row0) + (st - s0)) * 4];
   }
 
-  // Let the weight loads land before the brick loop: otherwise the wait
-  // counters at the loop head cannot tell them from the staging loads in
-  // flight and the MFMAs would wait for those.
-  __syncthreads();
+  // Bias of this lane's filters.
+  float4 bb[MFW];
+#pragma unroll
+  for (int i = 0; i < MFW; ++i) bb[i] = load_bias4(a, wt * 16 * MFW + 16 * i + 4 * g);
+
+  // Let these loads land before the brick loop: the wait counters are
+  // in-order, so a register still pending at the loop head would make the
+  // MFMAs and the epilogue wait for every staging load issued after it.
+#pragma unroll
+  for (int s = 0; s < STEPS; ++s) {
+#pragma unroll
+    for (int i = 0; i < MFW; ++i) settle(ra[s][i]);
+    settle(off[s]);
+  }
+#pragma unroll
+  for (int i = 0; i < MFW; ++i) settle(bb[i]);
 
   // LDS row of each fragment's voxel slot (slot 16j + n of the 1x2x32 brick).
   int vb[NF];
@@ -777,11 +802,6 @@ __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   };
 
-  // Bias of this lane's filters.
-  float4 bb[MFW];
-#pragma unroll
-  for (int i = 0; i < MFW; ++i) bb[i] = load_bias4(a, wt * 16 * MFW + 16 * i + 4 * g);
-
   int cur = 0;
   if (brick < a.nbricks) {
     issue(brick);
@@ -789,8 +809,13 @@ __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
     commit(mine);
   }
   for (; brick < a.nbricks; brick += bstride) {
+    // The next brick's loads are in flight during this brick.  The commit
+    // below runs on every path (after the last brick it rewrites the idle
+    // buffer with stale values): a conditional commit would look to the
+    // wait-count insertion like loads that may skip their wait, and it would
+    // then wait for them at the next issue and in the epilogue.
     const int next = brick + bstride;
-    if (next < a.nbricks) issue(next);  // in flight during this brick
+    if (next < a.nbricks) issue(next);
     wave_sync();
     const uint8_t *buf = mine + cur * buf_bytes;
     f32x4 acc[MFW][NF];
@@ -852,10 +877,8 @@ __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
           if (ok[j]) put4<T>(a, voxel(j), m0, v[j]);
       }
     }
-    if (next < a.nbricks) {
-      cur ^= 1;
-      commit(mine + cur * buf_bytes);
-    }
+    cur ^= 1;
+    commit(mine + cur * buf_bytes);
   }
 }
 
