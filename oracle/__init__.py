@@ -33,11 +33,14 @@ def _load():
         lib.oracle_maxpool3d.argtypes = [i] * 11 + [dp, dp]
         lib.oracle_conv3d_points.argtypes = ([i] * 17 + [dp, dp, ctypes.c_void_p, dp, dp, i,
                                               ctypes.c_long, ctypes.c_void_p, dp])
+        lib.oracle_group_reweight.argtypes = ([i] * 7 + [dp, dp] + [ctypes.c_double] * 4 +
+                                              [dp, dp, dp, ctypes.c_void_p, dp, dp])
         lib.oracle_num_threads.argtypes = []
         lib.oracle_set_threads.argtypes = [i]
         lib.oracle_set_threads.restype = None
         for f in (lib.oracle_conv3d_dense, lib.oracle_conv3d_kgs, lib.oracle_kgs_pack,
-                  lib.oracle_maxpool3d, lib.oracle_conv3d_points, lib.oracle_num_threads):
+                  lib.oracle_maxpool3d, lib.oracle_conv3d_points, lib.oracle_num_threads,
+                  lib.oracle_group_reweight):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -180,3 +183,42 @@ def maxpool3d(x, k, stride):
     if rc:
         raise ValueError("oracle_maxpool3d rejected its arguments")
     return y
+
+
+def group_reweight(w, g_m, g_n, norm=2, scope=0, pen=None, lam=1.0, eps=1e-6, tau=0.0, step=1.0,
+                   grad=None):
+    """Group norms and the reweighted group-lasso penalty, float64 (Section 4).
+
+    ``w`` is [c_out][c_in][kt][kh][kw].  scope 0 takes one norm per kernel
+    position of each kernel group (KGS), scope 1 one norm per whole group
+    (vanilla).  ``pen`` holds the current penalty factors, one per norm
+    (None = all ones).  ``grad`` (float64, w's shape) is accumulated into
+    in place when given.  Returns a dict with ``norms`` and ``pen_next``
+    ([P][Q][ks] or [P][Q]), ``reg`` (float), ``mask`` (uint8 [P][Q][ks]) and
+    ``w_prox`` (w's shape).
+    """
+    w = _f64(w)
+    c_out, c_in = w.shape[0], w.shape[1]
+    ks = int(np.prod(w.shape[2:]))
+    p_groups, q_groups = -(-c_out // g_m), -(-c_in // g_n)
+    ushape = (p_groups, q_groups, ks) if scope == 0 else (p_groups, q_groups)
+    p = None if pen is None else _f64(pen)
+    if p is not None and p.shape != ushape:
+        raise ValueError("pen shape %s, want %s" % (p.shape, ushape))
+    if grad is not None and (grad.dtype != np.float64 or grad.shape != w.shape
+                             or not grad.flags["C_CONTIGUOUS"]):
+        raise ValueError("grad must be a C-contiguous float64 array of w's shape")
+    norms = np.empty(ushape, dtype=np.float64)
+    pen_next = np.empty(ushape, dtype=np.float64)
+    mask = np.empty((p_groups, q_groups, ks), dtype=np.uint8)
+    w_prox = np.empty(w.shape, dtype=np.float64)
+    reg = ctypes.c_double()
+    rc = _load().oracle_group_reweight(
+        c_out, c_in, ks, g_m, g_n, norm, scope, _ptr(w), _ptr(p), float(lam), float(eps),
+        float(tau), float(step), _ptr(norms), _ptr(pen_next),
+        ctypes.cast(ctypes.addressof(reg), ctypes.POINTER(ctypes.c_double)), mask.ctypes.data,
+        _ptr(grad), _ptr(w_prox))
+    if rc:
+        raise ValueError("oracle_group_reweight rejected its arguments")
+    return {"norms": norms, "pen_next": pen_next, "reg": reg.value, "mask": mask,
+            "w_prox": w_prox}

@@ -11,6 +11,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "rt3d_oracle.c")
 LIB = os.path.join(HERE, "librt3d_oracle.so")
 CFLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-Wall", "-Wextra", "-Werror"]
+LIBS = ["-lm"]
 
 
 def build_oracle(force: bool = True) -> str:
@@ -18,7 +19,7 @@ def build_oracle(force: bool = True) -> str:
     if not force and os.path.exists(LIB):
         return LIB
     tmp = LIB + ".tmp%d" % os.getpid()
-    subprocess.run(["gcc", *CFLAGS, SRC, "-o", tmp], check=True)
+    subprocess.run(["gcc", *CFLAGS, SRC, "-o", tmp, *LIBS], check=True)
     os.replace(tmp, LIB)
     return LIB
 

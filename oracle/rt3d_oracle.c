@@ -18,6 +18,10 @@
  *     dense layer with the pruned weights removed.
  *   - Section 4: P = ceil(M / g_M), Q = ceil(N / g_N); trailing groups are
  *     partial.
+ *   - Section 4 (regularization-based and reweighted pruning): the l1 / l2
+ *     norm of a group's weights at one kernel position (KGS) or over the
+ *     whole group (vanilla), the penalty term of eq. (4) and the update of
+ *     its penalty factors.
  *
  * Conventions (the paper is silent on them; readings recorded in the design
  * notes):
@@ -37,6 +41,7 @@
 #include <stdint.h>
 #include <stddef.h>
 #include <string.h>
+#include <math.h>
 
 #define ORACLE_OK 0
 #define ORACLE_BAD_ARG 1
@@ -318,6 +323,99 @@ int oracle_maxpool3d(int n, int c, int t, int h, int w, int kt, int kh, int kw,
             ys[(ot * ho + oh) * wo + ow] = best;
         }
     }
+    return ORACLE_OK;
+}
+
+/*
+ * Group norms and the reweighted group-lasso penalty (Section 4).
+ *
+ * Weights w [c_out][c_in][ks] (ks = kt*kh*kw kernel positions), kernel
+ * groups of g_m x g_n kernels, P = ceil(c_out/g_m) by Q = ceil(c_in/g_n)
+ * (trailing groups partial).  A "unit" u is what one norm covers:
+ *   scope 0 (KGS):     one kernel position of one group, u = (p*Q + q)*ks + pos
+ *                      (the norm in the caption of Fig. 2 / eq. (3));
+ *   scope 1 (vanilla): a whole group, u = p*Q + q (the group norm of eq. (2)).
+ * norm = 1 or 2 selects the l1 or l2 norm of the unit's weights:
+ *   n_u = (sum over the unit of |w|^norm)^(1/norm).
+ * With P_u the current penalty factors (pen; NULL means all ones) the call
+ * evaluates
+ *   reg        = lambda * sum_u P_u * n_u        (penalty term of eq. (4))
+ *   pen_next_u = 1 / (n_u^2 + eps)               (reweighting update, Section 4)
+ *   mask       = n_u > tau for every kernel position of the unit (pruning the
+ *                units whose norm has converged to zero), layout [P][Q][ks]
+ *   grad      += lambda * P_u * d n_u / d w      (the penalty's contribution to
+ *                the weight gradient: w / n_u for l2, 0 when n_u = 0; sign(w)
+ *                for l1, 0 at w = 0)
+ *   w_prox     = argmin_z 1/2 |z - w|^2 + step * lambda * sum_u P_u * n_u(z):
+ *                l2: w * max(0, 1 - theta / n_u), 0 when n_u = 0;
+ *                l1: the unit's norm is a sum of |w|, so the map is the
+ *                elementwise sign(w) * max(0, |w| - theta);
+ *                theta = step * lambda * P_u.
+ * Any output may be NULL.  norms and pen_next have one entry per unit.
+ * Sums run in a fixed order (filters, then channels, then positions), float64.
+ */
+static double unit_weight_sum(const double *w, long c_in, long ks, long m0, long m1,
+                              long c0, long c1, long s0, long s1, int norm)
+{
+    double acc = 0.0;
+    for (long m = m0; m < m1; ++m)
+        for (long c = c0; c < c1; ++c)
+            for (long s = s0; s < s1; ++s) {
+                const double v = w[(m * c_in + c) * ks + s];
+                acc += norm == 2 ? v * v : fabs(v);
+            }
+    return acc;
+}
+
+int oracle_group_reweight(int c_out, int c_in, int ks, int g_m, int g_n, int norm, int scope,
+                          const double *w, const double *pen, double lambda, double eps,
+                          double tau, double step, double *norms, double *pen_next,
+                          double *reg, unsigned char *mask, double *grad, double *w_prox)
+{
+    if (c_out <= 0 || c_in <= 0 || ks <= 0 || g_m <= 0 || g_n <= 0) return ORACLE_BAD_ARG;
+    if ((norm != 1 && norm != 2) || (scope != 0 && scope != 1) || !w) return ORACLE_BAD_ARG;
+    if (!(eps > 0.0)) return ORACLE_BAD_ARG;
+    const long P = (c_out + g_m - 1) / g_m, Q = (c_in + g_n - 1) / g_n;
+    const long per_group = scope == 0 ? ks : 1;
+    double total = 0.0;
+    for (long p = 0; p < P; ++p)
+    for (long q = 0; q < Q; ++q)
+    for (long r = 0; r < per_group; ++r) {
+        const long m0 = p * g_m, m1 = m0 + g_m < c_out ? m0 + g_m : c_out;
+        const long c0 = q * g_n, c1 = c0 + g_n < c_in ? c0 + g_n : c_in;
+        const long s0 = scope == 0 ? r : 0, s1 = scope == 0 ? r + 1 : ks;
+        const long u = (p * Q + q) * per_group + r;
+        const double sum = unit_weight_sum(w, c_in, ks, m0, m1, c0, c1, s0, s1, norm);
+        const double n = norm == 2 ? sqrt(sum) : sum;
+        const double pu = pen ? pen[u] : 1.0;
+        total += pu * n;
+        if (norms) norms[u] = n;
+        if (pen_next) pen_next[u] = 1.0 / (n * n + eps);
+        if (mask)
+            for (long s = s0; s < s1; ++s) mask[(p * Q + q) * ks + s] = n > tau ? 1 : 0;
+        const double theta = step * lambda * pu;
+        for (long m = m0; m < m1; ++m)
+        for (long c = c0; c < c1; ++c)
+        for (long s = s0; s < s1; ++s) {
+            const long e = (m * c_in + c) * ks + s;
+            const double v = w[e];
+            const double sgn = v > 0.0 ? 1.0 : (v < 0.0 ? -1.0 : 0.0);
+            if (grad) {
+                if (norm == 2) grad[e] += n > 0.0 ? lambda * pu * v / n : 0.0;
+                else grad[e] += lambda * pu * sgn;
+            }
+            if (w_prox) {
+                if (norm == 2) {
+                    const double f = n > 0.0 ? 1.0 - theta / n : 0.0;
+                    w_prox[e] = f > 0.0 ? v * f : 0.0;
+                } else {
+                    const double a = fabs(v) - theta;
+                    w_prox[e] = a > 0.0 ? sgn * a : 0.0;
+                }
+            }
+        }
+    }
+    if (reg) *reg = lambda * total;
     return ORACLE_OK;
 }
 
