@@ -194,6 +194,79 @@ rt3d_status rt3d_maxpool3d_fwd(int32_t n, int32_t c, int32_t t, int32_t h, int32
                                int32_t st, int32_t sh, int32_t sw, int32_t dtype,
                                const void *x, void *y, void *stream);
 
+/* ------------------------------------------------------------------------
+ * Reweighted group-lasso penalty (Section 4)
+ *
+ * The pruning algorithms of Section 4 penalise the norm of kernel groups: the
+ * regularization-based algorithm adds lambda * sum ||W^G||_g to the training
+ * loss (eq. (3)), and the reweighted algorithm (eq. (4)) multiplies each norm
+ * by a penalty factor P that is reset after every iteration to
+ * 1 / (||W^G||_g^2 + eps), so that large groups are penalised less and small
+ * ones more; after a few iterations the groups whose norm has converged to
+ * zero are pruned.  For KGS sparsity a norm covers the g_M x g_N weights of
+ * one kernel group at one kernel position (Fig. 2 caption); for vanilla
+ * sparsity it covers the whole group.  These norms are called units below:
+ *   scope RT3D_SCOPE_KGS:     P * Q * K_s units, unit (p, q, pos) at index
+ *                             (p*Q + q)*K_s + pos;
+ *   scope RT3D_SCOPE_VANILLA: P * Q units, unit (p, q) at index p*Q + q.
+ * norm = 1 or 2 selects the l1 or l2 norm of the unit's weights (the paper
+ * allows either).
+ * ------------------------------------------------------------------------ */
+
+enum { RT3D_SCOPE_KGS = 0, RT3D_SCOPE_VANILLA = 1 };
+
+typedef struct {
+    int32_t c_out, c_in;      /* M filters, N input channels */
+    int32_t kt, kh, kw;       /* kernel extent, 1..7 each; K_s = kt*kh*kw */
+    int32_t g_m, g_n;         /* kernel-group size, 1..16 each (partial trailing groups) */
+    int32_t dtype;            /* rt3d_dtype of the weights and of w_prox */
+    int32_t norm;             /* 1 or 2 */
+    int32_t scope;            /* RT3D_SCOPE_KGS or RT3D_SCOPE_VANILLA */
+} rt3d_group_desc;
+
+/* Number of units (norms) of a layer for this desc.  Host only. */
+rt3d_status rt3d_group_units(const rt3d_group_desc *desc, int64_t *units);
+
+/* Device workspace (bytes, caller-owned, 4-byte aligned) that
+ * rt3d_group_reweight needs when it is asked for the penalty value reg (one
+ * float per workgroup, summed in a fixed order by a second kernel); 0
+ * otherwise.  Host only. */
+rt3d_status rt3d_group_workspace_size(const rt3d_group_desc *desc, uint64_t *bytes);
+
+/* One pass over device weights w [M][N][kt][kh][kw] (desc->dtype) computing,
+ * for every unit u with current penalty factor P_u (pen[u]; pen == NULL means
+ * all ones) and norm n_u:
+ *   norms[u]    = n_u                                     (float32 [units])
+ *   pen_next[u] = 1 / (n_u^2 + eps)   (the reweighting update; float32 [units])
+ *   *reg        = lambda * sum_u P_u * n_u   (the penalty term of eq. (4);
+ *                                             one float32 in device memory)
+ *   mask        = 1 where n_u > tau, else 0, for every kernel position the
+ *                 unit covers: uint8 [P][Q][K_s], the layout rt3d_kgs_pack
+ *                 takes (pruning what has converged to zero: tau = 0 prunes
+ *                 exactly the zero units)
+ *   grad       += lambda * P_u * d n_u / d w  (float32 [M][N][K_s], accumulated:
+ *                 the penalty's share of the weight gradient; l2: w / n_u, and
+ *                 0 for a zero unit; l1: sign(w), 0 at w = 0)
+ *   w_prox      = the minimiser z of 1/2 |z - w|^2 + step * lambda * sum_u
+ *                 P_u * n_u(z), in desc->dtype (rounded to nearest even):
+ *                 l2: w * max(0, 1 - theta / n_u); l1: sign(w) * max(0, |w| -
+ *                 theta) (the l1 norm of a unit is a sum over its weights);
+ *                 theta = step * lambda * P_u.  A proximal step on the penalty.
+ * Every output pointer may be NULL (not computed).  Norms and sums are
+ * float32 with a fixed summation order, so repeated calls give identical
+ * results.  pen_next may be the same array as pen, and w_prox the same array
+ * as w (in-place updates); no other outputs may overlap each other or the
+ * inputs.  eps must be > 0; lambda, step >= 0; all scalars finite.  A unit's
+ * weights (g_m * g_n * K_s values) must fit the kernel's staging buffer:
+ * g_m * g_n * K_s <= 12288, else RT3D_ERR_UNSUPPORTED.  reg needs workspace
+ * of rt3d_group_workspace_size bytes (RT3D_ERR_BUFFER_TOO_SMALL otherwise).
+ * Asynchronous on `stream`. */
+rt3d_status rt3d_group_reweight(const rt3d_group_desc *desc, const void *w, const float *pen,
+                                float lambda, float eps, float tau, float step,
+                                float *norms, float *pen_next, float *reg, uint8_t *mask,
+                                float *grad, void *w_prox,
+                                void *workspace, uint64_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -969,6 +969,67 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   return ok();
 }
 
+// ---------------------------------------------------------------------------
+// Reweighted group-lasso penalty (Section 4): validation and launch shape
+// ---------------------------------------------------------------------------
+
+constexpr int kGroupMaxUnitElems = 12288;  // g_m * g_n * K_s staged per channel group
+constexpr long kGroupTargetWgs = 2048;     // enough workgroups to keep HBM busy
+
+struct GroupPlan {
+  int P, Q, ks, qb, nqc;
+  long units, wgs;
+  size_t lds;
+  int buf_elems, unit_cap;
+};
+
+bool finite(float v) { return v == v && v - v == 0.f; }
+
+rt3d_status check_group_desc(const rt3d_group_desc *d) {
+  if (!d) return fail(RT3D_ERR_INVALID_ARG, "desc is NULL");
+  if (d->c_out <= 0 || d->c_in <= 0) return fail(RT3D_ERR_INVALID_ARG, "channel counts must be positive");
+  if (d->kt <= 0 || d->kh <= 0 || d->kw <= 0)
+    return fail(RT3D_ERR_INVALID_ARG, "kernel extents must be positive");
+  if (d->kt > 7 || d->kh > 7 || d->kw > 7)
+    return fail(RT3D_ERR_UNSUPPORTED, "kernel extents above 7 are not supported");
+  if (d->g_m <= 0 || d->g_n <= 0) return fail(RT3D_ERR_INVALID_ARG, "group sizes must be positive");
+  if (d->g_m > 16 || d->g_n > 16) return fail(RT3D_ERR_UNSUPPORTED, "group sizes above 16 are not supported");
+  if (d->dtype != RT3D_F32 && d->dtype != RT3D_BF16 && d->dtype != RT3D_F16)
+    return fail(RT3D_ERR_INVALID_ARG, "unknown dtype %d", d->dtype);
+  if (d->norm != 1 && d->norm != 2) return fail(RT3D_ERR_INVALID_ARG, "norm must be 1 or 2, got %d", d->norm);
+  if (d->scope != RT3D_SCOPE_KGS && d->scope != RT3D_SCOPE_VANILLA)
+    return fail(RT3D_ERR_INVALID_ARG, "unknown scope %d", d->scope);
+  const long ks = static_cast<long>(d->kt) * d->kh * d->kw;
+  if (static_cast<long>(d->g_m) * d->g_n * ks > kGroupMaxUnitElems)
+    return fail(RT3D_ERR_UNSUPPORTED, "g_m * g_n * K_s = %ld exceeds %d", static_cast<long>(d->g_m) * d->g_n * ks,
+                kGroupMaxUnitElems);
+  if (static_cast<double>(d->c_out) * d->c_in * ks > 2.0e9)
+    return fail(RT3D_ERR_UNSUPPORTED, "weight tensor too large");
+  return RT3D_OK;
+}
+
+GroupPlan group_plan(const rt3d_group_desc *d) {
+  GroupPlan g;
+  g.ks = d->kt * d->kh * d->kw;
+  g.P = (d->c_out + d->g_m - 1) / d->g_m;
+  g.Q = (d->c_in + d->g_n - 1) / d->g_n;
+  g.units = static_cast<long>(g.P) * g.Q * (d->scope == RT3D_SCOPE_KGS ? g.ks : 1);
+  const int per_q = d->g_m * d->g_n * g.ks;                        // staged floats per channel group
+  const int per_q_units = d->scope == RT3D_SCOPE_KGS ? g.ks : 1;
+  // staged block + two unit arrays + the reduction buffer within 64 KB of LDS
+  // (>= 1 channel group after validation)
+  const int lds_cap = std::min(kGroupMaxUnitElems / per_q,
+                               (65536 - 256 * 4) / (4 * (per_q + 2 * per_q_units)));
+  const long want = (static_cast<long>(g.P) * g.Q + kGroupTargetWgs - 1) / kGroupTargetWgs;
+  g.qb = static_cast<int>(std::min<long>({std::max<long>(want, 1), lds_cap, g.Q}));
+  g.nqc = (g.Q + g.qb - 1) / g.qb;
+  g.wgs = static_cast<long>(g.P) * g.nqc;
+  g.buf_elems = per_q * g.qb;
+  g.unit_cap = per_q_units * g.qb;
+  g.lds = sizeof(float) * (static_cast<size_t>(g.buf_elems) + 2 * static_cast<size_t>(g.unit_cap) + 256);
+  return g;
+}
+
 }  // namespace
 }  // namespace rt3d
 
@@ -1154,6 +1215,81 @@ rt3d_status rt3d_maxpool3d_fwd(int32_t n, int32_t c, int32_t t, int32_t h, int32
     return fail(RT3D_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
   const int to = (t - kt) / st + 1, ho = (h - kh) / sh + 1, wo = (w - kw) / sw + 1;
   const int e = launch_maxpool(n, c, t, h, w, kt, kh, kw, st, sh, sw, to, ho, wo, dtype, x, y, stream);
+  if (e != hipSuccess)
+    return fail(RT3D_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(static_cast<hipError_t>(e)));
+  return ok();
+}
+
+
+rt3d_status rt3d_group_units(const rt3d_group_desc *d, int64_t *units) {
+  const rt3d_status st = check_group_desc(d);
+  if (st != RT3D_OK) return st;
+  if (!units) return fail(RT3D_ERR_INVALID_ARG, "units must be non-NULL");
+  *units = group_plan(d).units;
+  return ok();
+}
+
+rt3d_status rt3d_group_workspace_size(const rt3d_group_desc *d, uint64_t *bytes) {
+  const rt3d_status st = check_group_desc(d);
+  if (st != RT3D_OK) return st;
+  if (!bytes) return fail(RT3D_ERR_INVALID_ARG, "bytes must be non-NULL");
+  *bytes = align_up(static_cast<uint64_t>(group_plan(d).wgs) * sizeof(float), kAlign);
+  return ok();
+}
+
+rt3d_status rt3d_group_reweight(const rt3d_group_desc *d, const void *w, const float *pen,
+                                float lambda, float eps, float tau, float step, float *norms,
+                                float *pen_next, float *reg, uint8_t *mask, float *grad,
+                                void *w_prox, void *workspace, uint64_t workspace_bytes,
+                                void *stream) {
+  const rt3d_status st = check_group_desc(d);
+  if (st != RT3D_OK) return st;
+  if (!w) return fail(RT3D_ERR_INVALID_ARG, "w must be non-NULL");
+  if (!finite(lambda) || !finite(eps) || !finite(tau) || !finite(step))
+    return fail(RT3D_ERR_INVALID_ARG, "lambda, eps, tau and step must be finite");
+  if (!(eps > 0.f)) return fail(RT3D_ERR_INVALID_ARG, "eps must be > 0");
+  if (lambda < 0.f || step < 0.f) return fail(RT3D_ERR_INVALID_ARG, "lambda and step must be >= 0");
+  const int es = esize_of(d->dtype);
+  auto misaligned = [](const void *p, uintptr_t a) {
+    return p && (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0;
+  };
+  if (misaligned(w, es) || misaligned(w_prox, es) || misaligned(pen, 4) || misaligned(norms, 4) ||
+      misaligned(pen_next, 4) || misaligned(reg, 4) || misaligned(grad, 4) || misaligned(workspace, 4))
+    return fail(RT3D_ERR_INVALID_ARG, "pointers must be aligned to their element size");
+  const GroupPlan g = group_plan(d);
+  const uint64_t need = static_cast<uint64_t>(g.wgs) * sizeof(float);
+  if (reg && (!workspace || workspace_bytes < need))
+    return fail(RT3D_ERR_BUFFER_TOO_SMALL, "reg needs %llu bytes of workspace, got %llu",
+                static_cast<unsigned long long>(need),
+                static_cast<unsigned long long>(workspace ? workspace_bytes : 0));
+  if (!norms && !pen_next && !reg && !mask && !grad && !w_prox) return ok();
+  GroupArgs a{};
+  a.w = w;
+  a.pen = pen;
+  a.norms = norms;
+  a.pen_next = pen_next;
+  a.partial = reg ? static_cast<float *>(workspace) : nullptr;
+  a.grad = grad;
+  a.mask = mask;
+  a.w_prox = w_prox;
+  a.M = d->c_out;
+  a.N = d->c_in;
+  a.ks = g.ks;
+  a.gm = d->g_m;
+  a.gn = d->g_n;
+  a.P = g.P;
+  a.Q = g.Q;
+  a.qb = g.qb;
+  a.nqc = g.nqc;
+  a.buf_elems = g.buf_elems;
+  a.unit_cap = g.unit_cap;
+  a.lambda = lambda;
+  a.eps = eps;
+  a.tau = tau;
+  a.step = step;
+  int e = launch_group_reweight(a, d->dtype, d->norm, d->scope, g.lds, stream);
+  if (e == hipSuccess && reg)
+    e = launch_reg_finalize(a.partial, static_cast<int>(g.wgs), lambda, reg, stream);
   if (e != hipSuccess)
     return fail(RT3D_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(static_cast<hipError_t>(e)));
   return ok();

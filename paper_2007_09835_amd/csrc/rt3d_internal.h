@@ -91,6 +91,25 @@ struct Launch {
   int order;  // ConvArgs::order
 };
 
+// Group norms / reweighted group-lasso penalty (Section 4).  A workgroup owns
+// filter group p and channel groups [qc*qb, qc*qb + qb) of one layer's
+// [M][N][ks] weights; blockIdx.x = p * nqc + qc.
+struct GroupArgs {
+  const void *w;
+  const float *pen;   // current penalty factor per unit, or NULL (all ones)
+  float *norms;       // per unit, or NULL
+  float *pen_next;    // per unit, or NULL
+  float *partial;     // per workgroup sum of pen * norm, or NULL
+  float *grad;        // [M][N][ks] fp32, accumulated, or NULL
+  uint8_t *mask;      // [P][Q][ks], or NULL
+  void *w_prox;       // [M][N][ks] in the weight dtype, or NULL
+  int32_t M, N, ks, gm, gn, P, Q;
+  int32_t qb, nqc;    // channel groups per workgroup, workgroups per filter group
+  int32_t buf_elems;  // LDS floats reserved for the staged block (gm * qb * gn * ks)
+  int32_t unit_cap;   // LDS floats reserved per unit array (qb * ks, or qb for vanilla)
+  float lambda, eps, tau, step;
+};
+
 // Kernel launchers (rt3d_kernels.hip).  Return hipSuccess or the launch error.
 // Workgroups of the conv kernel for (variant, dtype, mfw) that fit on one CU
 // with `lds` bytes of dynamic LDS each; 0 when the runtime cannot say.
@@ -102,6 +121,9 @@ int small_resident(const ConvArgs &a, int dtype, int mfw);
 int launch_items_f32(const ConvArgs &a, int mfw, void *stream);
 int launch_kgs_exact_f32(const ConvArgs &a, void *stream);
 int launch_reduce_splits(const ConvArgs &a, int dtype, void *stream);
+int launch_group_reweight(const GroupArgs &a, int dtype, int norm, int scope, size_t lds,
+                          void *stream);
+int launch_reg_finalize(const float *partial, int n, float lambda, float *reg, void *stream);
 int launch_maxpool(int n, int c, int t, int h, int w, int kt, int kh, int kw, int st, int sh,
                    int sw, int to, int ho, int wo, int dtype, const void *x, void *y, void *stream);
 

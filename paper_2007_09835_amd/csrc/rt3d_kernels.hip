@@ -1250,6 +1250,168 @@ __global__ __launch_bounds__(256) void maxpool_kernel(const T *__restrict__ x, T
   }
 }
 
+// ---------------------------------------------------------------------------
+// Group norms and the reweighted group-lasso penalty (Section 4).
+// A "unit" is what one norm covers: one kernel position of one kernel group
+// (KGS) or a whole group (vanilla).  A workgroup owns filter group p and qb
+// consecutive channel groups; in the [M][N][ks] weight tensor each of the
+// group's g_m filter rows holds that block as one contiguous run of
+// (channels x ks) elements, so the block is staged into LDS as fp32 with
+// coalesced loads, every norm becomes a short sum over LDS, and the gradient
+// and proximal outputs go back out in the same coalesced order.  Each unit
+// is summed by one thread (KGS) or one wave with a fixed butterfly (vanilla),
+// and the workgroup's penalty sum is a fixed tree: the results do not depend
+// on timing.  The whole block is in LDS before anything is written, so the
+// proximal output may overwrite the weights in place.
+// ---------------------------------------------------------------------------
+
+template <int NORM>
+__device__ __forceinline__ float norm_term(float v) {
+  return NORM == 2 ? v * v : fabsf(v);
+}
+
+template <typename T, int NORM, bool VANILLA>
+__global__ __launch_bounds__(256) void group_reweight_kernel(GroupArgs a) {
+  extern __shared__ __align__(16) float gl[];
+  float *buf = gl;                        // [gme][len] staged weights
+  float *unorm = gl + a.buf_elems;        // norm of each unit of the block
+  float *ulp = unorm + a.unit_cap;        // lambda * penalty factor of each unit
+  float *red = ulp + a.unit_cap;          // [256] penalty-sum reduction
+  const int tid = static_cast<int>(threadIdx.x);
+  const int blk = static_cast<int>(blockIdx.x);
+  const int p = blk / a.nqc, qc = blk - p * a.nqc;
+  const int m0 = p * a.gm, gme = min(a.gm, a.M - m0);
+  const int c0 = qc * a.qb * a.gn, c1 = min(a.N, c0 + a.qb * a.gn);
+  const int len = (c1 - c0) * a.ks;      // staged elements per filter row
+  const int span = a.gn * a.ks;          // elements of one channel group in a row
+  const int nq = (c1 - c0 + a.gn - 1) / a.gn;
+  const int q0 = qc * a.qb;
+  const int total = gme * len;
+  const T *src = static_cast<const T *>(a.w);
+  const long row0 = static_cast<long>(m0) * a.N * a.ks + static_cast<long>(c0) * a.ks;
+  const long pitch = static_cast<long>(a.N) * a.ks;  // elements between filter rows
+
+  // Stage: four loads in flight per thread per round.
+  for (int base = 0; base < total; base += 1024) {
+    float v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int idx = base + k * 256 + tid;
+      v[k] = 0.f;
+      if (idx < total) {
+        const DivMod d = divmod(idx, len);
+        v[k] = to_f32(src[row0 + d.q * pitch + d.r]);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int idx = base + k * 256 + tid;
+      if (idx < total) buf[idx] = v[k];
+    }
+  }
+  __syncthreads();
+
+  float local = 0.f;  // this thread's share of sum(pen * norm)
+  if constexpr (!VANILLA) {
+    for (int u = tid; u < nq * a.ks; u += 256) {
+      const DivMod d = divmod(u, a.ks);
+      const int ql = d.q, pos = d.r;
+      const int gne = min(a.gn, (c1 - c0) - ql * a.gn);
+      float acc = 0.f;
+      for (int i = 0; i < gme; ++i) {
+        const float *col = buf + i * len + ql * span + pos;
+        for (int j = 0; j < gne; ++j) acc += norm_term<NORM>(col[j * a.ks]);
+      }
+      const float n = NORM == 2 ? sqrtf(acc) : acc;
+      const long gu = (static_cast<long>(p) * a.Q + q0 + ql) * a.ks + pos;
+      const float pu = a.pen ? a.pen[gu] : 1.f;
+      local += pu * n;
+      if (a.norms) a.norms[gu] = n;
+      if (a.pen_next) a.pen_next[gu] = 1.f / (n * n + a.eps);
+      if (a.mask) a.mask[gu] = n > a.tau ? 1 : 0;
+      unorm[u] = n;
+      ulp[u] = a.lambda * pu;
+    }
+  } else {
+    const int wave = tid >> 6, lane = tid & 63;
+    for (int ql = wave; ql < nq; ql += 4) {
+      const int cnt = min(a.gn, (c1 - c0) - ql * a.gn) * a.ks;  // contiguous per row
+      float acc = 0.f;
+      for (int i = 0; i < gme; ++i) {
+        const float *run = buf + i * len + ql * span;
+        for (int r = lane; r < cnt; r += 64) acc += norm_term<NORM>(run[r]);
+      }
+      // Butterfly: every lane ends with the same sum (each step adds the
+      // same two values in either order).
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+      const float n = NORM == 2 ? sqrtf(acc) : acc;
+      const long gq = static_cast<long>(p) * a.Q + q0 + ql;
+      const float pu = a.pen ? a.pen[gq] : 1.f;
+      if (lane == 0) {
+        local += pu * n;
+        if (a.norms) a.norms[gq] = n;
+        if (a.pen_next) a.pen_next[gq] = 1.f / (n * n + a.eps);
+        unorm[ql] = n;
+        ulp[ql] = a.lambda * pu;
+      }
+      if (a.mask)
+        for (int r = lane; r < a.ks; r += 64) a.mask[gq * a.ks + r] = n > a.tau ? 1 : 0;
+    }
+  }
+
+  red[tid] = local;
+  __syncthreads();  // also publishes unorm / ulp
+  if (a.partial) {
+    for (int off = 128; off > 0; off >>= 1) {
+      if (tid < off) red[tid] += red[tid + off];
+      __syncthreads();
+    }
+    if (tid == 0) a.partial[blk] = red[0];
+  }
+
+  if (a.grad || a.w_prox) {
+    T *dst = static_cast<T *>(a.w_prox);
+    for (int idx = tid; idx < total; idx += 256) {
+      const DivMod d = divmod(idx, len);
+      const DivMod e = divmod(d.r, span);
+      const int u = VANILLA ? e.q : e.q * a.ks + divmod(e.r, a.ks).r;
+      const float v = buf[idx], n = unorm[u], lp = ulp[u];
+      const long gi = row0 + d.q * pitch + d.r;
+      const float sgn = v > 0.f ? 1.f : (v < 0.f ? -1.f : 0.f);
+      if (a.grad) a.grad[gi] += NORM == 2 ? (n > 0.f ? lp * v / n : 0.f) : lp * sgn;
+      if (dst) {
+        const float theta = a.step * lp;
+        float z;
+        if constexpr (NORM == 2) {
+          const float f = n > 0.f ? 1.f - theta / n : 0.f;
+          z = f > 0.f ? v * f : 0.f;
+        } else {
+          const float m = fabsf(v) - theta;
+          z = m > 0.f ? sgn * m : 0.f;
+        }
+        dst[gi] = static_cast<T>(z);
+      }
+    }
+  }
+}
+
+// reg = lambda * sum of the per-workgroup partial sums, in a fixed order.
+__global__ __launch_bounds__(256) void reg_finalize_kernel(const float *partial, int n,
+                                                           float lambda, float *reg) {
+  __shared__ float red[256];
+  const int tid = static_cast<int>(threadIdx.x);
+  float s = 0.f;
+  for (int i = tid; i < n; i += 256) s += partial[i];
+  red[tid] = s;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if (tid < off) red[tid] += red[tid + off];
+    __syncthreads();
+  }
+  if (tid == 0) *reg = lambda * red[0];
+}
+
 size_t halo_bytes(const ConvArgs &a) {
   const size_t halo = static_cast<size_t>(a.ht) * a.hh * a.hw * a.row;
   if (a.splits > 1) return halo;  // partials are stored from registers
@@ -1431,6 +1593,34 @@ int launch_maxpool(int n, int c, int t, int h, int w, int kt, int kh, int kw, in
     if (c % 8 == 0) RT3D_POOL(_Float16, 8); else RT3D_POOL(_Float16, 1);
   }
 #undef RT3D_POOL
+  return hipGetLastError();
+}
+
+int launch_group_reweight(const GroupArgs &a, int dtype, int norm, int scope, size_t lds,
+                          void *stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const dim3 grid(static_cast<unsigned>(a.P) * static_cast<unsigned>(a.nqc));
+#define RT3D_GROUP(T)                                                                        \
+  do {                                                                                       \
+    if (norm == 2 && scope == 0)                                                             \
+      hipLaunchKernelGGL((group_reweight_kernel<T, 2, false>), grid, dim3(256), lds, s, a);  \
+    else if (norm == 2)                                                                      \
+      hipLaunchKernelGGL((group_reweight_kernel<T, 2, true>), grid, dim3(256), lds, s, a);   \
+    else if (scope == 0)                                                                     \
+      hipLaunchKernelGGL((group_reweight_kernel<T, 1, false>), grid, dim3(256), lds, s, a);  \
+    else                                                                                     \
+      hipLaunchKernelGGL((group_reweight_kernel<T, 1, true>), grid, dim3(256), lds, s, a);   \
+  } while (0)
+  if (dtype == RT3D_F32) RT3D_GROUP(float);
+  else if (dtype == RT3D_BF16) RT3D_GROUP(__bf16);
+  else RT3D_GROUP(_Float16);
+#undef RT3D_GROUP
+  return hipGetLastError();
+}
+
+int launch_reg_finalize(const float *partial, int n, float lambda, float *reg, void *stream) {
+  hipLaunchKernelGGL(reg_finalize_kernel, dim3(1), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     partial, n, lambda, reg);
   return hipGetLastError();
 }
 

@@ -38,8 +38,11 @@ EXPORTED = (
     "rt3d_status_string", "rt3d_last_error_detail", "rt3d_conv3d_out_shape",
     "rt3d_kgs_pack_size", "rt3d_kgs_pack", "rt3d_kgs_unpack", "rt3d_conv3d_workspace_size",
     "rt3d_kgs_conv3d_fwd", "rt3d_dense_pack_size", "rt3d_dense_pack", "rt3d_conv3d_dense_fwd",
-    "rt3d_maxpool3d_fwd",
+    "rt3d_maxpool3d_fwd", "rt3d_group_units", "rt3d_group_workspace_size", "rt3d_group_reweight",
 )
+
+RT3D_SCOPE_KGS = 0
+RT3D_SCOPE_VANILLA = 1
 
 
 class Rt3dError(RuntimeError):
@@ -67,6 +70,11 @@ class PackInfo(ctypes.Structure):
         ("kept_positions", ctypes.c_uint64), ("kept_weights", ctypes.c_uint64),
         ("plan", ctypes.c_uint64 * 16),
     ]
+
+
+class GroupDesc(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int32) for name in (
+        "c_out", "c_in", "kt", "kh", "kw", "g_m", "g_n", "dtype", "norm", "scope")]
 
 
 _lib = None
@@ -99,6 +107,10 @@ def load():
         "rt3d_dense_pack": ([D, vp, vp, u64, I], ctypes.c_int),
         "rt3d_conv3d_dense_fwd": ([D, I, vp, vp, vp, vp, vp, vp, u64, vp], ctypes.c_int),
         "rt3d_maxpool3d_fwd": ([i32] * 12 + [vp, vp, vp], ctypes.c_int),
+        "rt3d_group_units": ([P(GroupDesc), P(ctypes.c_int64)], ctypes.c_int),
+        "rt3d_group_workspace_size": ([P(GroupDesc), P(u64)], ctypes.c_int),
+        "rt3d_group_reweight": ([P(GroupDesc), vp, vp] + [ctypes.c_float] * 4 + [vp] * 7 +
+                                [u64, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -255,3 +267,38 @@ def canonical_sections(info: PackInfo, blob: np.ndarray, np_dtype) -> Tuple[np.n
         off, nb = info.canon_off[i], info.canon_bytes[i]
         return blob[off:off + nb].view(dt)
     return sec(0, np.uint32), sec(1, np.uint16), sec(2, np.uint64), sec(3, np_dtype)
+
+
+def make_group_desc(c_out, c_in, k=(3, 3, 3), g=(4, 4), dtype="f32", norm=2,
+                    scope=RT3D_SCOPE_KGS) -> GroupDesc:
+    """Fill an rt3d_group_desc."""
+    code = DTYPE_CODES[dtype] if isinstance(dtype, str) else int(dtype)
+    return GroupDesc(c_out, c_in, *k, g[0], g[1], code, norm, scope)
+
+
+def rt3d_group_units(desc: GroupDesc) -> int:
+    out = ctypes.c_int64()
+    _check(load().rt3d_group_units(ctypes.byref(desc), ctypes.byref(out)))
+    return out.value
+
+
+def rt3d_group_workspace_size(desc: GroupDesc) -> int:
+    out = ctypes.c_uint64()
+    _check(load().rt3d_group_workspace_size(ctypes.byref(desc), ctypes.byref(out)))
+    return out.value
+
+
+def rt3d_group_reweight(desc: GroupDesc, w, pen=None, lam=1.0, eps=1e-6, tau=0.0, step=1.0,
+                        norms=None, pen_next=None, reg=None, mask=None, grad=None, w_prox=None,
+                        workspace=None, stream=None) -> None:
+    """Group norms / reweighted penalty over device weights ``w``
+    [c_out, c_in, kt, kh, kw]; every output is an optional device tensor
+    (float32 per unit, a float32 scalar ``reg``, uint8 mask [P, Q, K_s],
+    float32 ``grad`` and ``w_prox`` of w's shape and dtype)."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(load().rt3d_group_reweight(
+        ctypes.byref(desc), _dev_ptr(w, "w"), _dev_ptr(pen, "pen"), float(lam), float(eps),
+        float(tau), float(step), _dev_ptr(norms, "norms"), _dev_ptr(pen_next, "pen_next"),
+        _dev_ptr(reg, "reg"), _dev_ptr(mask, "mask"), _dev_ptr(grad, "grad"),
+        _dev_ptr(w_prox, "w_prox"), _dev_ptr(workspace, "workspace"), ws_bytes,
+        _stream_ptr(stream)))

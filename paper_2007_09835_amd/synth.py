@@ -278,6 +278,20 @@ def kaiming(rng: np.random.Generator, c_out: int, c_in: int, k: Tuple[int, int, 
     return rng.normal(0.0, np.sqrt(2.0 / fan_in), size=(c_out, c_in, *k))
 
 
+def unit_scaled_weights(rng: np.random.Generator, c_out: int, c_in: int, k: Tuple[int, int, int],
+                        g: Tuple[int, int], lo: float = 0.02) -> np.ndarray:
+    """Kaiming-normal weights with one log-uniform scale in [lo, 1] per kernel
+    group and kernel position, standing in for trained weights whose group
+    norms spread over orders of magnitude (the input of the group-lasso
+    penalty; no trained weights are available)."""
+    w = kaiming(rng, c_out, c_in, k)
+    p_groups, q_groups = -(-c_out // g[0]), -(-c_in // g[1])
+    ks = k[0] * k[1] * k[2]
+    scale = np.exp(rng.uniform(np.log(lo), 0.0, size=(p_groups, q_groups, ks)))
+    full = np.repeat(np.repeat(scale, g[0], axis=0)[:c_out], g[1], axis=1)[:, :c_in]
+    return w * full.reshape(c_out, c_in, *k)
+
+
 @dataclasses.dataclass
 class LayerData:
     layer: ConvLayer

@@ -208,3 +208,53 @@ def test_error_paths():
     assert st == rt3d.RT3D_ERR_INVALID_ARG
     assert lib.rt3d_status_string(99)
     assert lib.rt3d_status_string(rt3d.RT3D_ERR_HIP) == b"HIP runtime error"
+
+
+def test_group_units_and_workspace():
+    d = rt3d.make_group_desc(9, 6, k=(1, 3, 3), g=(4, 4))
+    assert rt3d.rt3d_group_units(d) == 3 * 2 * 9
+    d.scope = rt3d.RT3D_SCOPE_VANILLA
+    assert rt3d.rt3d_group_units(d) == 3 * 2
+    # one workgroup per filter group and block of channel groups, a float each
+    c5 = rt3d.make_group_desc(512, 512, g=(4, 4), dtype="bf16")
+    ws = rt3d.rt3d_group_workspace_size(c5)
+    assert ws % 256 == 0 and 4 * 2048 <= ws <= 4 * 4096
+
+
+def test_group_reweight_error_paths():
+    lib = rt3d.load()
+    good = rt3d.make_group_desc(8, 8, g=(4, 4), dtype="f32")
+
+    def call(desc, w=256, eps=1e-6, lam=1.0, step=1.0, tau=0.0, reg=None, ws=None, ws_bytes=0,
+             norms=None, wp=None):
+        return lib.rt3d_group_reweight(ctypes.byref(desc), w, None, lam, eps, tau, step, norms,
+                                       None, reg, None, None, wp, ws, ws_bytes, None)
+
+    def desc(**kw):
+        d = rt3d.GroupDesc.from_buffer_copy(good)
+        for k, v in kw.items():
+            setattr(d, k, v)
+        return d
+
+    assert call(desc(norm=3)) == rt3d.RT3D_ERR_INVALID_ARG
+    assert call(desc(scope=2)) == rt3d.RT3D_ERR_INVALID_ARG
+    assert call(desc(dtype=9)) == rt3d.RT3D_ERR_INVALID_ARG
+    assert call(desc(c_out=0)) == rt3d.RT3D_ERR_INVALID_ARG
+    assert call(desc(g_m=0)) == rt3d.RT3D_ERR_INVALID_ARG
+    assert call(desc(g_n=17)) == rt3d.RT3D_ERR_UNSUPPORTED
+    assert call(desc(kt=8)) == rt3d.RT3D_ERR_UNSUPPORTED
+    # one unit's weights must fit the staging buffer: 16 * 16 * 49 > 12288
+    assert call(desc(g_m=16, g_n=16, kt=1, kh=7, kw=7)) == rt3d.RT3D_ERR_UNSUPPORTED
+    assert call(good, w=None) == rt3d.RT3D_ERR_INVALID_ARG
+    assert call(good, eps=0.0) == rt3d.RT3D_ERR_INVALID_ARG
+    assert call(good, eps=float("nan")) == rt3d.RT3D_ERR_INVALID_ARG
+    assert call(good, lam=-1.0) == rt3d.RT3D_ERR_INVALID_ARG
+    assert call(good, step=-1.0) == rt3d.RT3D_ERR_INVALID_ARG
+    assert call(good, tau=float("inf")) == rt3d.RT3D_ERR_INVALID_ARG
+    assert call(good, norms=258) == rt3d.RT3D_ERR_INVALID_ARG          # misaligned float*
+    assert call(desc(dtype=rt3d.RT3D_BF16), wp=257) == rt3d.RT3D_ERR_INVALID_ARG
+    # the penalty value needs the per-workgroup workspace
+    assert call(good, reg=256) == rt3d.RT3D_ERR_BUFFER_TOO_SMALL
+    assert call(good, reg=256, ws=512, ws_bytes=2) == rt3d.RT3D_ERR_BUFFER_TOO_SMALL
+    # nothing requested: nothing launched
+    assert call(good) == rt3d.RT3D_OK
