@@ -46,6 +46,9 @@ def parse():
     p.add_argument("--report", default=None, help="write per-layer results to this JSON file")
     p.add_argument("--profile-layer", default=None,
                    help="only launch this layer's sparse conv --layer-reps times (for rocprofv3)")
+    p.add_argument("--profile-reweight", default=None, metavar="LAYER",
+                   help="launch only the reweight pass over this C3D layer's weights "
+                        "(bf16, all outputs) --layer-reps times, for rocprofv3")
     p.add_argument("--suite", default=None, metavar="PATH",
                    help="instead of the headline line, run the per-config measurement suite "
                         "(single layers, R(2+1)D, batch-32 rate sweep, warm/cold latency, oracle "
@@ -228,6 +231,97 @@ def latency(torch, fn, iters, stream, flush=None):
     return {"p10": pct(times, 10), "p50": pct(times, 50), "p90": pct(times, 90)}
 
 
+def reweight_layer(torch, layer, dtype, full):
+    """Device tensors and a launcher for one reweight pass over `layer`'s
+    weights (structured synthetic weights, KGS scope, l2 norm).  `full` adds
+    the gradient and proximal outputs to norms / update / mask / penalty."""
+    from paper_2007_09835_amd import rt3d, synth
+    l = layer
+    g = (4, 4)
+    desc = rt3d.make_group_desc(l.c_out, l.c_in, l.k, g, dtype, 2, rt3d.RT3D_SCOPE_KGS)
+    w64 = synth.unit_scaled_weights(synth.rng_for("bench-reweight", l.name), l.c_out, l.c_in,
+                                    l.k, g)
+    w_t = synth.to_dtype(w64, dtype)
+    w = w_t.cuda()
+    units = rt3d.rt3d_group_units(desc)
+    P, Q = -(-l.c_out // g[0]), -(-l.c_in // g[1])
+    ks = l.k[0] * l.k[1] * l.k[2]
+    t = {"pen": torch.ones(units, device="cuda"), "norms": torch.empty(units, device="cuda"),
+         "pen_next": torch.empty(units, device="cuda"), "reg": torch.empty(1, device="cuda"),
+         "mask": torch.empty((P, Q, ks), dtype=torch.uint8, device="cuda"),
+         "ws": torch.zeros(rt3d.rt3d_group_workspace_size(desc) // 4, device="cuda")}
+    if full:
+        t["grad"] = torch.zeros(w.shape, device="cuda")
+        t["w_prox"] = torch.empty_like(w)
+    lam, eps, tau, step = 1e-5, 1e-6, 1e-4, 1.0
+
+    def fn():
+        rt3d.rt3d_group_reweight(desc, w, t["pen"], lam, eps, tau, step, norms=t["norms"],
+                                 pen_next=t["pen_next"], reg=t["reg"], mask=t["mask"],
+                                 grad=t.get("grad"), w_prox=t.get("w_prox"), workspace=t["ws"])
+    es = w.element_size()
+    nw = w.numel()
+    nbytes = es * nw + 4 * units + 8 * units + P * Q * ks
+    if full:
+        nbytes += 8 * nw + es * nw
+    return {"fn": fn, "bytes": nbytes, "w_t": w_t, "t": t, "lam": lam, "eps": eps, "tau": tau,
+            "step": step, "units": units}
+
+
+def reweight_suite(torch, stream, iters, flush):
+    """Per C3D KGS layer: latency and HBM rate of the reweight pass, checked
+    against the oracle (which is also timed, as the CPU baseline)."""
+    import numpy as np
+
+    import oracle
+    from paper_2007_09835_amd import synth
+    rows = []
+    md = ["## NEXT #2: reweighted group-lasso penalty (C3D KGS layers, l2, per-position groups)", "",
+          "One pass over the layer's weights [M][N][3][3][3] computing norms, penalty factors, "
+          "penalty value and mask (`update`), plus the penalty gradient (accumulated fp32) and the "
+          "proximal map (`full`). Algorithmic bytes: weights read once, per-unit arrays, mask, and "
+          "for `full` the gradient read+write and the proximal output. HBM peak 8000 GB/s. relL2 "
+          "of the norms vs the float64 oracle; oracle timed on the host (all threads).", "",
+          "| layer | dtype | outputs | weights | warm p50 us | cold p50 us | GB/s (cold) | frac | relL2 | oracle ms |",
+          "|---|---|---|---|---|---|---|---|---|---|"]
+    for l in synth.c3d_layers():
+        if l.dense:
+            continue
+        for dtype in ("bf16", "f32"):
+            for full in (False, True):
+                r = reweight_layer(torch, l, dtype, full)
+                warm = latency(torch, r["fn"], iters, stream)
+                cold = latency(torch, r["fn"], max(iters // 2, 10), stream, flush)
+                r["t"]["pen"].fill_(1.0)
+                if full:
+                    r["t"]["grad"].zero_()
+                r["fn"]()
+                torch.cuda.synchronize()
+                w64 = r["w_t"].double().numpy()
+                t0 = time.perf_counter()
+                ref = oracle.group_reweight(w64, 4, 4, norm=2, scope=0, lam=r["lam"], eps=r["eps"],
+                                            tau=r["tau"], step=r["step"])
+                t_or = time.perf_counter() - t0
+                got = r["t"]["norms"].double().cpu().numpy()
+                err = float(np.linalg.norm(got - ref["norms"].ravel()) /
+                            max(np.linalg.norm(ref["norms"]), 1e-30))
+                gbs = r["bytes"] / (cold["p50"] * 1e-3) / 1e9
+                rows.append({"layer": l.name, "dtype": dtype, "full": full, "bytes": r["bytes"],
+                             "warm": warm, "cold": cold, "gbps_cold": gbs,
+                             "gbps_warm": r["bytes"] / (warm["p50"] * 1e-3) / 1e9,
+                             "relL2_norms": err, "oracle_s": t_or,
+                             "oracle_threads": oracle.num_threads()})
+                md.append("| %s | %s | %s | %.2f MB | %.1f | %.1f | %.0f | %.3f | %.1e | %.1f |" % (
+                    l.name, dtype, "full" if full else "update", r["bytes"] / 1e6, 1e3 * warm["p50"],
+                    1e3 * cold["p50"], gbs, gbs / 8000.0, err, 1e3 * t_or))
+                log("reweight %s %s %s: warm %.1f us cold %.1f us %.0f GB/s relL2 %.1e" % (
+                    l.name, dtype, "full" if full else "update", 1e3 * warm["p50"],
+                    1e3 * cold["p50"], gbs, err))
+                del r
+    md.append("")
+    return {"rows": rows, "md": md}
+
+
 def suite(args, torch, stream):
     import numpy as np
 
@@ -381,6 +475,11 @@ def suite(args, torch, stream):
         md.append("")
     out["configs"]["stacks"] = stacks
 
+    # NEXT #2: reweighted group-lasso penalty over every KGS layer of C3D.
+    rw = reweight_suite(torch, stream, iters, flush)
+    out["reweight"] = rw["rows"]
+    md += rw["md"]
+
     # Context: MIOpen dense conv3d (torch) per C3D layer, batch 1, bf16 channels-last.
     md += ["## Context: torch conv3d (MIOpen), C3D layers, batch 1, bf16 (warm p50 ms)", "",
            "| layer | MIOpen | our dense | our KGS (4x4) |", "|---|---|---|---|"]
@@ -430,6 +529,21 @@ def main():
 
     if args.profile_layer:
         profile_layer(args, torch, stream)
+        return
+    if args.profile_reweight:
+        layer = next(l for l in synth.c3d_layers() if l.name == args.profile_reweight)
+        r = reweight_layer(torch, layer, "bf16", True)
+        r["fn"]()
+        ms = time_region(torch, r["fn"], args.layer_reps, stream)
+        out = {"reweight_layer": layer.name, "launches": args.layer_reps, "ms_per_launch": ms,
+               "algorithmic_bytes": r["bytes"], "gbps": r["bytes"] / (ms * 1e-3) / 1e9}
+        if args.copy_calibration:
+            n = args.copy_calibration * (1 << 20) // 4
+            a = torch.ones(n, dtype=torch.float32, device="cuda")
+            torch.empty_like(a).copy_(a)
+            torch.cuda.synchronize()
+            out["copy_bytes_each_way"] = n * 4
+        print(json.dumps(out), flush=True)
         return
     if args.suite:
         suite(args, torch, stream)

@@ -228,9 +228,10 @@ typedef struct {
 rt3d_status rt3d_group_units(const rt3d_group_desc *desc, int64_t *units);
 
 /* Device workspace (bytes, caller-owned, 4-byte aligned) that
- * rt3d_group_reweight needs when it is asked for the penalty value reg (one
- * float per workgroup, summed in a fixed order by a second kernel); 0
- * otherwise.  Host only. */
+ * rt3d_group_reweight needs when it is asked for the penalty value reg: one
+ * float per workgroup, added up in index order by a second kernel.  No
+ * initial contents are needed.  Calls that share a workspace must not run
+ * concurrently.  Host only. */
 rt3d_status rt3d_group_workspace_size(const rt3d_group_desc *desc, uint64_t *bytes);
 
 /* One pass over device weights w [M][N][kt][kh][kw] (desc->dtype) computing,

@@ -985,6 +985,11 @@ struct GroupPlan {
 
 bool finite(float v) { return v == v && v - v == 0.f; }
 
+// Workspace: one float partial sum per workgroup.
+uint64_t group_workspace_bytes(const GroupPlan &g) {
+  return static_cast<uint64_t>(g.wgs) * sizeof(float);
+}
+
 rt3d_status check_group_desc(const rt3d_group_desc *d) {
   if (!d) return fail(RT3D_ERR_INVALID_ARG, "desc is NULL");
   if (d->c_out <= 0 || d->c_in <= 0) return fail(RT3D_ERR_INVALID_ARG, "channel counts must be positive");
@@ -1233,7 +1238,7 @@ rt3d_status rt3d_group_workspace_size(const rt3d_group_desc *d, uint64_t *bytes)
   const rt3d_status st = check_group_desc(d);
   if (st != RT3D_OK) return st;
   if (!bytes) return fail(RT3D_ERR_INVALID_ARG, "bytes must be non-NULL");
-  *bytes = align_up(static_cast<uint64_t>(group_plan(d).wgs) * sizeof(float), kAlign);
+  *bytes = align_up(group_workspace_bytes(group_plan(d)), kAlign);
   return ok();
 }
 
@@ -1257,7 +1262,7 @@ rt3d_status rt3d_group_reweight(const rt3d_group_desc *d, const void *w, const f
       misaligned(pen_next, 4) || misaligned(reg, 4) || misaligned(grad, 4) || misaligned(workspace, 4))
     return fail(RT3D_ERR_INVALID_ARG, "pointers must be aligned to their element size");
   const GroupPlan g = group_plan(d);
-  const uint64_t need = static_cast<uint64_t>(g.wgs) * sizeof(float);
+  const uint64_t need = group_workspace_bytes(g);
   if (reg && (!workspace || workspace_bytes < need))
     return fail(RT3D_ERR_BUFFER_TOO_SMALL, "reg needs %llu bytes of workspace, got %llu",
                 static_cast<unsigned long long>(need),

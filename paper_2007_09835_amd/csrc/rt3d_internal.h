@@ -99,7 +99,7 @@ struct GroupArgs {
   const float *pen;   // current penalty factor per unit, or NULL (all ones)
   float *norms;       // per unit, or NULL
   float *pen_next;    // per unit, or NULL
-  float *partial;     // per workgroup sum of pen * norm, or NULL
+  float *partial;     // per workgroup sum of pen * norm, or NULL (no penalty value)
   float *grad;        // [M][N][ks] fp32, accumulated, or NULL
   uint8_t *mask;      // [P][Q][ks], or NULL
   void *w_prox;       // [M][N][ks] in the weight dtype, or NULL

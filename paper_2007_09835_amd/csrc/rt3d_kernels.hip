@@ -1286,27 +1286,32 @@ __global__ __launch_bounds__(256) void group_reweight_kernel(GroupArgs a) {
   const int span = a.gn * a.ks;          // elements of one channel group in a row
   const int nq = (c1 - c0 + a.gn - 1) / a.gn;
   const int q0 = qc * a.qb;
-  const int total = gme * len;
   const T *src = static_cast<const T *>(a.w);
   const long row0 = static_cast<long>(m0) * a.N * a.ks + static_cast<long>(c0) * a.ks;
   const long pitch = static_cast<long>(a.N) * a.ks;  // elements between filter rows
 
-  // Stage: four loads in flight per thread per round.
-  for (int base = 0; base < total; base += 1024) {
-    float v[4];
+  // Stage: tiles of 4 rows x 4 columns (o, o + 256, ...) per thread, so 16
+  // loads are in flight before the LDS stores and each address is a row
+  // base plus the column.
+  for (int o0 = tid; o0 < len; o0 += 4 * 256) {
+    for (int i0 = 0; i0 < gme; i0 += 4) {
+      float v[4][4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int idx = base + k * 256 + tid;
-      v[k] = 0.f;
-      if (idx < total) {
-        const DivMod d = divmod(idx, len);
-        v[k] = to_f32(src[row0 + d.q * pitch + d.r]);
+      for (int r = 0; r < 4; ++r) {
+        const T *rp = src + row0 + static_cast<long>(min(i0 + r, gme - 1)) * pitch;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int o = o0 + 256 * c;
+          v[r][c] = (i0 + r < gme && o < len) ? to_f32(rp[o]) : 0.f;
+        }
       }
-    }
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int idx = base + k * 256 + tid;
-      if (idx < total) buf[idx] = v[k];
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int o = o0 + 256 * c;
+          if (i0 + r < gme && o < len) buf[(i0 + r) * len + o] = v[r][c];
+        }
     }
   }
   __syncthreads();
@@ -1371,32 +1376,63 @@ __global__ __launch_bounds__(256) void group_reweight_kernel(GroupArgs a) {
   }
 
   if (a.grad || a.w_prox) {
+    // Same 4 x 4 tiles: the unit of a column is the same in every row, and
+    // a tile's gradient loads are all issued before its stores, so the
+    // read-modify-write waits for memory once per tile.
     T *dst = static_cast<T *>(a.w_prox);
-    for (int idx = tid; idx < total; idx += 256) {
-      const DivMod d = divmod(idx, len);
-      const DivMod e = divmod(d.r, span);
-      const int u = VANILLA ? e.q : e.q * a.ks + divmod(e.r, a.ks).r;
-      const float v = buf[idx], n = unorm[u], lp = ulp[u];
-      const long gi = row0 + d.q * pitch + d.r;
-      const float sgn = v > 0.f ? 1.f : (v < 0.f ? -1.f : 0.f);
-      if (a.grad) a.grad[gi] += NORM == 2 ? (n > 0.f ? lp * v / n : 0.f) : lp * sgn;
-      if (dst) {
-        const float theta = a.step * lp;
-        float z;
-        if constexpr (NORM == 2) {
-          const float f = n > 0.f ? 1.f - theta / n : 0.f;
-          z = f > 0.f ? v * f : 0.f;
-        } else {
-          const float m = fabsf(v) - theta;
-          z = m > 0.f ? sgn * m : 0.f;
+    for (int o0 = tid; o0 < len; o0 += 4 * 256) {
+      float un[4], ul[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int o = min(o0 + 256 * c, len - 1);
+        const DivMod e = divmod(o, span);
+        const int u = VANILLA ? e.q : e.q * a.ks + divmod(e.r, a.ks).r;
+        un[c] = unorm[u];
+        ul[c] = ulp[u];
+      }
+      for (int i0 = 0; i0 < gme; i0 += 4) {
+        float g0[4][4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const long rb = row0 + static_cast<long>(min(i0 + r, gme - 1)) * pitch;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const int o = o0 + 256 * c;
+            g0[r][c] = (a.grad && i0 + r < gme && o < len) ? a.grad[rb + o] : 0.f;
+          }
         }
-        dst[gi] = static_cast<T>(z);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const long rb = row0 + static_cast<long>(min(i0 + r, gme - 1)) * pitch;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const int o = o0 + 256 * c;
+            if (i0 + r >= gme || o >= len) continue;
+            const float v = buf[(i0 + r) * len + o], n = un[c], lp = ul[c];
+            const float sgn = v > 0.f ? 1.f : (v < 0.f ? -1.f : 0.f);
+            if (a.grad)
+              a.grad[rb + o] = g0[r][c] + (NORM == 2 ? (n > 0.f ? lp * v / n : 0.f) : lp * sgn);
+            if (dst) {
+              const float theta = a.step * lp;
+              float z;
+              if constexpr (NORM == 2) {
+                const float f = n > 0.f ? 1.f - theta / n : 0.f;
+                z = f > 0.f ? v * f : 0.f;
+              } else {
+                const float m = fabsf(v) - theta;
+                z = m > 0.f ? sgn * m : 0.f;
+              }
+              dst[rb + o] = static_cast<T>(z);
+            }
+          }
+        }
       }
     }
   }
 }
 
-// reg = lambda * sum of the per-workgroup partial sums, in a fixed order.
+// reg = lambda * the sum of the per-workgroup partial sums, in index order
+// (a second launch: the kernel boundary makes every partial visible).
 __global__ __launch_bounds__(256) void reg_finalize_kernel(const float *partial, int n,
                                                            float lambda, float *reg) {
   __shared__ float red[256];

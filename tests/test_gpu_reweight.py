@@ -52,7 +52,7 @@ def run_gpu(desc, w_dev, pen=None, lam=0.1, eps=1e-4, tau=0.0, step=1.0, grad0=N
     else:
         out["w_prox"] = torch.zeros_like(w_dev)
         src = w_dev
-    ws = torch.empty(rt3d.rt3d_group_workspace_size(desc) // 4, device=dev)
+    ws = torch.zeros(rt3d.rt3d_group_workspace_size(desc) // 4, device=dev)
     pen_t = None if pen is None else torch.from_numpy(np.ascontiguousarray(pen, np.float32)).to(dev)
     rt3d.rt3d_group_reweight(desc, src, pen_t, lam, eps, tau, step, norms=out["norms"],
                              pen_next=out["pen_next"], reg=out["reg"], mask=out["mask"],
@@ -191,10 +191,41 @@ def test_c3d_stack_norms_bf16():
         w_dev, w64 = weights("c3d_" + layer.name, layer.c_out, layer.c_in, layer.k, (4, 4), "bf16")
         norms = torch.empty(rt3d.rt3d_group_units(desc), device="cuda")
         reg = torch.empty(1, device="cuda")
-        ws = torch.empty(rt3d.rt3d_group_workspace_size(desc) // 4, device="cuda")
+        ws = torch.zeros(rt3d.rt3d_group_workspace_size(desc) // 4, device="cuda")
         rt3d.rt3d_group_reweight(desc, w_dev, None, 1.0, 1e-6, 0.0, 1.0, norms=norms, reg=reg,
                                  workspace=ws)
         torch.cuda.synchronize()
         ref = oracle.group_reweight(w64, 4, 4, norm=2, scope=0)
         assert rel_l2(norms.cpu().numpy(), ref["norms"].ravel()) <= 1e-5
         assert abs(reg.item() - ref["reg"]) <= 1e-5 * ref["reg"]
+
+
+def test_penalty_workspace_reuse_and_graph_replay():
+    """One workspace serves layers of different sizes in turn, and a captured
+    call gives the eager result on every replay."""
+    descs = [rt3d.make_group_desc(64, 48, (3, 3, 3), (4, 4), "bf16", 2, 0),
+             rt3d.make_group_desc(256, 256, (3, 3, 3), (4, 4), "bf16", 2, 0),
+             rt3d.make_group_desc(40, 36, (1, 3, 3), (4, 4), "bf16", 1, 1)]
+    ws = torch.zeros(max(rt3d.rt3d_group_workspace_size(d) for d in descs) // 4, device="cuda")
+    reg = torch.empty(1, device="cuda")
+    for rep in range(2):
+        for i, d in enumerate(descs):
+            w_dev, w64 = weights("reuse%d" % i, d.c_out, d.c_in, (d.kt, d.kh, d.kw), (4, 4), "bf16")
+            rt3d.rt3d_group_reweight(d, w_dev, None, 0.5, 1e-6, 0.0, 1.0, reg=reg, workspace=ws)
+            torch.cuda.synchronize()
+            ref = oracle.group_reweight(w64, 4, 4, norm=d.norm, scope=d.scope, lam=0.5)["reg"]
+            assert abs(reg.item() - ref) <= 1e-5 * ref, (rep, i)
+    d = descs[1]
+    w_dev, _ = weights("reuse1", d.c_out, d.c_in, (3, 3, 3), (4, 4), "bf16")
+    rt3d.rt3d_group_reweight(d, w_dev, None, 0.5, 1e-6, 0.0, 1.0, reg=reg, workspace=ws)
+    torch.cuda.synchronize()
+    eager = reg.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        rt3d.rt3d_group_reweight(d, w_dev, None, 0.5, 1e-6, 0.0, 1.0, reg=reg, workspace=ws)
+    for _ in range(3):
+        reg.fill_(-1.0)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(reg, eager)
+        _ = (w_dev.float() * 2).sum().item()  # unrelated eager work between replays
