@@ -486,7 +486,7 @@ void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
     mfw = g.c_out > 16 ? 2 : 1;
     if (const char *env = std::getenv("RT3D_SMALL_MFW")) {
       const int v = std::atoi(env);
-      if (v == 1 || v == 2 || v == 4) mfw = v;
+      if (v == 1 || v == 2) mfw = v;
     }
   }
   const int wt_count = (g.c_out + 16 * mfw - 1) / (16 * mfw);

@@ -356,12 +356,13 @@ __device__ __forceinline__ float4 load_bias4(const ConvArgs &a, int m0) {
   return make_float4(r[0], r[1], r[2], r[3]);
 }
 
-template <typename T>
+// RES = false compiles the residual path out (the caller knows a.res is NULL).
+template <typename T, bool RES = true>
 __device__ __forceinline__ float4 activate4(const ConvArgs &a, long vox, int m0, float4 v,
                                             float4 bb) {
   float r[4] = {v.x + bb.x, v.y + bb.y, v.z + bb.z, v.w + bb.w};
   const bool full = (a.c_out & 3) == 0;
-  if (a.res) {
+  if (RES && a.res) {
     const T *res = static_cast<const T *>(a.res) + vox * a.c_out + m0;
     if (full && sizeof(T) == 4) {
       const float4 rr = *reinterpret_cast<const float4 *>(res);
@@ -679,8 +680,9 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
 
 constexpr int kSmallLines = 12;      // halo lines (t, h) per brick: kt * (kh + 1) <= 12
 
-// LL = halo-line elements per lane (hw * c_in <= 64 * LL).
-template <typename T, int MFW, int LL>
+// LL = halo-line elements per lane (hw * c_in <= 64 * LL).  RES: the layer
+// adds a residual (a separate instantiation keeps the common epilogue short).
+template <typename T, int MFW, int LL, bool RES>
 __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
   constexpr int kSmallLineLoads = LL;
   using V8 = std::conditional_t<std::is_same_v<T, __bf16>, bf16x8, f16x8>;
@@ -859,7 +861,7 @@ __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
         const int oh = b.oh0 + (j >> 1), ow = b.ow0 + 16 * (j & 1) + n;
         ok[j] = b.ot0 < a.to && oh < a.ho && ow < a.wo;
         const float4 raw = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
-        v[j] = ok[j] ? activate4<T>(a, voxel(j), m0, raw, bb[i]) : raw;
+        v[j] = ok[j] ? activate4<T, RES>(a, voxel(j), m0, raw, bb[i]) : raw;
       }
       if (a.qh == 2) {  // window 1x2x2 (bricks hold whole windows)
 #pragma unroll
@@ -1535,24 +1537,25 @@ int launch_small(K kernel, const ConvArgs &a, void *stream) {
 
 int small_line_loads(const ConvArgs &a) { return a.hw * a.c_in <= 128 ? 2 : 3; }
 
+#define RT3D_SMALL_LL(T, M, FN, ...)                                                     \
+  do {                                                                                   \
+    if (ll == 2)                                                                         \
+      return res ? FN((small_kernel<T, M, 2, true>), __VA_ARGS__)                        \
+                 : FN((small_kernel<T, M, 2, false>), __VA_ARGS__);                      \
+    return res ? FN((small_kernel<T, M, 3, true>), __VA_ARGS__)                          \
+               : FN((small_kernel<T, M, 3, false>), __VA_ARGS__);                        \
+  } while (0)
+#define RT3D_SMALL_MFW(T, FN, ...)                                                       \
+  do {                                                                                   \
+    if (mfw == 1) RT3D_SMALL_LL(T, 1, FN, __VA_ARGS__);                                  \
+    if (mfw == 2) RT3D_SMALL_LL(T, 2, FN, __VA_ARGS__);                                  \
+  } while (0)
 #define RT3D_SMALL_DISPATCH(FN, ...)                                                     \
   do {                                                                                   \
     const int ll = small_line_loads(a);                                                  \
-    if (dtype == RT3D_BF16) {                                                            \
-      if (mfw == 1) return ll == 2 ? FN(small_kernel<__bf16, 1, 2>, __VA_ARGS__)         \
-                                   : FN(small_kernel<__bf16, 1, 3>, __VA_ARGS__);        \
-      if (mfw == 2) return ll == 2 ? FN(small_kernel<__bf16, 2, 2>, __VA_ARGS__)         \
-                                   : FN(small_kernel<__bf16, 2, 3>, __VA_ARGS__);        \
-      if (mfw == 4) return ll == 2 ? FN(small_kernel<__bf16, 4, 2>, __VA_ARGS__)         \
-                                   : FN(small_kernel<__bf16, 4, 3>, __VA_ARGS__);        \
-    } else {                                                                             \
-      if (mfw == 1) return ll == 2 ? FN(small_kernel<_Float16, 1, 2>, __VA_ARGS__)       \
-                                   : FN(small_kernel<_Float16, 1, 3>, __VA_ARGS__);      \
-      if (mfw == 2) return ll == 2 ? FN(small_kernel<_Float16, 2, 2>, __VA_ARGS__)       \
-                                   : FN(small_kernel<_Float16, 2, 3>, __VA_ARGS__);      \
-      if (mfw == 4) return ll == 2 ? FN(small_kernel<_Float16, 4, 2>, __VA_ARGS__)       \
-                                   : FN(small_kernel<_Float16, 4, 3>, __VA_ARGS__);      \
-    }                                                                                    \
+    const bool res = a.res != nullptr;                                                   \
+    if (dtype == RT3D_BF16) RT3D_SMALL_MFW(__bf16, FN, __VA_ARGS__);                      \
+    else RT3D_SMALL_MFW(_Float16, FN, __VA_ARGS__);                                      \
   } while (0)
 
 int launch_small16(const ConvArgs &a, int dtype, int mfw, void *stream) {
