@@ -30,10 +30,11 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=10)
-    p.add_argument("--net", default="c3d", choices=["c3d", "r2plus1d"])
+    p.add_argument("--net", default="c3d", choices=["c3d", "r2plus1d", "s3d"])
     p.add_argument("--batch", type=int, default=1)
     p.add_argument("--dtype", default="bf16", choices=["bf16", "f16", "f32"])
-    p.add_argument("--rate", type=float, default=3.0, help="whole-stack MAC pruning rate (KGS)")
+    p.add_argument("--rate", type=float, default=None,
+                   help="whole-stack MAC pruning rate (KGS); default 3 (C3D) or 2.1 (S3D)")
     p.add_argument("--mode", default="kgs", choices=["kgs", "vanilla"])
     p.add_argument("--group", default="4x4", help="kernel group size g_MxG_N of the masks")
     p.add_argument("--no-graph", action="store_true", help="launch eagerly instead of a HIP graph")
@@ -84,16 +85,9 @@ def time_region(torch, fn, steps, stream):
 def per_layer_ms(torch, stack, reps, stream):
     """Average duration of each layer's conv kernel, launched back to back."""
     out = []
-    inputs = {}
-    cur = stack.x
-    for l, conv in zip(stack.layers, stack.convs):
-        inp = stack.bufs[l.input_from] if l.input_from else cur
-        res = stack.bufs[l.residual_from] if l.residual_from else None
-        fn = (lambda conv=conv, inp=inp, res=res, o=stack.bufs[l.name]: conv(inp, res, out=o))
+    for _, fn in stack.layer_calls():
         fn()
         out.append(time_region(torch, fn, reps, stream))
-        cur = stack.pool_bufs.get(l.name, stack.bufs[l.name])
-        inputs[l.name] = cur
     return out
 
 
@@ -126,15 +120,17 @@ def measured_traffic(layer):
 def profile_layer(args, torch, stream):
     """Launch one layer of the sparse stack back to back (and optionally a
     plain copy of known size) so rocprofv3 sees only these kernels."""
-    from paper_2007_09835_amd.stack import Stack
-    sparse = Stack(args.net, args.batch, args.dtype, args.mode, args.rate,
-                   fuse_pool=not args.separate_pool, group=group_of(args))
+    from paper_2007_09835_amd.stack import make_stack
+    sparse = make_stack(args.net, args.batch, args.dtype, args.mode, args.rate,
+                        fuse_pool=not args.separate_pool, group=group_of(args))
     idx = [l.name for l in sparse.layers].index(args.profile_layer)
     l, conv = sparse.layers[idx], sparse.convs[idx]
     inp = torch.randn(conv.desc_for(args.batch).n, l.t, l.h, l.w, l.c_in, device="cuda").abs()
     inp = inp.to(sparse.x.dtype)
     res = torch.zeros_like(sparse.bufs[l.name]) if l.residual_from else None
-    fn = lambda: conv(inp, res, out=sparse.bufs[l.name])
+    out_buf = (sparse.bufs[l.name] if l.name in sparse.bufs else
+               torch.empty(conv.out_shape(args.batch), dtype=sparse.x.dtype, device="cuda"))
+    fn = lambda: conv(inp, res, out=out_buf)
     fn()
     ms = time_region(torch, fn, args.layer_reps, stream)
     info = conv.info
@@ -328,7 +324,7 @@ def suite(args, torch, stream):
     import oracle
     from paper_2007_09835_amd import layers as L
     from paper_2007_09835_amd import synth
-    from paper_2007_09835_amd.stack import Stack
+    from paper_2007_09835_amd.stack import make_stack
 
     scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")   # 1 GiB
     flush = lambda: scratch.fill_(1.0)
@@ -419,8 +415,8 @@ def suite(args, torch, stream):
 
     # Configs 3-5: stacks (whole pass in one HIP graph), per-layer warm latency.
     def stack_pair(net, batch, mode, rate, group=(4, 4)):
-        sp = Stack(net, batch, "bf16", mode, rate, group=group)
-        dn = Stack(net, batch, "bf16", "dense", group=group)
+        sp = make_stack(net, batch, "bf16", mode, rate, group=group)
+        dn = make_stack(net, batch, "bf16", "dense", rate, group=group)
         l0 = sp.layers[0]
         x = synth.to_dtype(synth.clip_input("bench-clip", batch, "uniform01", l0.c_in, l0.t, l0.h,
                                             l0.w), "bf16").permute(0, 2, 3, 4, 1).contiguous().cuda()
@@ -444,7 +440,8 @@ def suite(args, torch, stream):
            "|---|---|---|---|---|---|---|---|"]
     sweep = [("C3D batch 1 (cfg 3)", "c3d", 1, "kgs", 3.0, (4, 4)),
              ("C3D batch 1, g=16x4 (NEXT #1)", "c3d", 1, "kgs", 3.0, (16, 4)),
-             ("R(2+1)D-18 batch 1 (cfg 4)", "r2plus1d", 1, "kgs", 3.0, (4, 4))]
+             ("R(2+1)D-18 batch 1 (cfg 4)", "r2plus1d", 1, "kgs", 3.0, (4, 4)),
+             ("S3D 16x224x224 batch 1, 2.1x (NEXT #4)", "s3d", 1, "kgs", 2.1, (4, 4))]
     sweep += [("C3D batch 32, KGS %gx (cfg 5)" % r, "c3d", 32, "kgs", r, (4, 4)) for r in (2.0, 3.0, 4.0, 5.0)]
     sweep += [("C3D batch 32, vanilla 3x (cfg 5)", "c3d", 32, "vanilla", 3.0, (4, 4))]
     stacks = []
@@ -466,7 +463,7 @@ def suite(args, torch, stream):
         torch.cuda.empty_cache()
     md.append("")
     for e in stacks:
-        if "batch 32" not in e["label"] and "R(2+1)D" not in e["label"]:
+        if "batch 32" not in e["label"] and "R(2+1)D" not in e["label"] and "S3D" not in e["label"]:
             continue
         md += ["### %s: per layer (ms per launch, warm)" % e["label"], "",
                "| layer | R | KGS | dense | speedup | speedup / R |", "|---|---|---|---|---|---|"]
@@ -511,6 +508,8 @@ def suite(args, torch, stream):
 
 def main():
     args = parse()
+    if args.rate is None:
+        args.rate = 2.1 if args.net == "s3d" else 3.0
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
               "(clips are independent, so --gpus N would be N copies of this run)",
@@ -521,7 +520,7 @@ def main():
     import torch
 
     from paper_2007_09835_amd import build, synth
-    from paper_2007_09835_amd.stack import Stack
+    from paper_2007_09835_amd.stack import make_stack
 
     build.build(force=False)
     torch.cuda.set_device(0)
@@ -551,10 +550,11 @@ def main():
 
     log("building stacks ...")
     fuse = not args.separate_pool
-    sparse = Stack(args.net, args.batch, args.dtype, args.mode, args.rate, fuse_pool=fuse,
-                   group=group_of(args))
-    dense = Stack(args.net, args.batch, args.dtype, "dense", fuse_pool=fuse)
+    sparse = make_stack(args.net, args.batch, args.dtype, args.mode, args.rate, fuse_pool=fuse,
+                        group=group_of(args))
+    dense = make_stack(args.net, args.batch, args.dtype, "dense", args.rate, fuse_pool=fuse)
     l0 = sparse.layers[0]
+    clip_thw = (l0.t, l0.h, l0.w)
     clip = synth.clip_input("bench-clip", args.batch, "uniform01", l0.c_in, l0.t, l0.h, l0.w)
     x = synth.to_dtype(clip, args.dtype).permute(0, 2, 3, 4, 1).contiguous().cuda()
     sparse.x.copy_(x)
@@ -567,14 +567,15 @@ def main():
         for _ in range(3):
             stack.forward()
         torch.cuda.synchronize()
-        eager = stack.forward().clone()
+        out = stack.forward()
+        eager = out.clone()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             stack.forward()
+        out.zero_()
         g.replay()
         torch.cuda.synchronize()
-        replay = stack.bufs[stack.layers[-1].name]
-        if not torch.equal(eager, replay):
+        if not torch.equal(eager, out):
             raise RuntimeError("graph replay differs from the eager pass")
         return g.replay
 
@@ -652,12 +653,12 @@ def main():
         "dtype": args.dtype,
         "data": "synthetic (seeded clip and Kaiming-normal weights; no dataset or trained model)",
         "config": {
-            "workload": "%s conv stack, %d x 16x112x112 clip, %s %s masks g=%s, whole-stack "
-                        "pruning rate %.2fx (conv1 dense)%s"
-                        % (args.net.upper(), args.batch, args.dtype, args.mode.upper(),
-                           args.group.lower(), rate,
+            "workload": "%s conv stack, %d x %s clip, %s %s masks g=%s, whole-stack "
+                        "pruning rate %.2fx (%s dense)%s"
+                        % (args.net.upper(), args.batch, "x".join(map(str, clip_thw)), args.dtype,
+                           args.mode.upper(), args.group.lower(), rate, sparse.layers[0].name,
                            ", HIP graph" if not args.no_graph else ", eager launches"),
-            "batch": args.batch, "clip": [16, 112, 112], "pruning_rate": round(rate, 4),
+            "batch": args.batch, "clip": list(clip_thw), "pruning_rate": round(rate, 4),
         },
         "ms_per_clip": round(ms_sparse / args.batch, 5),
         "executed_tflops": round(dense_flops / rate / (ms_sparse * 1e-3) / 1e12, 3),

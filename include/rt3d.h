@@ -77,6 +77,14 @@ typedef struct {
                                  and 2x2x2 after conv2/3b/4b.  y then has the pooled
                                  extent floor(to/qt) x floor(ho/qh) x floor(wo/qw);
                                  the residual keeps the unpooled extent. */
+    int32_t y_c_total, y_c_off; /* fused channel concatenation: y holds y_c_total
+                                 channels per voxel and this layer writes channels
+                                 [y_c_off, y_c_off + c_out) of it (the branches of an
+                                 Inception block writing one output).  0, 0 = y has
+                                 exactly c_out channels.  Otherwise y_c_off >= 0,
+                                 y_c_off + c_out <= y_c_total, and both y_c_total and
+                                 y_c_off are multiples of 4.  The residual always has
+                                 c_out channels per voxel. */
 } rt3d_conv3d_desc;
 
 /* Filled by the pack calls; plain data owned by the caller.  It describes
@@ -187,11 +195,15 @@ rt3d_status rt3d_conv3d_dense_fwd(const rt3d_conv3d_desc *desc, const rt3d_pack_
                                   void *workspace, uint64_t workspace_bytes, void *stream);
 
 /* 3-D max pooling between layers (C3D pools 1x2x2 after conv1 and 2x2x2
- * after conv2, conv3b, conv4b): no padding, floor output size, channels-last
- * x [n][t][h][w][c] -> y [n][to][ho][wo][c].  Asynchronous on `stream`. */
+ * after conv2, conv3b, conv4b; the S3D-shaped stack pools 1x3x3 and 3x3x3
+ * windows with padding): channels-last x [n][t][h][w][c] -> y
+ * [n][to][ho][wo][c], to = (t + 2 pt - kt) / st + 1 (floor), likewise ho, wo.
+ * Padded positions take no part in the max; padding is at most half the
+ * window (so every window holds input voxels).  Asynchronous on `stream`. */
 rt3d_status rt3d_maxpool3d_fwd(int32_t n, int32_t c, int32_t t, int32_t h, int32_t w,
                                int32_t kt, int32_t kh, int32_t kw,
-                               int32_t st, int32_t sh, int32_t sw, int32_t dtype,
+                               int32_t st, int32_t sh, int32_t sw,
+                               int32_t pt, int32_t ph, int32_t pw, int32_t dtype,
                                const void *x, void *y, void *stream);
 
 /* ------------------------------------------------------------------------

@@ -30,7 +30,7 @@ def _load():
         lib.oracle_conv3d_dense.argtypes = [i] * 15 + [dp, dp, dp, dp, i, dp]
         lib.oracle_conv3d_kgs.argtypes = [i] * 17 + [dp, dp, ctypes.c_void_p, dp, dp, i, dp]
         lib.oracle_kgs_pack.argtypes = [i] * 8 + [ctypes.c_void_p] * 8
-        lib.oracle_maxpool3d.argtypes = [i] * 11 + [dp, dp]
+        lib.oracle_maxpool3d.argtypes = [i] * 14 + [dp, dp]
         lib.oracle_conv3d_points.argtypes = ([i] * 17 + [dp, dp, ctypes.c_void_p, dp, dp, i,
                                               ctypes.c_long, ctypes.c_void_p, dp])
         lib.oracle_group_reweight.argtypes = ([i] * 7 + [dp, dp] + [ctypes.c_double] * 4 +
@@ -173,13 +173,13 @@ def kgs_pack(w, mask, g_m, g_n):
     return group_ptr, pos[:npos.value], val_ptr, vals[:nval.value]
 
 
-def maxpool3d(x, k, stride):
-    """3-D max pooling, no padding, floor output size."""
+def maxpool3d(x, k, stride, pad=(0, 0, 0)):
+    """3-D max pooling, floor output size; padded positions take no part."""
     x = _f64(x)
     n, c, t, h, w = x.shape
-    to, ho, wo = out_shape(t, h, w, k, stride, (0, 0, 0))
+    to, ho, wo = out_shape(t, h, w, k, stride, pad)
     y = np.empty((n, c, to, ho, wo), dtype=np.float64)
-    rc = _load().oracle_maxpool3d(n, c, t, h, w, *k, *stride, _ptr(x), _ptr(y))
+    rc = _load().oracle_maxpool3d(n, c, t, h, w, *k, *stride, *pad, _ptr(x), _ptr(y))
     if rc:
         raise ValueError("oracle_maxpool3d rejected its arguments")
     return y

@@ -296,15 +296,20 @@ int oracle_kgs_pack(int c_out, int c_in, int kt, int kh, int kw, int g_m, int g_
     return ORACLE_OK;
 }
 
-/* 3-D max pooling (the pooling layers between the C3D convolutions): no
- * padding, floor output size, window kt x kh x kw, strides st, sh, sw.
+/* 3-D max pooling (the pooling layers between the convolutions): window
+ * kt x kh x kw, strides st, sh, sw, padding pt, ph, pw on each side; padded
+ * positions take no part in the max (every window must hold an input voxel:
+ * padding at most half the window), floor output size.
  * x [n][c][t][h][w] -> y [n][c][to][ho][wo]. */
 int oracle_maxpool3d(int n, int c, int t, int h, int w, int kt, int kh, int kw,
-                     int st, int sh, int sw, const double *x, double *y)
+                     int st, int sh, int sw, int pt, int ph, int pw, const double *x, double *y)
 {
-    if (check_geometry(n, c, c, t, h, w, kt, kh, kw, st, sh, sw, 0, 0, 0)) return ORACLE_BAD_ARG;
+    if (n < 0 || c <= 0 || t <= 0 || h <= 0 || w <= 0 || kt <= 0 || kh <= 0 || kw <= 0 ||
+        st <= 0 || sh <= 0 || sw <= 0) return ORACLE_BAD_ARG;
+    if (pt < 0 || ph < 0 || pw < 0 || 2 * pt > kt || 2 * ph > kh || 2 * pw > kw) return ORACLE_BAD_ARG;
     if (!x || !y) return ORACLE_BAD_ARG;
-    const long to = out_len(t, kt, st, 0), ho = out_len(h, kh, sh, 0), wo = out_len(w, kw, sw, 0);
+    const long to = out_len(t, kt, st, pt), ho = out_len(h, kh, sh, ph), wo = out_len(w, kw, sw, pw);
+    if (to <= 0 || ho <= 0 || wo <= 0) return ORACLE_BAD_ARG;
     long bc;
 #pragma omp parallel for
     for (bc = 0; bc < (long)n * c; ++bc) {
@@ -313,12 +318,16 @@ int oracle_maxpool3d(int n, int c, int t, int h, int w, int kt, int kh, int kw,
         for (long ot = 0; ot < to; ++ot)
         for (long oh = 0; oh < ho; ++oh)
         for (long ow = 0; ow < wo; ++ow) {
-            double best = xs[((ot * st) * h + oh * sh) * w + ow * sw];
+            int seen = 0;
+            double best = 0.0;
             for (long it = 0; it < kt; ++it)
             for (long ih = 0; ih < kh; ++ih)
             for (long iw = 0; iw < kw; ++iw) {
-                const double v = xs[((ot * st + it) * h + (oh * sh + ih)) * w + (ow * sw + iw)];
-                if (v > best) best = v;
+                const long zt = ot * st - pt + it, zh = oh * sh - ph + ih, zw = ow * sw - pw + iw;
+                if (zt < 0 || zt >= t || zh < 0 || zh >= h || zw < 0 || zw >= w) continue;
+                const double v = xs[(zt * h + zh) * w + zw];
+                if (!seen || v > best) best = v;
+                seen = 1;
             }
             ys[(ot * ho + oh) * wo + ow] = best;
         }

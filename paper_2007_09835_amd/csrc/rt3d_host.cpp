@@ -80,6 +80,14 @@ rt3d_status check_desc(const rt3d_conv3d_desc *d, bool need_groups) {
         out_len(d->w, d->kw, d->sw, d->pw) / qw <= 0)
       return fail(RT3D_ERR_INVALID_ARG, "the pooling window does not fit the conv output");
   }
+  if (d->y_c_total != 0 || d->y_c_off != 0) {
+    if (d->y_c_off < 0 || d->y_c_total < d->c_out ||
+        static_cast<long>(d->y_c_off) + d->c_out > d->y_c_total)
+      return fail(RT3D_ERR_INVALID_ARG, "output channels [%d, %d) do not fit y_c_total=%d",
+                  d->y_c_off, d->y_c_off + d->c_out, d->y_c_total);
+    if (d->y_c_total % 4 != 0 || d->y_c_off % 4 != 0)
+      return fail(RT3D_ERR_UNSUPPORTED, "y_c_total and y_c_off must be multiples of 4");
+  }
   if (need_groups) {
     auto okg = [](int g) { return g == 4 || g == 8 || g == 16; };
     if (!okg(d->g_m) || !okg(d->g_n))
@@ -895,6 +903,8 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   ConvArgs a{};
   a.x = x;
   a.y = y;
+  a.y_pitch = d->y_c_total != 0 ? d->y_c_total : d->c_out;
+  a.y_off = d->y_c_off;
   a.res = residual;
   a.bias = bias;
   a.step_ptr = reinterpret_cast<const uint32_t *>(b + p.step_ptr_off);
@@ -1207,19 +1217,25 @@ rt3d_status rt3d_conv3d_dense_fwd(const rt3d_conv3d_desc *d, const rt3d_pack_inf
 
 rt3d_status rt3d_maxpool3d_fwd(int32_t n, int32_t c, int32_t t, int32_t h, int32_t w, int32_t kt,
                                int32_t kh, int32_t kw, int32_t st, int32_t sh, int32_t sw,
-                               int32_t dtype, const void *x, void *y, void *stream) {
+                               int32_t pt, int32_t ph, int32_t pw, int32_t dtype, const void *x,
+                               void *y, void *stream) {
   if (n < 0 || c <= 0 || t <= 0 || h <= 0 || w <= 0 || kt <= 0 || kh <= 0 || kw <= 0 || st <= 0 ||
       sh <= 0 || sw <= 0)
     return fail(RT3D_ERR_INVALID_ARG, "pooling sizes must be positive");
+  if (pt < 0 || ph < 0 || pw < 0 || 2 * pt > kt || 2 * ph > kh || 2 * pw > kw)
+    return fail(RT3D_ERR_INVALID_ARG, "pooling padding must be between 0 and half the window");
   if (dtype != RT3D_F32 && dtype != RT3D_BF16 && dtype != RT3D_F16)
     return fail(RT3D_ERR_INVALID_ARG, "unknown dtype %d", dtype);
-  if (kt > t || kh > h || kw > w) return fail(RT3D_ERR_INVALID_ARG, "window larger than the input");
+  if (kt > t + 2 * pt || kh > h + 2 * ph || kw > w + 2 * pw)
+    return fail(RT3D_ERR_INVALID_ARG, "window larger than the padded input");
   if (n == 0) return ok();
   if (!x || !y) return fail(RT3D_ERR_INVALID_ARG, "x and y must be non-NULL");
   if (!aligned16(x) || !aligned16(y))
     return fail(RT3D_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
-  const int to = (t - kt) / st + 1, ho = (h - kh) / sh + 1, wo = (w - kw) / sw + 1;
-  const int e = launch_maxpool(n, c, t, h, w, kt, kh, kw, st, sh, sw, to, ho, wo, dtype, x, y, stream);
+  const int to = (t + 2 * pt - kt) / st + 1, ho = (h + 2 * ph - kh) / sh + 1,
+            wo = (w + 2 * pw - kw) / sw + 1;
+  const int e = launch_maxpool(n, c, t, h, w, kt, kh, kw, st, sh, sw, pt, ph, pw, to, ho, wo, dtype,
+                               x, y, stream);
   if (e != hipSuccess)
     return fail(RT3D_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(static_cast<hipError_t>(e)));
   return ok();

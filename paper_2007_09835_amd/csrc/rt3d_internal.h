@@ -80,6 +80,8 @@ struct ConvArgs {
   int32_t nbricks;    // n * nbt * nbh * nbw
   int32_t ntg;        // workgroups along the filters: ceil(wave_tiles / wpw)
   int32_t grid;       // workgroups launched (0: one per tile); fewer loop over tiles
+  int32_t y_pitch;    // channels per voxel of y (>= c_out: fused concatenation)
+  int32_t y_off;      // first channel of y this layer writes
   int32_t pad1;
 };
 
@@ -125,6 +127,7 @@ int launch_group_reweight(const GroupArgs &a, int dtype, int norm, int scope, si
                           void *stream);
 int launch_reg_finalize(const float *partial, int n, float lambda, float *reg, void *stream);
 int launch_maxpool(int n, int c, int t, int h, int w, int kt, int kh, int kw, int st, int sh,
-                   int sw, int to, int ho, int wo, int dtype, const void *x, void *y, void *stream);
+                   int sw, int pt, int ph, int pw, int to, int ho, int wo, int dtype, const void *x,
+                   void *y, void *stream);
 
 }  // namespace rt3d

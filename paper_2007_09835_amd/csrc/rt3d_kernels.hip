@@ -384,9 +384,9 @@ __device__ __forceinline__ float4 activate4(const ConvArgs &a, long vox, int m0,
 // Round and store filters m0..m0+3 of output voxel vox (of y's own extent).
 template <typename T>
 __device__ __forceinline__ void put4(const ConvArgs &a, long vox, int m0, float4 v) {
-  T *y = static_cast<T *>(a.y) + vox * a.c_out + m0;
+  T *y = static_cast<T *>(a.y) + vox * a.y_pitch + a.y_off + m0;
   const float r[4] = {v.x, v.y, v.z, v.w};
-  if ((a.c_out & 3) == 0) {
+  if ((a.c_out & 3) == 0) {  // y_pitch and y_off are multiples of 4 as well
     if constexpr (sizeof(T) == 4) {
       *reinterpret_cast<float4 *>(y) = v;
     } else {
@@ -1222,7 +1222,8 @@ template <typename T, int VEC>
 __global__ __launch_bounds__(256) void maxpool_kernel(const T *__restrict__ x, T *__restrict__ y,
                                                       int n, int c, int t, int h, int w, int kt,
                                                       int kh, int kw, int st, int sh, int sw,
-                                                      int to, int ho, int wo) {
+                                                      int pt, int ph, int pw, int to, int ho,
+                                                      int wo) {
   const long cv = c / VEC;
   const long total = static_cast<long>(n) * to * ho * wo * cv;
   for (long idx = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
@@ -1235,18 +1236,30 @@ __global__ __launch_bounds__(256) void maxpool_kernel(const T *__restrict__ x, T
     r /= ho;
     const int ot = static_cast<int>(r % to);
     const long nb = r / to;
+    // Padded positions take no part (every window holds at least one input
+    // voxel: the host keeps the padding at most half the window).
     float best[VEC];
-    for (int e = 0; e < VEC; ++e) best[e] = -__builtin_huge_valf();
-    for (int it = 0; it < kt; ++it)
-      for (int ih = 0; ih < kh; ++ih)
+    bool any = false;
+    for (int e = 0; e < VEC; ++e) best[e] = 0.f;
+    for (int it = 0; it < kt; ++it) {
+      const int zt = ot * st - pt + it;
+      if (zt < 0 || zt >= t) continue;
+      for (int ih = 0; ih < kh; ++ih) {
+        const int zh = oh * sh - ph + ih;
+        if (zh < 0 || zh >= h) continue;
         for (int iw = 0; iw < kw; ++iw) {
-          const long vox = ((nb * t + ot * st + it) * h + oh * sh + ih) * w + ow * sw + iw;
+          const int zw = ow * sw - pw + iw;
+          if (zw < 0 || zw >= w) continue;
+          const long vox = ((nb * t + zt) * h + zh) * w + zw;
           const T *src = x + vox * c + cb * VEC;
           for (int e = 0; e < VEC; ++e) {
             const float v = static_cast<float>(src[e]);
-            best[e] = (v > best[e] || (it == 0 && ih == 0 && iw == 0)) ? v : best[e];
+            best[e] = (!any || v > best[e]) ? v : best[e];
           }
+          any = true;
         }
+      }
+    }
     T *dst = y + (((nb * to + ot) * ho + oh) * wo + ow) * c + cb * VEC;
     for (int e = 0; e < VEC; ++e) dst[e] = static_cast<T>(best[e]);
   }
@@ -1611,8 +1624,8 @@ int launch_kgs_exact_f32(const ConvArgs &a, void *stream) {
 }
 
 int launch_maxpool(int n, int c, int t, int h, int w, int kt, int kh, int kw, int st, int sh,
-                   int sw, int to, int ho, int wo, int dtype, const void *x, void *y,
-                   void *stream) {
+                   int sw, int pt, int ph, int pw, int to, int ho, int wo, int dtype,
+                   const void *x, void *y, void *stream) {
   const long outs = static_cast<long>(n) * to * ho * wo;
   if (outs == 0 || c == 0) return hipSuccess;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -1623,7 +1636,7 @@ int launch_maxpool(int n, int c, int t, int h, int w, int kt, int kh, int kw, in
 #define RT3D_POOL(T, VEC)                                                                      \
   hipLaunchKernelGGL((maxpool_kernel<T, VEC>), dim3(grid_for(outs * (c / VEC))), dim3(256), 0, s, \
                      static_cast<const T *>(x), static_cast<T *>(y), n, c, t, h, w, kt, kh, kw,   \
-                     st, sh, sw, to, ho, wo)
+                     st, sh, sw, pt, ph, pw, to, ho, wo)
   if (dtype == RT3D_F32) {
     if (c % 4 == 0) RT3D_POOL(float, 4); else RT3D_POOL(float, 1);
   } else if (dtype == RT3D_BF16) {

@@ -67,22 +67,27 @@ class Conv3d:
 
     def __call__(self, x: torch.Tensor, residual: Optional[torch.Tensor] = None,
                  out: Optional[torch.Tensor] = None, stream=None,
-                 use_workspace: bool = True) -> torch.Tensor:
+                 use_workspace: bool = True, c_off: int = 0) -> torch.Tensor:
+        """``out`` may hold more channels than c_out: the layer then writes
+        channels [c_off, c_off + c_out) of it (fused concatenation)."""
         n = x.shape[0]
         if out is None:
             out = torch.empty(self.out_shape(n), dtype=TORCH_DTYPES[self.dtype], device=x.device)
         ws = self.workspace(n) if use_workspace and n > 0 else None
+        d = self.desc_for(n)
+        if out.shape[-1] != self.c_out or c_off:
+            d.y_c_total, d.y_c_off = out.shape[-1], c_off
         fwd = rt3d.rt3d_kgs_conv3d_fwd if self.sparse else rt3d.rt3d_conv3d_dense_fwd
-        fwd(self.desc_for(n), self.info, self.blob, x, self.bias, residual, out, ws, stream)
+        fwd(d, self.info, self.blob, x, self.bias, residual, out, ws, stream)
         return out
 
 
 def maxpool3d(x: torch.Tensor, k, stride, dtype: str, out: Optional[torch.Tensor] = None,
-              stream=None) -> torch.Tensor:
+              stream=None, pad=(0, 0, 0)) -> torch.Tensor:
     n, t, h, w, c = x.shape
-    to, ho, wo = ((t - k[0]) // stride[0] + 1, (h - k[1]) // stride[1] + 1,
-                  (w - k[2]) // stride[2] + 1)
+    to, ho, wo = ((t + 2 * pad[0] - k[0]) // stride[0] + 1, (h + 2 * pad[1] - k[1]) // stride[1] + 1,
+                  (w + 2 * pad[2] - k[2]) // stride[2] + 1)
     if out is None:
         out = torch.empty((n, to, ho, wo, c), dtype=x.dtype, device=x.device)
-    rt3d.rt3d_maxpool3d_fwd(x, out, k, stride, dtype, stream)
+    rt3d.rt3d_maxpool3d_fwd(x, out, k, stride, dtype, stream, pad)
     return out

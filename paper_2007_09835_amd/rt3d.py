@@ -56,7 +56,7 @@ class Conv3dDesc(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in (
         "n", "c_in", "c_out", "t", "h", "w", "kt", "kh", "kw", "st", "sh", "sw",
         "pt", "ph", "pw", "g_m", "g_n", "dtype")] + [("flags", ctypes.c_uint32)] + [
-        (name, ctypes.c_int32) for name in ("qt", "qh", "qw")]
+        (name, ctypes.c_int32) for name in ("qt", "qh", "qw", "y_c_total", "y_c_off")]
 
 
 class PackInfo(ctypes.Structure):
@@ -106,7 +106,7 @@ def load():
         "rt3d_dense_pack_size": ([D, P(u64)], ctypes.c_int),
         "rt3d_dense_pack": ([D, vp, vp, u64, I], ctypes.c_int),
         "rt3d_conv3d_dense_fwd": ([D, I, vp, vp, vp, vp, vp, vp, u64, vp], ctypes.c_int),
-        "rt3d_maxpool3d_fwd": ([i32] * 12 + [vp, vp, vp], ctypes.c_int),
+        "rt3d_maxpool3d_fwd": ([i32] * 15 + [vp, vp, vp], ctypes.c_int),
         "rt3d_group_units": ([P(GroupDesc), P(ctypes.c_int64)], ctypes.c_int),
         "rt3d_group_workspace_size": ([P(GroupDesc), P(u64)], ctypes.c_int),
         "rt3d_group_reweight": ([P(GroupDesc), vp, vp] + [ctypes.c_float] * 4 + [vp] * 7 +
@@ -133,11 +133,14 @@ def _check(status: int):
 
 
 def make_desc(n, c_in, c_out, thw, k=(3, 3, 3), stride=(1, 1, 1), pad=(1, 1, 1), g=(4, 4),
-              dtype="f32", relu=True, residual=False, pool=(1, 1, 1)) -> Conv3dDesc:
-    """Fill an rt3d_conv3d_desc (``pool``: fused max-pool window = stride)."""
+              dtype="f32", relu=True, residual=False, pool=(1, 1, 1), y_c_total=0,
+              y_c_off=0) -> Conv3dDesc:
+    """Fill an rt3d_conv3d_desc (``pool``: fused max-pool window = stride;
+    ``y_c_total`` / ``y_c_off``: write into a channel slice of a wider y)."""
     flags = (RT3D_RELU if relu else 0) | (RT3D_RESIDUAL if residual else 0)
     code = DTYPE_CODES[dtype] if isinstance(dtype, str) else int(dtype)
-    return Conv3dDesc(n, c_in, c_out, *thw, *k, *stride, *pad, g[0], g[1], code, flags, *pool)
+    return Conv3dDesc(n, c_in, c_out, *thw, *k, *stride, *pad, g[0], g[1], code, flags, *pool,
+                      y_c_total, y_c_off)
 
 
 def _host_ptr(a: np.ndarray) -> int:
@@ -254,10 +257,10 @@ def rt3d_conv3d_dense_fwd(desc: Conv3dDesc, info: PackInfo, blob_dev, x, bias, r
         _dev_ptr(workspace, "workspace"), ws_bytes, _stream_ptr(stream)))
 
 
-def rt3d_maxpool3d_fwd(x, y, k, stride, dtype: str, stream=None) -> None:
+def rt3d_maxpool3d_fwd(x, y, k, stride, dtype: str, stream=None, pad=(0, 0, 0)) -> None:
     """x [n, t, h, w, c] -> y [n, to, ho, wo, c] (device, channels-last)."""
     n, t, h, w, c = x.shape
-    _check(load().rt3d_maxpool3d_fwd(n, c, t, h, w, *k, *stride, DTYPE_CODES[dtype],
+    _check(load().rt3d_maxpool3d_fwd(n, c, t, h, w, *k, *stride, *pad, DTYPE_CODES[dtype],
                                      _dev_ptr(x, "x"), _dev_ptr(y, "y"), _stream_ptr(stream)))
 
 

@@ -1,6 +1,8 @@
 """Whole-network forward passes built from librt3d calls: the C3D conv stack
-(eight 3x3x3 convs with max-pools) and the R(2+1)D-18-shaped stack
-(factorised (2+1)-D convs with residual adds fused into the epilogue).
+(eight 3x3x3 convs with max-pools), the R(2+1)D-18-shaped stack
+(factorised (2+1)-D convs with residual adds fused into the epilogue) and
+the S3D-shaped stack (Inception blocks whose branches write channel slices
+of one output, separable convs, padded max-pools).
 
 Only orchestration lives here: packing at construction, preallocated
 activation buffers, and the sequence of C-ABI launches on one stream (so the
@@ -84,6 +86,19 @@ class Stack:
             return self.dense_macs()
         return int(round(self.dense_macs() / self.kept_rate()))
 
+    def layer_calls(self):
+        """(layer, fn) for every conv: fn launches that conv alone on the
+        buffers a forward pass gives it (for per-layer timing)."""
+        calls = []
+        cur = self.x
+        for l, conv in zip(self.layers, self.convs):
+            inp = self.bufs[l.input_from] if l.input_from else cur
+            res = self.bufs[l.residual_from] if l.residual_from else None
+            calls.append((l, lambda conv=conv, inp=inp, res=res, o=self.bufs[l.name]:
+                          conv(inp, res, out=o)))
+            cur = self.pool_bufs.get(l.name, self.bufs[l.name])
+        return calls
+
     def forward(self, x: Optional[torch.Tensor] = None, timers=None) -> torch.Tensor:
         """Run the stack on ``x`` (default: the internal input buffer).
         ``timers`` maps a layer index to a (start, end) event pair recorded
@@ -106,3 +121,94 @@ class Stack:
                 outs[l.name] = y
             cur = y
         return cur
+
+
+class S3DStack:
+    """The S3D-shaped stack (synth.s3d_layers): convs and padded max-pools
+    over named buffers; the four branches of an Inception block write their
+    channel slices of the block output directly (fused concatenation)."""
+
+    net = "s3d"
+
+    def __init__(self, batch: int = 1, dtype: str = "bf16", mode: str = "kgs",
+                 rate: float = 2.1, tag: str = "s3d", device: str = "cuda", group=(4, 4),
+                 clip=(16, 224)):
+        """``clip`` = (frames, height = width) of the input."""
+        self.batch, self.dtype, self.mode, self.rate = batch, dtype, mode, rate
+        self.group = tuple(group)
+        self.layers, self.ops = synth.s3d_stack(rate if mode == "kgs" else 2.1, tag=tag,
+                                                g=self.group, clip=tuple(clip))
+        tdt = layers.TORCH_DTYPES[dtype]
+        self.convs, self.masks = [], []
+        by_name = {}
+        for l in self.layers:
+            d = synth.layer_params(tag, l, mask_kind=("dense" if mode == "dense" else mode),
+                                   rate=rate)
+            mask = None if (l.dense or mode == "dense") else d.mask
+            self.masks.append(None if l.dense else d.mask)
+            conv = layers.Conv3d(l.c_in, l.c_out, (l.t, l.h, l.w), l.k, l.stride, l.pad,
+                                 synth.to_dtype(d.w, dtype), d.bias.astype(np.float32), mask,
+                                 dtype, relu=l.relu, g=l.g, device=device, batch=batch)
+            self.convs.append(conv)
+            by_name[l.name] = (l, conv)
+        self._by_name = by_name
+        # buffer shapes from the op list
+        l0 = self.layers[0]
+        shapes = {"x": (l0.t, l0.h, l0.w, l0.c_in)}
+        for op in self.ops:
+            if op[0] == "conv":
+                _, name, src, dst, c_off = op
+                l, conv = by_name[name]
+                c_prev = shapes.get(dst, (0, 0, 0, 0))[3]
+                shapes[dst] = (*conv.out_thw, max(c_prev, c_off + l.c_out))
+            else:
+                _, src, dst, k, st, pd = op
+                t, h, w, c = shapes[src]
+                shapes[dst] = (*((i + 2 * p - kk) // s + 1
+                                 for i, kk, s, p in zip((t, h, w), k, st, pd)), c)
+        self.x = torch.zeros((batch, *shapes["x"]), dtype=tdt, device=device)
+        self.bufs: Dict[str, torch.Tensor] = {"x": self.x}
+        for name, shp in shapes.items():
+            if name != "x":
+                self.bufs[name] = torch.empty((batch, *shp), dtype=tdt, device=device)
+        self.pool_bufs: Dict[str, torch.Tensor] = {}
+        self.out_name = self.ops[-1][3]
+
+    def kept_rate(self) -> float:
+        if self.mode == "dense":
+            return 1.0
+        return synth.stack_rate(self.layers, self.masks)
+
+    def dense_macs(self) -> int:
+        return sum(l.dense_macs(self.batch) for l in self.layers)
+
+    def layer_calls(self):
+        calls = []
+        for op in self.ops:
+            if op[0] == "conv":
+                _, name, src, dst, c_off = op
+                l, conv = self._by_name[name]
+                calls.append((l, lambda conv=conv, i=self.bufs[src], o=self.bufs[dst], c=c_off:
+                              conv(i, None, out=o, c_off=c)))
+        return calls
+
+    def forward(self, x: Optional[torch.Tensor] = None) -> torch.Tensor:
+        if x is not None:
+            self.x.copy_(x)
+        for op in self.ops:
+            if op[0] == "conv":
+                _, name, src, dst, c_off = op
+                _, conv = self._by_name[name]
+                conv(self.bufs[src], None, out=self.bufs[dst], c_off=c_off)
+            else:
+                _, src, dst, k, st, pd = op
+                layers.maxpool3d(self.bufs[src], k, st, self.dtype, out=self.bufs[dst], pad=pd)
+        return self.bufs[self.out_name]
+
+
+def make_stack(net: str, batch: int = 1, dtype: str = "bf16", mode: str = "kgs",
+               rate: float = 3.0, fuse_pool: bool = True, group=(4, 4)):
+    """The named stack (c3d, r2plus1d or s3d)."""
+    if net == "s3d":
+        return S3DStack(batch, dtype, mode, rate, group=group)
+    return Stack(net, batch, dtype, mode, rate, fuse_pool=fuse_pool, group=group)

@@ -55,6 +55,7 @@ class ConvLayer:
     pool_after: Optional[Tuple[Tuple[int, int, int], Tuple[int, int, int]]] = None
     keep: Optional[int] = None         # kept positions per group (KGS layers)
     g: Tuple[int, int] = (GROUP, GROUP)  # kernel group size (g_M filters, g_N channels)
+    group_rate: Optional[float] = None   # 1x1x1 KGS layers: whole-group pruning rate
 
     @property
     def ks(self) -> int:
@@ -152,6 +153,117 @@ def r2plus1d_layers() -> List[ConvLayer]:
             c = width
             prev = layers[-1].name
     return layers
+
+
+# S3D (Inception-style blocks with separable convs).  Each entry of the op
+# list is ("conv", layer name, input buffer, output buffer, channel offset)
+# or ("pool", input buffer, output buffer, window, stride, padding).
+S3D_MIXED = [  # name, in, b0, b1 reduce, b1, b2 reduce, b2, b3
+    ("m3b", 192, 64, 96, 128, 16, 32, 32),
+    ("m3c", 256, 128, 128, 192, 32, 96, 64),
+    ("m4b", 480, 192, 96, 208, 16, 48, 64),
+    ("m4c", 512, 160, 112, 224, 24, 64, 64),
+    ("m4d", 512, 128, 128, 256, 24, 64, 64),
+    ("m4e", 512, 112, 144, 288, 32, 64, 64),
+    ("m4f", 528, 256, 160, 320, 32, 128, 128),
+    ("m5b", 832, 256, 160, 320, 32, 128, 128),
+    ("m5c", 832, 384, 192, 384, 48, 128, 128),
+]
+
+
+def s3d_layers(t: int = 16, hw: int = 224) -> Tuple[List[ConvLayer], list]:
+    """S3D-shaped conv stack on one t x hw x hw RGB clip: a separable 7x7x7
+    stem (1x7x7 stride (1,2,2), then 7x1x1 stride (2,1,1)), max-pool 1x3x3
+    stride (1,2,2), 1x1x1 and separable 3x3x3 convs, max-pool, then nine
+    Inception blocks (mixed 3b-3c, 4b-4f, 5b-5c) separated by 3x3x3 / 2x2x2
+    stride-2 pools.  A block's four branches write channel slices of one
+    output: 1x1x1; 1x1x1 then separable 3x3x3 (1x3x3 then 3x1x1); the same
+    with other widths; 3x3x3 stride-1 max-pool then 1x1x1.  Every conv has a
+    ReLU (batch-norm folded into weights and bias).  Returns (layers, ops)."""
+    layers: List[ConvLayer] = []
+    ops: list = []
+    shapes = {"x": (3, t, hw, hw)}
+
+    def conv(name, src, dst, c_out, k, stride=(1, 1, 1), pad=(0, 0, 0), c_off=0, dense=False):
+        c_in, ti, hi, wi = shapes[src]
+        l = ConvLayer(name, c_in, c_out, ti, hi, wi, k, stride, pad, dense=dense)
+        layers.append(l)
+        ops.append(("conv", name, src, dst, c_off))
+        return l.out_thw
+
+    def pool(src, dst, k, stride, pad):
+        c, ti, hi, wi = shapes[src]
+        out = tuple((i + 2 * p - kk) // s + 1 for i, kk, s, p in zip((ti, hi, wi), k, stride, pad))
+        ops.append(("pool", src, dst, k, stride, pad))
+        shapes[dst] = (c, *out)
+
+    def sep(name, src, dst, c_out, c_off=0, k=3, stride=(1, 1, 1), dense=False):
+        pk = k // 2
+        thw = conv(name + "_s", src, name + "_s", c_out, (1, k, k), (1, stride[1], stride[2]),
+                   (0, pk, pk), dense=dense)
+        shapes[name + "_s"] = (c_out, *thw)
+        thw = conv(name + "_t", name + "_s", dst, c_out, (k, 1, 1), (stride[0], 1, 1), (pk, 0, 0),
+                   c_off=c_off)
+        return thw
+
+    thw = sep("c1a", "x", "c1a", 64, k=7, stride=(2, 2, 2), dense=True)
+    # only the spatial stem conv (3 input channels) stays dense
+    layers[-1].dense = False
+    shapes["c1a"] = (64, *thw)
+    pool("c1a", "p2a", (1, 3, 3), (1, 2, 2), (0, 1, 1))
+    thw = conv("c2b", "p2a", "c2b", 64, (1, 1, 1))
+    shapes["c2b"] = (64, *thw)
+    thw = sep("c2c", "c2b", "c2c", 192)
+    shapes["c2c"] = (192, *thw)
+    pool("c2c", "p3a", (1, 3, 3), (1, 2, 2), (0, 1, 1))
+    cur = "p3a"
+    for name, c_in, b0, b1r, b1, b2r, b2, b3 in S3D_MIXED:
+        if name == "m4b":
+            pool(cur, "p4a", (3, 3, 3), (2, 2, 2), (1, 1, 1))
+            cur = "p4a"
+        if name == "m5b":
+            pool(cur, "p5a", (2, 2, 2), (2, 2, 2), (0, 0, 0))
+            cur = "p5a"
+        c, ti, hi, wi = shapes[cur]
+        assert c == c_in, (name, c, c_in)
+        out = name
+        conv(name + "_b0", cur, out, b0, (1, 1, 1), c_off=0)
+        thw = conv(name + "_b1r", cur, name + "_b1r", b1r, (1, 1, 1))
+        shapes[name + "_b1r"] = (b1r, *thw)
+        sep(name + "_b1", name + "_b1r", out, b1, c_off=b0)
+        thw = conv(name + "_b2r", cur, name + "_b2r", b2r, (1, 1, 1))
+        shapes[name + "_b2r"] = (b2r, *thw)
+        sep(name + "_b2", name + "_b2r", out, b2, c_off=b0 + b1)
+        pool(cur, name + "_p", (3, 3, 3), (1, 1, 1), (1, 1, 1))
+        conv(name + "_b3", name + "_p", out, b3, (1, 1, 1), c_off=b0 + b1 + b2)
+        shapes[out] = (b0 + b1 + b2 + b3, ti, hi, wi)
+        cur = out
+    return layers, ops
+
+
+def s3d_stack(rate: float = 2.1, tag: str = "s3d", g: Tuple[int, int] = (GROUP, GROUP),
+              clip: Tuple[int, int] = (16, 224)) -> Tuple[List[ConvLayer], list]:
+    """S3D stack with KGS masks for a whole-stack MAC pruning rate of about
+    ``rate`` (the 3-channel stem conv stays dense, so the other layers are
+    pruned at r = (D - D_dense) / (D / rate - D_dense)): kernels of K_s
+    positions keep K_s / r of them per group (randomised rounding per
+    layer), 1x1x1 layers keep round(P*Q/r) whole groups."""
+    layers, ops = s3d_layers(*clip)
+    r = rng_for(tag, "keep", int(rate * 1000))
+    d_total = sum(l.dense_macs() for l in layers)
+    d_dense = sum(l.dense_macs() for l in layers if l.dense)
+    layer_rate = (d_total - d_dense) / (d_total / rate - d_dense) if rate > 1.0 else 1.0
+    for l in layers:
+        l.g = tuple(g)
+        if l.dense or rate <= 1.0:
+            continue
+        if l.ks == 1:
+            l.group_rate = layer_rate
+        else:
+            kstar = l.ks / layer_rate
+            lo = int(np.floor(kstar))
+            l.keep = min(l.ks, max(1, lo + int(r.random() < kstar - lo)))
+    return layers, ops
 
 
 # --------------------------------------------------------------------------
@@ -315,6 +427,10 @@ def layer_params(tag: str, layer: ConvLayer, mask_kind: str = "kgs", rate: float
         mask = None
     elif mask_kind == "vanilla":
         mask = vanilla_mask(rng_for(tag, layer.name, "mask"), p_groups, q_groups, layer.ks, rate)
+    elif layer.group_rate is not None:
+        # one kernel position: keeping or pruning it is keeping or pruning the group
+        mask = vanilla_mask(rng_for(tag, layer.name, "mask"), p_groups, q_groups, layer.ks,
+                            layer.group_rate)
     else:
         mask = kgs_mask(rng_for(tag, layer.name, "mask"), p_groups, q_groups, layer.ks, layer.keep)
     return LayerData(layer, w, b, mask)

@@ -204,8 +204,18 @@ def test_error_paths():
     st = lib.rt3d_kgs_conv3d_fwd(ctypes.byref(good), ctypes.byref(info), 256, 258, None, None, 256,
                                  None, 0, None)
     assert st == rt3d.RT3D_ERR_INVALID_ARG
-    st = lib.rt3d_maxpool3d_fwd(1, 8, 4, 4, 4, 5, 2, 2, 1, 2, 2, 0, 256, 256, None)
+    st = lib.rt3d_maxpool3d_fwd(1, 8, 4, 4, 4, 5, 2, 2, 1, 2, 2, 0, 0, 0, 0, 256, 256, None)
     assert st == rt3d.RT3D_ERR_INVALID_ARG
+    # padding above half the window
+    st = lib.rt3d_maxpool3d_fwd(1, 8, 4, 4, 4, 3, 3, 3, 1, 1, 1, 2, 1, 1, 0, 256, 256, None)
+    assert st == rt3d.RT3D_ERR_INVALID_ARG
+    # fused concatenation: the slice must fit and keep 4-channel alignment
+    cat = rt3d.make_desc(1, 8, 8, (4, 4, 4), dtype="f32", y_c_total=12, y_c_off=6)
+    _expect_status(rt3d.RT3D_ERR_INVALID_ARG, rt3d.rt3d_conv3d_out_shape, cat)
+    cat = rt3d.make_desc(1, 8, 8, (4, 4, 4), dtype="f32", y_c_total=18, y_c_off=2)
+    _expect_status(rt3d.RT3D_ERR_UNSUPPORTED, rt3d.rt3d_conv3d_out_shape, cat)
+    cat = rt3d.make_desc(1, 8, 8, (4, 4, 4), dtype="f32", y_c_total=16, y_c_off=8)
+    assert rt3d.rt3d_conv3d_out_shape(cat) == (4, 4, 4)
     assert lib.rt3d_status_string(99)
     assert lib.rt3d_status_string(rt3d.RT3D_ERR_HIP) == b"HIP runtime error"
 

@@ -257,14 +257,50 @@ def test_empty_batch_is_a_no_op():
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
-@pytest.mark.parametrize("k,stride", [((1, 2, 2), (1, 2, 2)), ((2, 2, 2), (2, 2, 2)),
-                                      ((3, 3, 3), (2, 1, 2))])
-def test_maxpool_exact(dtype, k, stride):
-    x64 = synth.clip_input("pool", 2, "halfnormal", 24, 6, 9, 10) - 0.5
+@pytest.mark.parametrize("k,stride,pad", [((1, 2, 2), (1, 2, 2), (0, 0, 0)),
+                                          ((2, 2, 2), (2, 2, 2), (0, 0, 0)),
+                                          ((3, 3, 3), (2, 1, 2), (0, 0, 0)),
+                                          ((3, 3, 3), (1, 1, 1), (1, 1, 1)),
+                                          ((1, 3, 3), (1, 2, 2), (0, 1, 1)),
+                                          ((3, 3, 3), (2, 2, 2), (1, 1, 1))])
+def test_maxpool_exact(dtype, k, stride, pad):
+    # shifted negative so that a padded zero would win if padding took part
+    x64 = synth.clip_input("pool", 2, "halfnormal", 24, 6, 9, 10) - 3.0
     x_t, x_ref = rounded(x64, dtype)
-    y = layers.maxpool3d(to_device_ndhwc(x_t), k, stride, dtype)
-    ref = oracle.maxpool3d(x_ref, k, stride)
+    y = layers.maxpool3d(to_device_ndhwc(x_t), k, stride, dtype, pad=pad)
+    ref = oracle.maxpool3d(x_ref, k, stride, pad)
     assert np.array_equal(from_device_ndhwc(y), ref)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_fused_concatenation_writes_only_its_slice(dtype):
+    """Three layers (dense 1x1x1, KGS 3x3x3, KGS 1x3x3) write channel slices
+    of one wider output, as the branches of an Inception block do; each
+    slice matches its oracle and the channels no layer owns keep their
+    sentinel."""
+    n, thw = 1, (4, 10, 12)
+    specs = [("cat_a", 16, 12, (1, 1, 1), (0, 0, 0), None, 0),
+             ("cat_b", 16, 20, (3, 3, 3), (1, 1, 1), 9, 16),
+             ("cat_c", 16, 8, (1, 3, 3), (0, 1, 1), 4, 40)]
+    c_total = 52  # channels 12..15 and 36..39 and 48..51 belong to nobody
+    x64 = synth.clip_input("cat", n, "halfnormal", 16, *thw)
+    x_t, x_ref = rounded(x64, dtype)
+    x = to_device_ndhwc(x_t)
+    y = torch.full((n, *thw, c_total), -7.0, dtype=layers.TORCH_DTYPES[dtype], device="cuda")
+    refs = []
+    for tag, c_in, c_out, k, pad, keep, off in specs:
+        mask = None if keep is None else masked(tag, c_out, c_in, k, keep)
+        case = LayerCase(tag, n, c_in, c_out, thw, k, (1, 1, 1), pad, dtype, mask)
+        case.x_t, case.x64 = x_t, x_ref
+        case.conv(x, out=y, c_off=off)
+        refs.append((off, c_out, case.oracle_full()))
+    torch.cuda.synchronize()
+    got = from_device_ndhwc(y)
+    owned = np.zeros(c_total, bool)
+    for off, c_out, ref in refs:
+        assert rel_l2(got[:, off:off + c_out], ref) <= TOL[dtype]
+        owned[off:off + c_out] = True
+    assert np.all(got[:, ~owned] == -7.0)
 
 
 # ---------------------------------------------------------------------------
@@ -330,3 +366,77 @@ def test_c3d_batch32_layers(variant, li):
                      l.stride, l.pad, "bf16", mask)
     check_sampled(case, f"b32 {variant} {l.name}", count=2000)
 
+
+
+# ---------------------------------------------------------------------------
+# S3D-shaped stack: Inception blocks (fused concatenation), padded pools
+# ---------------------------------------------------------------------------
+
+def _s3d_oracle_op(op, stack, src64, layer_by_name):
+    """float64 result of one op of the S3D stack on the float64 input src64
+    ([n][c][t][h][w]); a conv returns its c_out channels."""
+    if op[0] == "pool":
+        _, _, _, k, st, pd = op
+        return oracle.maxpool3d(src64, k, st, pd)
+    _, name, _, _, _ = op
+    i, l = layer_by_name[name]
+    d = synth.layer_params("s3d", l)
+    w64 = synth.to_dtype(d.w, stack.dtype).double().numpy()
+    b64 = d.bias.astype(np.float32).astype(np.float64)
+    mask = stack.masks[i]
+    if mask is None:
+        return oracle.conv3d_dense(src64, w64, b64, None, l.stride, l.pad, l.relu)
+    return oracle.conv3d_kgs(src64, w64, mask, *l.g, b64, None, l.stride, l.pad, l.relu)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_s3d_small_clip_every_op(dtype):
+    """The whole S3D-shaped stack at a small clip (8x32x32, KGS at 2.1x):
+    every conv and pool checked against the oracle applied to the GPU's own
+    input buffer of that op (pools bit-exact), and for fp32 the whole chain
+    against the oracle run end to end."""
+    from paper_2007_09835_amd.stack import S3DStack
+    st = S3DStack(1, dtype, "kgs", 2.1, clip=(8, 32))
+    x64 = synth.clip_input("s3d-small", 1, "uniform01", 3, 8, 32, 32)
+    x_t, x_ref = rounded(x64, dtype)
+    st.x.copy_(to_device_ndhwc(x_t))
+    st.forward()
+    torch.cuda.synchronize()
+    layer_by_name = {l.name: (i, l) for i, l in enumerate(st.layers)}
+    host = {name: from_device_ndhwc(buf) for name, buf in st.bufs.items()}
+    chain = {"x": x_ref}
+    for op in st.ops:
+        src, dst = (op[2], op[3]) if op[0] == "conv" else (op[1], op[2])
+        ref = _s3d_oracle_op(op, st, host[src], layer_by_name)
+        if op[0] == "pool":
+            assert np.array_equal(host[dst], ref), op
+        else:
+            off, c_out = op[4], layer_by_name[op[1]][1].c_out
+            err = rel_l2(host[dst][:, off:off + c_out], ref)
+            assert err <= TOL[dtype], (op, err)
+        if dtype == "f32":
+            full = _s3d_oracle_op(op, st, chain[src], layer_by_name)
+            if op[0] == "pool":
+                chain[dst] = full
+            else:
+                if dst not in chain:
+                    chain[dst] = np.zeros_like(host[dst])
+                chain[dst][:, op[4]:op[4] + full.shape[1]] = full
+    if dtype == "f32":
+        assert rel_l2(host[st.out_name], chain[st.out_name]) <= 1e-4
+    print("s3d small", dtype, "ops", len(st.ops), "rate %.2f" % st.kept_rate(), flush=True)
+
+
+S3D_LAYERS = synth.s3d_stack()[0]
+
+
+@pytest.mark.parametrize("li", range(0, len(S3D_LAYERS), 3))
+def test_s3d_layers_full_size(li):
+    """Every third layer of the S3D-shaped stack at its full 16x224x224-clip
+    size, bf16, KGS at 2.1x (1x1x1 layers: whole groups), sampled outputs."""
+    l = S3D_LAYERS[li]
+    d = synth.layer_params("s3d", l)
+    mask = None if l.dense else d.mask
+    case = LayerCase("s3d-" + l.name, 1, l.c_in, l.c_out, (l.t, l.h, l.w), l.k, l.stride, l.pad,
+                     "bf16", mask, x_kind="uniform01" if li == 0 else "halfnormal")
+    check_sampled(case, f"s3d {l.name}")

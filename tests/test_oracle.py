@@ -313,12 +313,17 @@ def test_invalid_mask_byte_is_rejected():
         oracle.conv3d_kgs(x, w, mask, 4, 4)
 
 
-@pytest.mark.parametrize("k,stride", [((1, 2, 2), (1, 2, 2)), ((2, 2, 2), (2, 2, 2)),
-                                      ((3, 3, 3), (2, 1, 2))])
-def test_maxpool_matches_torch(k, stride):
-    x = np.random.default_rng(6).standard_normal((2, 3, 5, 7, 9))
-    y = oracle.maxpool3d(x, k, stride)
-    ref = F.max_pool3d(torch.from_numpy(x), k, stride).numpy()
+@pytest.mark.parametrize("k,stride,pad", [((1, 2, 2), (1, 2, 2), (0, 0, 0)),
+                                          ((2, 2, 2), (2, 2, 2), (0, 0, 0)),
+                                          ((3, 3, 3), (2, 1, 2), (0, 0, 0)),
+                                          ((3, 3, 3), (1, 1, 1), (1, 1, 1)),
+                                          ((1, 3, 3), (1, 2, 2), (0, 1, 1)),
+                                          ((3, 3, 3), (2, 2, 2), (1, 1, 1))])
+def test_maxpool_matches_torch(k, stride, pad):
+    # negative inputs: a padded zero would win if padding took part
+    x = np.random.default_rng(6).standard_normal((2, 3, 5, 7, 9)) - 3.0
+    y = oracle.maxpool3d(x, k, stride, pad)
+    ref = F.max_pool3d(torch.from_numpy(x), k, stride, pad).numpy()
     assert np.array_equal(y, ref)
 
 
