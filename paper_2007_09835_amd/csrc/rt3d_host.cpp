@@ -1234,6 +1234,8 @@ rt3d_status rt3d_maxpool3d_fwd(int32_t n, int32_t c, int32_t t, int32_t h, int32
     return fail(RT3D_ERR_INVALID_ARG, "device pointers must be 16-byte aligned");
   const int to = (t + 2 * pt - kt) / st + 1, ho = (h + 2 * ph - kh) / sh + 1,
             wo = (w + 2 * pw - kw) / sw + 1;
+  if (static_cast<long>(n) * to * ho * wo >= (1l << 24))
+    return fail(RT3D_ERR_UNSUPPORTED, "2^24 or more output voxels per call");
   const int e = launch_maxpool(n, c, t, h, w, kt, kh, kw, st, sh, sw, pt, ph, pw, to, ho, wo, dtype,
                                x, y, stream);
   if (e != hipSuccess)

@@ -17,6 +17,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 
 #include <type_traits>
@@ -1218,51 +1219,91 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(ConvArgs a) {
 // and run of VEC channels.
 // ---------------------------------------------------------------------------
 
-template <typename T, int VEC>
+struct PoolArgs {
+  int n, c, t, h, w, kt, kh, kw, st, sh, sw, pt, ph, pw, to, ho, wo;
+  int cv;       // channel vectors per voxel (c / VEC)
+  int item0;    // first (voxel, channel vector) item of this launch
+  int items;    // items of this launch (< 2^24)
+};
+
+// One thread per (output voxel, VEC-channel vector); channel vectors are
+// the fastest index, so a wave reads and writes contiguous 16-byte runs.
+// KT/KH/KW > 0: a compile-time window, unrolled so that all its loads are in
+// flight together (from clamped, always valid addresses; positions outside
+// the input are dropped at the max); 0: the window from the arguments.
+template <typename T, int VEC, int KT, int KH, int KW>
 __global__ __launch_bounds__(256) void maxpool_kernel(const T *__restrict__ x, T *__restrict__ y,
-                                                      int n, int c, int t, int h, int w, int kt,
-                                                      int kh, int kw, int st, int sh, int sw,
-                                                      int pt, int ph, int pw, int to, int ho,
-                                                      int wo) {
-  const long cv = c / VEC;
-  const long total = static_cast<long>(n) * to * ho * wo * cv;
-  for (long idx = static_cast<long>(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
-       idx += static_cast<long>(gridDim.x) * blockDim.x) {
-    const int cb = static_cast<int>(idx % cv);
-    long r = idx / cv;
-    const int ow = static_cast<int>(r % wo);
-    r /= wo;
-    const int oh = static_cast<int>(r % ho);
-    r /= ho;
-    const int ot = static_cast<int>(r % to);
-    const long nb = r / to;
-    // Padded positions take no part (every window holds at least one input
-    // voxel: the host keeps the padding at most half the window).
-    float best[VEC];
-    bool any = false;
-    for (int e = 0; e < VEC; ++e) best[e] = 0.f;
-    for (int it = 0; it < kt; ++it) {
-      const int zt = ot * st - pt + it;
-      if (zt < 0 || zt >= t) continue;
-      for (int ih = 0; ih < kh; ++ih) {
-        const int zh = oh * sh - ph + ih;
-        if (zh < 0 || zh >= h) continue;
-        for (int iw = 0; iw < kw; ++iw) {
-          const int zw = ow * sw - pw + iw;
-          if (zw < 0 || zw >= w) continue;
-          const long vox = ((nb * t + zt) * h + zh) * w + zw;
-          const T *src = x + vox * c + cb * VEC;
-          for (int e = 0; e < VEC; ++e) {
-            const float v = static_cast<float>(src[e]);
-            best[e] = (!any || v > best[e]) ? v : best[e];
-          }
-          any = true;
+                                                      PoolArgs p) {
+  const int item = static_cast<int>(blockIdx.x) * 256 + static_cast<int>(threadIdx.x);
+  if (item >= p.items) return;
+  const DivMod vc = divmod(item, p.cv);     // local item: < 2^24
+  const int cb = vc.r;
+  const int vox = vc.q + p.item0 / p.cv;    // item0 is a multiple of cv
+  const DivMod a = divmod(vox, p.wo);
+  const DivMod b = divmod(a.q, p.ho);
+  const DivMod d = divmod(b.q, p.to);
+  const int ow = a.r, oh = b.r, ot = d.r, nb = d.q;
+  using Vec = std::conditional_t<VEC * sizeof(T) == 16, uint4, T>;
+  union Pack { Vec u; T e[VEC]; };
+  float best[VEC];
+  bool any = false;
+  for (int e = 0; e < VEC; ++e) best[e] = 0.f;
+  auto take = [&](const Pack &v, bool ok) {
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const float f = static_cast<float>(v.e[e]);
+      best[e] = ok && (!any || f > best[e]) ? f : best[e];
+    }
+    any = any || ok;
+  };
+  auto load = [&](int zt, int zh, int zw) {
+    Pack v;
+    const long vx = ((static_cast<long>(nb) * p.t + zt) * p.h + zh) * p.w + zw;
+    v.u = *reinterpret_cast<const Vec *>(x + vx * p.c + cb * VEC);
+    return v;
+  };
+  if constexpr (KT > 0) {
+    Pack v[KT][KH][KW];
+#pragma unroll
+    for (int it = 0; it < KT; ++it)
+#pragma unroll
+      for (int ih = 0; ih < KH; ++ih)
+#pragma unroll
+        for (int iw = 0; iw < KW; ++iw)
+          v[it][ih][iw] = load(min(max(ot * p.st - p.pt + it, 0), p.t - 1),
+                               min(max(oh * p.sh - p.ph + ih, 0), p.h - 1),
+                               min(max(ow * p.sw - p.pw + iw, 0), p.w - 1));
+#pragma unroll
+    for (int it = 0; it < KT; ++it)
+#pragma unroll
+      for (int ih = 0; ih < KH; ++ih)
+#pragma unroll
+        for (int iw = 0; iw < KW; ++iw) {
+          const int zt = ot * p.st - p.pt + it, zh = oh * p.sh - p.ph + ih,
+                    zw = ow * p.sw - p.pw + iw;
+          take(v[it][ih][iw], zt >= 0 && zt < p.t && zh >= 0 && zh < p.h && zw >= 0 && zw < p.w);
+        }
+  } else {
+    for (int it = 0; it < p.kt; ++it) {
+      const int zt = ot * p.st - p.pt + it;
+      if (zt < 0 || zt >= p.t) continue;
+      for (int ih = 0; ih < p.kh; ++ih) {
+        const int zh = oh * p.sh - p.ph + ih;
+        if (zh < 0 || zh >= p.h) continue;
+        for (int iw = 0; iw < p.kw; ++iw) {
+          const int zw = ow * p.sw - p.pw + iw;
+          if (zw < 0 || zw >= p.w) continue;
+          take(load(zt, zh, zw), true);
         }
       }
     }
-    T *dst = y + (((nb * to + ot) * ho + oh) * wo + ow) * c + cb * VEC;
-    for (int e = 0; e < VEC; ++e) dst[e] = static_cast<T>(best[e]);
   }
+  // (the host keeps padding at most half the window: every window holds
+  // at least one input voxel, so `any` is set here)
+  Pack o;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) o.e[e] = static_cast<T>(best[e]);
+  *reinterpret_cast<Vec *>(y + static_cast<long>(vox) * p.c + cb * VEC) = o.u;
 }
 
 // ---------------------------------------------------------------------------
@@ -1623,29 +1664,54 @@ int launch_kgs_exact_f32(const ConvArgs &a, void *stream) {
   return launch_conv(kgs_exact_f32_kernel<2>, a, stream);
 }
 
+// The windows of the C3D and S3D stacks get unrolled kernels.
+template <typename T, int VEC>
+void pool_launch(dim3 grid, hipStream_t s, const void *x, void *y, const PoolArgs &p) {
+  const T *xs = static_cast<const T *>(x);
+  T *ys = static_cast<T *>(y);
+  auto win = [&](int a, int b, int c) { return p.kt == a && p.kh == b && p.kw == c; };
+  if (win(3, 3, 3))
+    hipLaunchKernelGGL((maxpool_kernel<T, VEC, 3, 3, 3>), grid, dim3(256), 0, s, xs, ys, p);
+  else if (win(1, 3, 3))
+    hipLaunchKernelGGL((maxpool_kernel<T, VEC, 1, 3, 3>), grid, dim3(256), 0, s, xs, ys, p);
+  else if (win(2, 2, 2))
+    hipLaunchKernelGGL((maxpool_kernel<T, VEC, 2, 2, 2>), grid, dim3(256), 0, s, xs, ys, p);
+  else if (win(1, 2, 2))
+    hipLaunchKernelGGL((maxpool_kernel<T, VEC, 1, 2, 2>), grid, dim3(256), 0, s, xs, ys, p);
+  else
+    hipLaunchKernelGGL((maxpool_kernel<T, VEC, 0, 0, 0>), grid, dim3(256), 0, s, xs, ys, p);
+}
+
 int launch_maxpool(int n, int c, int t, int h, int w, int kt, int kh, int kw, int st, int sh,
                    int sw, int pt, int ph, int pw, int to, int ho, int wo, int dtype,
                    const void *x, void *y, void *stream) {
   const long outs = static_cast<long>(n) * to * ho * wo;
   if (outs == 0 || c == 0) return hipSuccess;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  auto grid_for = [&](long items) {
-    long blocks = (items + 255) / 256;
-    return static_cast<unsigned>(blocks < 65536 ? blocks : 65536);
-  };
-#define RT3D_POOL(T, VEC)                                                                      \
-  hipLaunchKernelGGL((maxpool_kernel<T, VEC>), dim3(grid_for(outs * (c / VEC))), dim3(256), 0, s, \
-                     static_cast<const T *>(x), static_cast<T *>(y), n, c, t, h, w, kt, kh, kw,   \
-                     st, sh, sw, pt, ph, pw, to, ho, wo)
-  if (dtype == RT3D_F32) {
-    if (c % 4 == 0) RT3D_POOL(float, 4); else RT3D_POOL(float, 1);
-  } else if (dtype == RT3D_BF16) {
-    if (c % 8 == 0) RT3D_POOL(__bf16, 8); else RT3D_POOL(__bf16, 1);
-  } else {
-    if (c % 8 == 0) RT3D_POOL(_Float16, 8); else RT3D_POOL(_Float16, 1);
+  const int vec = dtype == RT3D_F32 ? (c % 4 == 0 ? 4 : 1) : (c % 8 == 0 ? 8 : 1);
+  PoolArgs p{n, c, t, h, w, kt, kh, kw, st, sh, sw, pt, ph, pw, to, ho, wo, c / vec, 0, 0};
+  // Launches of whole voxels with fewer than 2^24 items each (the fast
+  // divide in the kernel needs that).
+  const long per_launch = ((1l << 24) - 1) / p.cv * p.cv;
+  const long total = outs * p.cv;
+  for (long first = 0; first < total; first += per_launch) {
+    p.item0 = static_cast<int>(first);
+    p.items = static_cast<int>(std::min(per_launch, total - first));
+    const dim3 grid(static_cast<unsigned>((p.items + 255) / 256));
+    if (dtype == RT3D_F32) {
+      if (vec == 4) pool_launch<float, 4>(grid, s, x, y, p);
+      else pool_launch<float, 1>(grid, s, x, y, p);
+    } else if (dtype == RT3D_BF16) {
+      if (vec == 8) pool_launch<__bf16, 8>(grid, s, x, y, p);
+      else pool_launch<__bf16, 1>(grid, s, x, y, p);
+    } else {
+      if (vec == 8) pool_launch<_Float16, 8>(grid, s, x, y, p);
+      else pool_launch<_Float16, 1>(grid, s, x, y, p);
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-#undef RT3D_POOL
-  return hipGetLastError();
+  return hipSuccess;
 }
 
 int launch_group_reweight(const GroupArgs &a, int dtype, int norm, int scope, size_t lds,
