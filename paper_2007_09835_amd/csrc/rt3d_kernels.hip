@@ -222,12 +222,16 @@ __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, cons
 // commit() writes them to LDS.  The kernels issue chunk c+1 before computing
 // chunk c, so the loads overlap the MFMA work.  `ok` is false when the halo
 // needs more than MAXI pieces per thread; the kernels then use stage_halo.
-template <int ES, int MAXI>
+// FAST (c_in a multiple of the piece): every piece is one 16-byte load from
+// a clamped, always valid address, and pieces that are padding are zeroed
+// at commit, so the loads issue back to back without branches.
+template <int ES, int MAXI, bool FAST = false>
 struct Stager {
   static constexpr int EPP = 16 / ES;
   int vox[MAXI];   // flat input voxel; -1 padding (zeros); -2 no piece
   uint4 d[MAXI];
   int total, shift, ppr;
+  unsigned live;   // FAST: bit k set when piece k holds input data
   bool ok;
 
   __device__ __forceinline__ void init(const ConvArgs &a, const Brick &b) {
@@ -263,8 +267,22 @@ struct Stager {
   }
 
   __device__ __forceinline__ void issue(const ConvArgs &a, int c0) {
-    const bool vec = (a.c_in % EPP) == 0;
     const uint8_t *xb = static_cast<const uint8_t *>(a.x);
+    if constexpr (FAST) {
+      unsigned bits = 0;
+#pragma unroll
+      for (int k = 0; k < MAXI; ++k) {
+        const int idx = threadIdx.x + k * blockDim.x;
+        const int c = c0 + (idx & (ppr - 1)) * EPP;
+        const bool in = vox[k] >= 0 && c < a.c_in;
+        const long el = static_cast<long>(max(vox[k], 0)) * a.c_in + min(c, a.c_in - EPP);
+        d[k] = *reinterpret_cast<const uint4 *>(xb + el * ES);
+        bits |= (in ? 1u : 0u) << k;
+      }
+      live = bits;
+      return;
+    }
+    const bool vec = (a.c_in % EPP) == 0;
 #pragma unroll
     for (int k = 0; k < MAXI; ++k) {
       const int idx = threadIdx.x + k * blockDim.x;
@@ -298,7 +316,11 @@ struct Stager {
     for (int k = 0; k < MAXI; ++k) {
       const int idx = threadIdx.x + k * blockDim.x;
       if (vox[k] != -2) {
-        *reinterpret_cast<uint4 *>(lds + (idx >> shift) * a.row + (idx & (ppr - 1)) * 16) = d[k];
+        uint4 v = d[k];
+        if constexpr (FAST) {
+          if (!((live >> k) & 1u)) v = make_uint4(0, 0, 0, 0);
+        }
+        *reinterpret_cast<uint4 *>(lds + (idx >> shift) * a.row + (idx & (ppr - 1)) * 16) = v;
       }
     }
   }
@@ -495,7 +517,8 @@ __device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, co
 // groups keep, with the pruned entries of that union stored as zero weights.
 // ---------------------------------------------------------------------------
 
-template <typename T, int MFW, int NF>
+// FAST: c_in is a multiple of 8 (branch-free halo staging).
+template <typename T, int MFW, int NF, bool FAST>
 __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
   using V8 = std::conditional_t<std::is_same_v<T, __bf16>, bf16x8, f16x8>;
   // Software pipeline of a wave (step t = one K-step of 8 items):
@@ -573,7 +596,7 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
   const uint32_t S0 = uniform(sp[ch0]), S1 = uniform(sp[ch1]);
   const bool work = active && S1 > S0;
   const uint32_t LAST = work ? S1 - 1 : S0;
-  Stager<2, 8> st;
+  Stager<2, 8, FAST> st;
   st.init(a, b);
   if (st.ok && ch0 < ch1) st.issue(a, ch0 * a.cc);
   if (work) {
@@ -1552,13 +1575,13 @@ int conv_resident(int variant, int dtype, int mfw, size_t lds) {
     case kVarDenseItems16:
     case kVarKgsUnion16:
       if (dtype == RT3D_BF16) {
-        if (mfw == 1) return resident(items16_kernel<__bf16, 1, 8>, lds);
-        if (mfw == 2) return resident(items16_kernel<__bf16, 2, 8>, lds);
-        if (mfw == 4) return resident(items16_kernel<__bf16, 4, 8>, lds);
+        if (mfw == 1) return resident(items16_kernel<__bf16, 1, 8, true>, lds);
+        if (mfw == 2) return resident(items16_kernel<__bf16, 2, 8, true>, lds);
+        if (mfw == 4) return resident(items16_kernel<__bf16, 4, 8, true>, lds);
       } else {
-        if (mfw == 1) return resident(items16_kernel<_Float16, 1, 8>, lds);
-        if (mfw == 2) return resident(items16_kernel<_Float16, 2, 8>, lds);
-        if (mfw == 4) return resident(items16_kernel<_Float16, 4, 8>, lds);
+        if (mfw == 1) return resident(items16_kernel<_Float16, 1, 8, true>, lds);
+        if (mfw == 2) return resident(items16_kernel<_Float16, 2, 8, true>, lds);
+        if (mfw == 4) return resident(items16_kernel<_Float16, 4, 8, true>, lds);
       }
       return 0;
     case kVarDenseItemsF32:
@@ -1625,15 +1648,20 @@ int small_resident(const ConvArgs &a, int dtype, int mfw) {
 }
 
 int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream) {
+  const bool fast = a.c_in % 8 == 0;
+#define RT3D_ITEMS16(T, M)                                                         \
+  return fast ? launch_conv(items16_kernel<T, M, 8, true>, a, stream)              \
+              : launch_conv(items16_kernel<T, M, 8, false>, a, stream)
   if (dtype == RT3D_BF16) {
-    if (mfw == 1) return launch_conv(items16_kernel<__bf16, 1, 8>, a, stream);
-    if (mfw == 2) return launch_conv(items16_kernel<__bf16, 2, 8>, a, stream);
-    if (mfw == 4) return launch_conv(items16_kernel<__bf16, 4, 8>, a, stream);
+    if (mfw == 1) RT3D_ITEMS16(__bf16, 1);
+    if (mfw == 2) RT3D_ITEMS16(__bf16, 2);
+    if (mfw == 4) RT3D_ITEMS16(__bf16, 4);
   } else if (dtype == RT3D_F16) {
-    if (mfw == 1) return launch_conv(items16_kernel<_Float16, 1, 8>, a, stream);
-    if (mfw == 2) return launch_conv(items16_kernel<_Float16, 2, 8>, a, stream);
-    if (mfw == 4) return launch_conv(items16_kernel<_Float16, 4, 8>, a, stream);
+    if (mfw == 1) RT3D_ITEMS16(_Float16, 1);
+    if (mfw == 2) RT3D_ITEMS16(_Float16, 2);
+    if (mfw == 4) RT3D_ITEMS16(_Float16, 4);
   }
+#undef RT3D_ITEMS16
   return hipErrorInvalidValue;
 }
 
