@@ -276,12 +276,18 @@ rt3d_status canon_index(const rt3d_conv3d_desc *d, const uint8_t *mask, Canon &c
 // 12 halo lines of <= 192 elements per brick, the kernel's register budget),
 // and no pooling or the 1x2x2 window (pooled in registers).  Disable with
 // RT3D_SMALL_KERNEL=0.
+// The small-channel kernel: c_in <= 4 (one 4-channel block per tap), a
+// halo of at most 12 lines (kt * (sh + kh)) of at most 256 elements
+// ((31 sw + kw) * c_in), at most 64 taps (8 K-steps of 8), and pooling that
+// is either absent or 1x2x2 (the brick's two rows and adjacent lanes).
 bool small_ok(const Geom &g) {
   if (const char *env = std::getenv("RT3D_SMALL_KERNEL"))
     if (std::atoi(env) == 0) return false;
   const bool pool_ok = (g.qt == 1 && g.qh == 1 && g.qw == 1) || (g.qt == 1 && g.qh == 2 && g.qw == 2);
-  return g.es == 2 && g.c_in <= 4 && g.kt <= 3 && g.kh <= 3 && g.kw <= 3 && g.st == 1 &&
-         g.sh == 1 && g.sw == 1 && pool_ok;
+  const int lines = g.kt * (g.sh + g.kh);
+  const int line_elems = (31 * g.sw + g.kw) * g.c_in;
+  return g.es == 2 && g.c_in <= 4 && lines <= 12 && line_elems <= 256 &&
+         g.kt * g.kh * g.kw <= 64 && pool_ok;
 }
 
 // Bricks of 1 x 2 x 32 output voxels; halo rows of 4 channels (8 bytes).
@@ -291,8 +297,8 @@ Tiling small_tiling(const Geom &g) {
   t.bh = 2;
   t.bw = 32;
   t.ht = g.kt;
-  t.hh = 1 + g.kh;
-  t.hw = 31 + g.kw;
+  t.hh = g.sh + g.kh;
+  t.hw = 31 * g.sw + g.kw;
   t.cc = 4;
   t.row = 8;
   t.slots = 64;
@@ -903,6 +909,7 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   ConvArgs a{};
   a.x = x;
   a.y = y;
+  a.steps_max = p.tile_steps;
   a.y_pitch = d->y_c_total != 0 ? d->y_c_total : d->c_out;
   a.y_off = d->y_c_off;
   a.res = residual;

@@ -82,7 +82,7 @@ struct ConvArgs {
   int32_t grid;       // workgroups launched (0: one per tile); fewer loop over tiles
   int32_t y_pitch;    // channels per voxel of y (>= c_out: fused concatenation)
   int32_t y_off;      // first channel of y this layer writes
-  int32_t pad1;
+  int32_t steps_max;  // most K-steps of one wave tile (the plan's tile_steps)
 };
 
 // Launch shape chosen at forward time from the batch size.

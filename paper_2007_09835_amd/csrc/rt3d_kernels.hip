@@ -702,15 +702,17 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
 // Halo rows hold 4 channels (8 bytes); channels >= c_in stay zero.
 // ---------------------------------------------------------------------------
 
-constexpr int kSmallLines = 12;      // halo lines (t, h) per brick: kt * (kh + 1) <= 12
+constexpr int kSmallLines = 12;      // halo lines (t, h) per brick: kt * (sh + kh) <= 12
 
 // LL = halo-line elements per lane (hw * c_in <= 64 * LL).  RES: the layer
 // adds a residual (a separate instantiation keeps the common epilogue short).
-template <typename T, int MFW, int LL, bool RES>
+// STEPS: K-steps held in registers (4: kernels up to 32 taps; 8: up to 64,
+// e.g. the 1x7x7 stem convs).
+template <typename T, int MFW, int LL, bool RES, int STEPS>
 __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
   constexpr int kSmallLineLoads = LL;
   using V8 = std::conditional_t<std::is_same_v<T, __bf16>, bf16x8, f16x8>;
-  constexpr int NF = 4, STEPS = 4;
+  constexpr int NF = 4;
   extern __shared__ __align__(16) uint8_t lds[];
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
@@ -785,7 +787,7 @@ __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
   const int nlines = a.ht * a.hh;
   uint16_t sv[kSmallLines][kSmallLineLoads];
   unsigned long long okbits = 0;  // element (L, k) is inside the input (else it stages a zero)
-  static_assert(kSmallLines * 3 <= 64, "ok bits");
+  static_assert(kSmallLines * kSmallLineLoads <= 64, "ok bits");
   const uint16_t *xin = static_cast<const uint16_t *>(a.x);
   // Staging is branch-free: every lane loads from a clamped in-range address
   // and selects zero where the element is padding, and writes go to a sink
@@ -793,24 +795,34 @@ __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
   // back to back and the LDS writes wait once.
   auto issue = [&](int br) {
     const Brick b = decode_brick(a, br);
+    // Column offsets within a line are the same for every line of the
+    // brick; each line's base address is uniform (scalar registers), so a
+    // load is a scalar base plus one 32-bit lane offset.
+    int eo[kSmallLineLoads];
+    unsigned colok = 0;
+#pragma unroll
+    for (int k = 0; k < kSmallLineLoads; ++k) {
+      const int zw = b.zw0 + ex[k];
+      colok |= (lane + 64 * k < line_len && zw >= 0 && zw < a.w ? 1u : 0u) << k;
+      eo[k] = min(max(zw, 0), a.w - 1) * a.c_in + ec[k];
+    }
+    unsigned long long bits = 0;
 #pragma unroll
     for (int L = 0; L < kSmallLines; ++L) {
       const DivMod lt = divmod(L, a.hh);
       const int zt = b.zt0 + lt.q, zh = b.zh0 + lt.r;
       const bool line_ok = L < nlines && zt >= 0 && zt < a.t && zh >= 0 && zh < a.h;
       const int ztc = min(max(zt, 0), a.t - 1), zhc = min(max(zh, 0), a.h - 1);
-      const long base = ((static_cast<long>(b.nb) * a.t + ztc) * a.h + zhc) * a.w;
+      const int row = uniform((b.nb * a.t + ztc) * a.h + zhc);  // < 2^31: checked on the host
+      const uint16_t *lp = xin + static_cast<long>(row) * (a.w * a.c_in);
 #pragma unroll
-      for (int k = 0; k < kSmallLineLoads; ++k) {
-        const int zw = b.zw0 + ex[k];
-        const bool ok = line_ok && lane + 64 * k < line_len && zw >= 0 && zw < a.w;
-        const int zwc = min(max(zw, 0), a.w - 1);
-        sv[L][k] = xin[(base + zwc) * a.c_in + ec[k]];  // selected at commit, after the wait
-        okbits = (okbits & ~(1ull << (L * kSmallLineLoads + k))) |
-                 (static_cast<unsigned long long>(ok) << (L * kSmallLineLoads + k));
-      }
+      for (int k = 0; k < kSmallLineLoads; ++k)
+        sv[L][k] = lp[static_cast<unsigned>(eo[k])];  // selected at commit
+      if (line_ok) bits |= static_cast<unsigned long long>(colok) << (L * kSmallLineLoads);
     }
+    okbits = bits;
   };
+
   auto commit = [&](uint8_t *buf) {
 #pragma unroll
     for (int L = 0; L < kSmallLines; ++L)
@@ -1612,24 +1624,29 @@ int launch_small(K kernel, const ConvArgs &a, void *stream) {
   return hipGetLastError();
 }
 
-int small_line_loads(const ConvArgs &a) { return a.hw * a.c_in <= 128 ? 2 : 3; }
+int small_line_loads(const ConvArgs &a) { return a.hw * a.c_in <= 128 ? 2 : 3; }  // 4 with 8 steps
 
 #define RT3D_SMALL_LL(T, M, FN, ...)                                                     \
   do {                                                                                   \
+    if (steps8)                                                                          \
+      return res ? FN((small_kernel<T, M, 4, true, 8>), __VA_ARGS__)                     \
+                 : FN((small_kernel<T, M, 4, false, 8>), __VA_ARGS__);                   \
     if (ll == 2)                                                                         \
-      return res ? FN((small_kernel<T, M, 2, true>), __VA_ARGS__)                        \
-                 : FN((small_kernel<T, M, 2, false>), __VA_ARGS__);                      \
-    return res ? FN((small_kernel<T, M, 3, true>), __VA_ARGS__)                          \
-               : FN((small_kernel<T, M, 3, false>), __VA_ARGS__);                        \
+      return res ? FN((small_kernel<T, M, 2, true, 4>), __VA_ARGS__)                     \
+                 : FN((small_kernel<T, M, 2, false, 4>), __VA_ARGS__);                   \
+    return res ? FN((small_kernel<T, M, 3, true, 4>), __VA_ARGS__)                       \
+               : FN((small_kernel<T, M, 3, false, 4>), __VA_ARGS__);                     \
   } while (0)
 #define RT3D_SMALL_MFW(T, FN, ...)                                                       \
   do {                                                                                   \
     if (mfw == 1) RT3D_SMALL_LL(T, 1, FN, __VA_ARGS__);                                  \
     if (mfw == 2) RT3D_SMALL_LL(T, 2, FN, __VA_ARGS__);                                  \
   } while (0)
+// Kernels with more than 4 K-steps (up to 8) use 4 line loads per lane.
 #define RT3D_SMALL_DISPATCH(FN, ...)                                                     \
   do {                                                                                   \
     const int ll = small_line_loads(a);                                                  \
+    const bool steps8 = a.steps_max > 4;                                                 \
     const bool res = a.res != nullptr;                                                   \
     if (dtype == RT3D_BF16) RT3D_SMALL_MFW(__bf16, FN, __VA_ARGS__);                      \
     else RT3D_SMALL_MFW(_Float16, FN, __VA_ARGS__);                                      \

@@ -101,15 +101,20 @@ SMALL_CIN = [
     ("c3", 1, 4, 20, (2, 6, 33), (1, 3, 3), (0, 1, 1), (1, 1, 1), "bf16", False, True),
     ("c4", 1, 1, 16, (5, 5, 9), (3, 3, 3), (0, 1, 1), (1, 2, 2), "bf16", True, False),
     ("c5", 3, 2, 64, (3, 9, 40), (3, 1, 3), (1, 0, 1), (1, 2, 2), "f16", False, True),
+    # 1x7x7 stride (1,2,2) stems (S3D 3->64, R(2+1)D 3->45: 8 K-steps) and a 5x5 tap window
+    ("c6", 1, 3, 64, (3, 13, 75), (1, 7, 7), (0, 3, 3), (1, 1, 1), "bf16", False, False),
+    ("c7", 2, 3, 45, (2, 9, 66), (1, 7, 7), (0, 3, 3), (1, 1, 1), "f16", True, False),
+    ("c8", 1, 2, 20, (2, 8, 40), (1, 5, 5), (0, 2, 2), (1, 2, 2), "bf16", False, True),
 ]
+SMALL_CIN_STRIDE = {"c6": (1, 2, 2), "c7": (1, 2, 2)}
 
 
 @pytest.mark.parametrize("ci", range(len(SMALL_CIN)))
 def test_small_input_channel_layers(ci):
     tag, n, c_in, c_out, thw, k, pad, pool, dtype, sparse, residual = SMALL_CIN[ci]
     mask = masked(tag, c_out, c_in, k, max(1, (k[0] * k[1] * k[2]) // 3)) if sparse else None
-    case = LayerCase(tag, n, c_in, c_out, thw, k, (1, 1, 1), pad, dtype, mask, residual=residual,
-                     pool=pool)
+    case = LayerCase(tag, n, c_in, c_out, thw, k, SMALL_CIN_STRIDE.get(tag, (1, 1, 1)), pad, dtype,
+                     mask, residual=residual, pool=pool)
     assert case.conv.info.variant in (5, 6), case.conv.info.variant
     check_full(case, f"small c_in {tag} {dtype} {'kgs' if sparse else 'dense'}")
 
