@@ -85,6 +85,11 @@ typedef struct {
                                  y_c_off + c_out <= y_c_total, and both y_c_total and
                                  y_c_off are multiples of 4.  The residual always has
                                  c_out channels per voxel. */
+    int32_t x_c_total, x_c_off; /* channel slice of the input: x holds x_c_total
+                                 channels per voxel and the layer reads channels
+                                 [x_c_off, x_c_off + c_in) (a layer consuming part of a
+                                 wider tensor).  0, 0 = x has exactly c_in channels.
+                                 Layers with c_in <= 4 (network inputs) need 0, 0. */
 } rt3d_conv3d_desc;
 
 /* Filled by the pack calls; plain data owned by the caller.  It describes

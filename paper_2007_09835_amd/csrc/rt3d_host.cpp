@@ -88,6 +88,14 @@ rt3d_status check_desc(const rt3d_conv3d_desc *d, bool need_groups) {
     if (d->y_c_total % 4 != 0 || d->y_c_off % 4 != 0)
       return fail(RT3D_ERR_UNSUPPORTED, "y_c_total and y_c_off must be multiples of 4");
   }
+  if (d->x_c_total != 0 || d->x_c_off != 0) {
+    if (d->x_c_off < 0 || d->x_c_total < d->c_in ||
+        static_cast<long>(d->x_c_off) + d->c_in > d->x_c_total)
+      return fail(RT3D_ERR_INVALID_ARG, "input channels [%d, %d) do not fit x_c_total=%d",
+                  d->x_c_off, d->x_c_off + d->c_in, d->x_c_total);
+    if (d->c_in <= 4 && (d->x_c_total != d->c_in || d->x_c_off != 0))
+      return fail(RT3D_ERR_UNSUPPORTED, "layers with c_in <= 4 read whole voxels");
+  }
   if (need_groups) {
     auto okg = [](int g) { return g == 4 || g == 8 || g == 16; };
     if (!okg(d->g_m) || !okg(d->g_n))
@@ -912,6 +920,8 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   a.steps_max = p.tile_steps;
   a.y_pitch = d->y_c_total != 0 ? d->y_c_total : d->c_out;
   a.y_off = d->y_c_off;
+  a.x_pitch = d->x_c_total != 0 ? d->x_c_total : d->c_in;
+  a.x_off = d->x_c_off;
   a.res = residual;
   a.bias = bias;
   a.step_ptr = reinterpret_cast<const uint32_t *>(b + p.step_ptr_off);

@@ -83,6 +83,9 @@ struct ConvArgs {
   int32_t y_pitch;    // channels per voxel of y (>= c_out: fused concatenation)
   int32_t y_off;      // first channel of y this layer writes
   int32_t steps_max;  // most K-steps of one wave tile (the plan's tile_steps)
+  int32_t x_pitch;    // channels per voxel of x (>= c_in: a slice of a wider tensor)
+  int32_t x_off;      // first channel of x this layer reads
+  int32_t pad2;
 };
 
 // Launch shape chosen at forward time from the batch size.

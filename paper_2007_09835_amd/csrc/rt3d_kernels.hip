@@ -181,7 +181,7 @@ __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, cons
   constexpr int EPP = 16 / ES;                 // elements per 16-byte piece
   const int ppr = a.cc / EPP;                  // pieces per halo row
   const int total = a.ht * a.hh * a.hw * ppr;
-  const bool vec = (a.c_in % EPP) == 0;
+  const bool vec = (a.c_in % EPP) == 0 && (a.x_pitch % EPP) == 0 && (a.x_off % EPP) == 0;
   const uint8_t *xb = static_cast<const uint8_t *>(a.x);
   for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
     const DivMod p = divmod(idx, ppr), x = divmod(p.q, a.hw), y = divmod(x.q, a.hh);
@@ -192,7 +192,7 @@ __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, cons
     uint4 v = make_uint4(0, 0, 0, 0);
     if (zt >= 0 && zt < a.t && zh >= 0 && zh < a.h && zw >= 0 && zw < a.w && c < a.c_in) {
       const long vox = ((static_cast<long>(b.nb) * a.t + zt) * a.h + zh) * a.w + zw;
-      const uint8_t *src = xb + (vox * a.c_in + c) * ES;
+      const uint8_t *src = xb + (vox * a.x_pitch + a.x_off + c) * ES;
       if (vec) {
         v = *reinterpret_cast<const uint4 *>(src);
       } else {
@@ -222,7 +222,8 @@ __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, cons
 // commit() writes them to LDS.  The kernels issue chunk c+1 before computing
 // chunk c, so the loads overlap the MFMA work.  `ok` is false when the halo
 // needs more than MAXI pieces per thread; the kernels then use stage_halo.
-// FAST (c_in a multiple of the piece): every piece is one 16-byte load from
+// FAST (c_in, the input pitch and the input offset multiples of the piece):
+// every piece is one 16-byte load from
 // a clamped, always valid address, and pieces that are padding are zeroed
 // at commit, so the loads issue back to back without branches.
 template <int ES, int MAXI, bool FAST = false>
@@ -275,21 +276,22 @@ struct Stager {
         const int idx = threadIdx.x + k * blockDim.x;
         const int c = c0 + (idx & (ppr - 1)) * EPP;
         const bool in = vox[k] >= 0 && c < a.c_in;
-        const long el = static_cast<long>(max(vox[k], 0)) * a.c_in + min(c, a.c_in - EPP);
+        const long el =
+            static_cast<long>(max(vox[k], 0)) * a.x_pitch + a.x_off + min(c, a.c_in - EPP);
         d[k] = *reinterpret_cast<const uint4 *>(xb + el * ES);
         bits |= (in ? 1u : 0u) << k;
       }
       live = bits;
       return;
     }
-    const bool vec = (a.c_in % EPP) == 0;
+    const bool vec = (a.c_in % EPP) == 0 && (a.x_pitch % EPP) == 0 && (a.x_off % EPP) == 0;
 #pragma unroll
     for (int k = 0; k < MAXI; ++k) {
       const int idx = threadIdx.x + k * blockDim.x;
       const int c = c0 + (idx & (ppr - 1)) * EPP;
       uint4 v = make_uint4(0, 0, 0, 0);
       if (vox[k] >= 0 && c < a.c_in) {
-        const uint8_t *src = xb + (static_cast<long>(vox[k]) * a.c_in + c) * ES;
+        const uint8_t *src = xb + (static_cast<long>(vox[k]) * a.x_pitch + a.x_off + c) * ES;
         if (vec) {
           v = *reinterpret_cast<const uint4 *>(src);
         } else {
@@ -1665,7 +1667,7 @@ int small_resident(const ConvArgs &a, int dtype, int mfw) {
 }
 
 int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream) {
-  const bool fast = a.c_in % 8 == 0;
+  const bool fast = a.c_in % 8 == 0 && a.x_pitch % 8 == 0 && a.x_off % 8 == 0;
 #define RT3D_ITEMS16(T, M)                                                         \
   return fast ? launch_conv(items16_kernel<T, M, 8, true>, a, stream)              \
               : launch_conv(items16_kernel<T, M, 8, false>, a, stream)

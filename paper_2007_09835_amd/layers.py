@@ -67,9 +67,11 @@ class Conv3d:
 
     def __call__(self, x: torch.Tensor, residual: Optional[torch.Tensor] = None,
                  out: Optional[torch.Tensor] = None, stream=None,
-                 use_workspace: bool = True, c_off: int = 0) -> torch.Tensor:
+                 use_workspace: bool = True, c_off: int = 0, x_off: int = 0) -> torch.Tensor:
         """``out`` may hold more channels than c_out: the layer then writes
-        channels [c_off, c_off + c_out) of it (fused concatenation)."""
+        channels [c_off, c_off + c_out) of it (fused concatenation); ``x``
+        may hold more channels than c_in: the layer reads [x_off, x_off +
+        c_in) of it."""
         n = x.shape[0]
         if out is None:
             out = torch.empty(self.out_shape(n), dtype=TORCH_DTYPES[self.dtype], device=x.device)
@@ -77,6 +79,8 @@ class Conv3d:
         d = self.desc_for(n)
         if out.shape[-1] != self.c_out or c_off:
             d.y_c_total, d.y_c_off = out.shape[-1], c_off
+        if x.shape[-1] != d.c_in or x_off:
+            d.x_c_total, d.x_c_off = x.shape[-1], x_off
         fwd = rt3d.rt3d_kgs_conv3d_fwd if self.sparse else rt3d.rt3d_conv3d_dense_fwd
         fwd(d, self.info, self.blob, x, self.bias, residual, out, ws, stream)
         return out

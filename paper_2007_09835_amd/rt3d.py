@@ -56,7 +56,8 @@ class Conv3dDesc(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in (
         "n", "c_in", "c_out", "t", "h", "w", "kt", "kh", "kw", "st", "sh", "sw",
         "pt", "ph", "pw", "g_m", "g_n", "dtype")] + [("flags", ctypes.c_uint32)] + [
-        (name, ctypes.c_int32) for name in ("qt", "qh", "qw", "y_c_total", "y_c_off")]
+        (name, ctypes.c_int32) for name in ("qt", "qh", "qw", "y_c_total", "y_c_off",
+                                            "x_c_total", "x_c_off")]
 
 
 class PackInfo(ctypes.Structure):
@@ -134,13 +135,14 @@ def _check(status: int):
 
 def make_desc(n, c_in, c_out, thw, k=(3, 3, 3), stride=(1, 1, 1), pad=(1, 1, 1), g=(4, 4),
               dtype="f32", relu=True, residual=False, pool=(1, 1, 1), y_c_total=0,
-              y_c_off=0) -> Conv3dDesc:
+              y_c_off=0, x_c_total=0, x_c_off=0) -> Conv3dDesc:
     """Fill an rt3d_conv3d_desc (``pool``: fused max-pool window = stride;
-    ``y_c_total`` / ``y_c_off``: write into a channel slice of a wider y)."""
+    ``y_c_total`` / ``y_c_off``: write into a channel slice of a wider y;
+    ``x_c_total`` / ``x_c_off``: read a channel slice of a wider x)."""
     flags = (RT3D_RELU if relu else 0) | (RT3D_RESIDUAL if residual else 0)
     code = DTYPE_CODES[dtype] if isinstance(dtype, str) else int(dtype)
     return Conv3dDesc(n, c_in, c_out, *thw, *k, *stride, *pad, g[0], g[1], code, flags, *pool,
-                      y_c_total, y_c_off)
+                      y_c_total, y_c_off, x_c_total, x_c_off)
 
 
 def _host_ptr(a: np.ndarray) -> int:

@@ -157,7 +157,7 @@ class S3DStack:
         shapes = {"x": (l0.t, l0.h, l0.w, l0.c_in)}
         for op in self.ops:
             if op[0] == "conv":
-                _, name, src, dst, c_off = op
+                _, name, src, dst, c_off, _ = op
                 l, conv = by_name[name]
                 c_prev = shapes.get(dst, (0, 0, 0, 0))[3]
                 shapes[dst] = (*conv.out_thw, max(c_prev, c_off + l.c_out))
@@ -186,10 +186,10 @@ class S3DStack:
         calls = []
         for op in self.ops:
             if op[0] == "conv":
-                _, name, src, dst, c_off = op
+                _, name, src, dst, c_off, x_off = op
                 l, conv = self._by_name[name]
-                calls.append((l, lambda conv=conv, i=self.bufs[src], o=self.bufs[dst], c=c_off:
-                              conv(i, None, out=o, c_off=c)))
+                calls.append((l, lambda conv=conv, i=self.bufs[src], o=self.bufs[dst], c=c_off,
+                              xo=x_off: conv(i, None, out=o, c_off=c, x_off=xo)))
         return calls
 
     def forward(self, x: Optional[torch.Tensor] = None) -> torch.Tensor:
@@ -197,9 +197,9 @@ class S3DStack:
             self.x.copy_(x)
         for op in self.ops:
             if op[0] == "conv":
-                _, name, src, dst, c_off = op
+                _, name, src, dst, c_off, x_off = op
                 _, conv = self._by_name[name]
-                conv(self.bufs[src], None, out=self.bufs[dst], c_off=c_off)
+                conv(self.bufs[src], None, out=self.bufs[dst], c_off=c_off, x_off=x_off)
             else:
                 _, src, dst, k, st, pd = op
                 layers.maxpool3d(self.bufs[src], k, st, self.dtype, out=self.bufs[dst], pad=pd)

@@ -176,19 +176,31 @@ def s3d_layers(t: int = 16, hw: int = 224) -> Tuple[List[ConvLayer], list]:
     stem (1x7x7 stride (1,2,2), then 7x1x1 stride (2,1,1)), max-pool 1x3x3
     stride (1,2,2), 1x1x1 and separable 3x3x3 convs, max-pool, then nine
     Inception blocks (mixed 3b-3c, 4b-4f, 5b-5c) separated by 3x3x3 / 2x2x2
-    stride-2 pools.  A block's four branches write channel slices of one
-    output: 1x1x1; 1x1x1 then separable 3x3x3 (1x3x3 then 3x1x1); the same
-    with other widths; 3x3x3 stride-1 max-pool then 1x1x1.  Every conv has a
-    ReLU (batch-norm folded into weights and bias).  Returns (layers, ops)."""
+    stride-2 pools.  A block's branches are 1x1x1; 1x1x1 then separable 3x3x3
+    (1x3x3 then 3x1x1); the same with other widths; 3x3x3 stride-1 max-pool
+    then 1x1x1.  Every conv has a ReLU (batch-norm folded into weights and
+    bias).
+
+    The three 1x1x1 convs that read the block input are one conv (their
+    filters concatenated, written [b1 reduce | b2 reduce | b0] into the block
+    buffer), and every branch writes its slice of that buffer, so a block
+    buffer holds [b1 reduce | b2 reduce | b0 | b1 | b2 | b3] and the next
+    block reads its channels from b0 on.  Returns (layers, ops): an op is
+    ("conv", layer, input buffer, output buffer, output channel offset,
+    input channel offset) or ("pool", input, output, window, stride, pad)."""
     layers: List[ConvLayer] = []
     ops: list = []
-    shapes = {"x": (3, t, hw, hw)}
+    shapes = {"x": (3, t, hw, hw)}   # buffer -> (channels per voxel, t, h, w)
 
-    def conv(name, src, dst, c_out, k, stride=(1, 1, 1), pad=(0, 0, 0), c_off=0, dense=False):
-        c_in, ti, hi, wi = shapes[src]
+    def conv(name, src, dst, c_out, k, stride=(1, 1, 1), pad=(0, 0, 0), c_off=0, dense=False,
+             x_off=0, c_in=None):
+        c_buf, ti, hi, wi = shapes[src]
+        c_in = c_buf - x_off if c_in is None else c_in
         l = ConvLayer(name, c_in, c_out, ti, hi, wi, k, stride, pad, dense=dense)
         layers.append(l)
-        ops.append(("conv", name, src, dst, c_off))
+        ops.append(("conv", name, src, dst, c_off, x_off))
+        c_prev = shapes.get(dst, (0,))[0]
+        shapes[dst] = (max(c_prev, c_off + c_out), *l.out_thw)
         return l.out_thw
 
     def pool(src, dst, k, stride, pad):
@@ -197,26 +209,21 @@ def s3d_layers(t: int = 16, hw: int = 224) -> Tuple[List[ConvLayer], list]:
         ops.append(("pool", src, dst, k, stride, pad))
         shapes[dst] = (c, *out)
 
-    def sep(name, src, dst, c_out, c_off=0, k=3, stride=(1, 1, 1), dense=False):
+    def sep(name, src, dst, c_out, c_off=0, k=3, stride=(1, 1, 1), dense=False, x_off=0,
+            c_in=None):
         pk = k // 2
-        thw = conv(name + "_s", src, name + "_s", c_out, (1, k, k), (1, stride[1], stride[2]),
-                   (0, pk, pk), dense=dense)
-        shapes[name + "_s"] = (c_out, *thw)
-        thw = conv(name + "_t", name + "_s", dst, c_out, (k, 1, 1), (stride[0], 1, 1), (pk, 0, 0),
-                   c_off=c_off)
-        return thw
+        conv(name + "_s", src, name + "_s", c_out, (1, k, k), (1, stride[1], stride[2]),
+             (0, pk, pk), dense=dense, x_off=x_off, c_in=c_in)
+        conv(name + "_t", name + "_s", dst, c_out, (k, 1, 1), (stride[0], 1, 1), (pk, 0, 0),
+             c_off=c_off)
 
-    thw = sep("c1a", "x", "c1a", 64, k=7, stride=(2, 2, 2), dense=True)
-    # only the spatial stem conv (3 input channels) stays dense
-    layers[-1].dense = False
-    shapes["c1a"] = (64, *thw)
+    sep("c1a", "x", "c1a", 64, k=7, stride=(2, 2, 2), dense=True)
+    layers[-1].dense = False  # only the spatial stem conv (3 input channels) stays dense
     pool("c1a", "p2a", (1, 3, 3), (1, 2, 2), (0, 1, 1))
-    thw = conv("c2b", "p2a", "c2b", 64, (1, 1, 1))
-    shapes["c2b"] = (64, *thw)
-    thw = sep("c2c", "c2b", "c2c", 192)
-    shapes["c2c"] = (192, *thw)
+    conv("c2b", "p2a", "c2b", 64, (1, 1, 1))
+    sep("c2c", "c2b", "c2c", 192)
     pool("c2c", "p3a", (1, 3, 3), (1, 2, 2), (0, 1, 1))
-    cur = "p3a"
+    cur, cur_off = "p3a", 0
     for name, c_in, b0, b1r, b1, b2r, b2, b3 in S3D_MIXED:
         if name == "m4b":
             pool(cur, "p4a", (3, 3, 3), (2, 2, 2), (1, 1, 1))
@@ -224,20 +231,14 @@ def s3d_layers(t: int = 16, hw: int = 224) -> Tuple[List[ConvLayer], list]:
         if name == "m5b":
             pool(cur, "p5a", (2, 2, 2), (2, 2, 2), (0, 0, 0))
             cur = "p5a"
-        c, ti, hi, wi = shapes[cur]
-        assert c == c_in, (name, c, c_in)
-        out = name
-        conv(name + "_b0", cur, out, b0, (1, 1, 1), c_off=0)
-        thw = conv(name + "_b1r", cur, name + "_b1r", b1r, (1, 1, 1))
-        shapes[name + "_b1r"] = (b1r, *thw)
-        sep(name + "_b1", name + "_b1r", out, b1, c_off=b0)
-        thw = conv(name + "_b2r", cur, name + "_b2r", b2r, (1, 1, 1))
-        shapes[name + "_b2r"] = (b2r, *thw)
-        sep(name + "_b2", name + "_b2r", out, b2, c_off=b0 + b1)
+        e = b1r + b2r + b0
+        conv(name + "_e", cur, name, e, (1, 1, 1), x_off=cur_off, c_in=c_in)
+        sep(name + "_b1", name, name, b1, c_off=e, x_off=0, c_in=b1r)
+        sep(name + "_b2", name, name, b2, c_off=e + b1, x_off=b1r, c_in=b2r)
         pool(cur, name + "_p", (3, 3, 3), (1, 1, 1), (1, 1, 1))
-        conv(name + "_b3", name + "_p", out, b3, (1, 1, 1), c_off=b0 + b1 + b2)
-        shapes[out] = (b0 + b1 + b2 + b3, ti, hi, wi)
-        cur = out
+        conv(name + "_b3", name + "_p", name, b3, (1, 1, 1), c_off=e + b1 + b2, x_off=cur_off,
+             c_in=c_in)
+        cur, cur_off = name, b1r + b2r
     return layers, ops
 
 

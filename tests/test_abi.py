@@ -216,6 +216,13 @@ def test_error_paths():
     _expect_status(rt3d.RT3D_ERR_UNSUPPORTED, rt3d.rt3d_conv3d_out_shape, cat)
     cat = rt3d.make_desc(1, 8, 8, (4, 4, 4), dtype="f32", y_c_total=16, y_c_off=8)
     assert rt3d.rt3d_conv3d_out_shape(cat) == (4, 4, 4)
+    # input channel slice: must fit; network-input layers (c_in <= 4) read whole voxels
+    sl = rt3d.make_desc(1, 8, 8, (4, 4, 4), dtype="f32", x_c_total=12, x_c_off=6)
+    _expect_status(rt3d.RT3D_ERR_INVALID_ARG, rt3d.rt3d_conv3d_out_shape, sl)
+    sl = rt3d.make_desc(1, 3, 8, (4, 4, 4), dtype="bf16", x_c_total=8, x_c_off=0)
+    _expect_status(rt3d.RT3D_ERR_UNSUPPORTED, rt3d.rt3d_conv3d_out_shape, sl)
+    sl = rt3d.make_desc(1, 8, 8, (4, 4, 4), dtype="f32", x_c_total=20, x_c_off=12)
+    assert rt3d.rt3d_conv3d_out_shape(sl) == (4, 4, 4)
     assert lib.rt3d_status_string(99)
     assert lib.rt3d_status_string(rt3d.RT3D_ERR_HIP) == b"HIP runtime error"
 

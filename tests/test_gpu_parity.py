@@ -383,8 +383,9 @@ def _s3d_oracle_op(op, stack, src64, layer_by_name):
     if op[0] == "pool":
         _, _, _, k, st, pd = op
         return oracle.maxpool3d(src64, k, st, pd)
-    _, name, _, _, _ = op
+    _, name, _, _, _, x_off = op
     i, l = layer_by_name[name]
+    src64 = src64[:, x_off:x_off + l.c_in]
     d = synth.layer_params("s3d", l)
     w64 = synth.to_dtype(d.w, stack.dtype).double().numpy()
     b64 = d.bias.astype(np.float32).astype(np.float64)
