@@ -38,6 +38,8 @@ def parse():
     p.add_argument("--mode", default="kgs", choices=["kgs", "vanilla"])
     p.add_argument("--group", default="4x4", help="kernel group size g_MxG_N of the masks")
     p.add_argument("--no-graph", action="store_true", help="launch eagerly instead of a HIP graph")
+    p.add_argument("--streams", type=int, default=4,
+                   help="S3D: streams for independent Inception branches (1 = in order)")
     p.add_argument("--separate-pool", action="store_true",
                    help="run max-pools as their own kernels instead of in the conv epilogue")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -551,8 +553,9 @@ def main():
     log("building stacks ...")
     fuse = not args.separate_pool
     sparse = make_stack(args.net, args.batch, args.dtype, args.mode, args.rate, fuse_pool=fuse,
-                        group=group_of(args))
-    dense = make_stack(args.net, args.batch, args.dtype, "dense", args.rate, fuse_pool=fuse)
+                        group=group_of(args), streams=args.streams)
+    dense = make_stack(args.net, args.batch, args.dtype, "dense", args.rate, fuse_pool=fuse,
+                       streams=args.streams)
     l0 = sparse.layers[0]
     clip_thw = (l0.t, l0.h, l0.w)
     clip = synth.clip_input("bench-clip", args.batch, "uniform01", l0.c_in, l0.t, l0.h, l0.w)

@@ -132,8 +132,9 @@ class S3DStack:
 
     def __init__(self, batch: int = 1, dtype: str = "bf16", mode: str = "kgs",
                  rate: float = 2.1, tag: str = "s3d", device: str = "cuda", group=(4, 4),
-                 clip=(16, 224)):
-        """``clip`` = (frames, height = width) of the input."""
+                 clip=(16, 224), n_streams: int = 4):
+        """``clip`` = (frames, height = width) of the input; ``n_streams``
+        streams run independent ops concurrently (1 = strictly in order)."""
         self.batch, self.dtype, self.mode, self.rate = batch, dtype, mode, rate
         self.group = tuple(group)
         self.layers, self.ops = synth.s3d_stack(rate if mode == "kgs" else 2.1, tag=tag,
@@ -173,6 +174,46 @@ class S3DStack:
                 self.bufs[name] = torch.empty((batch, *shp), dtype=tdt, device=device)
         self.pool_bufs: Dict[str, torch.Tensor] = {}
         self.out_name = self.ops[-1][3]
+        self._schedule(n_streams)
+
+    def _schedule(self, n_streams: int):
+        """Dependencies between ops by the channel ranges they read and
+        write (branches of a block write disjoint slices of one buffer), and a
+        stream per op: an op continues the stream of a dependency that stream
+        ended with, else takes the least recently used stream.  The branches
+        of a block then run concurrently."""
+        def ranges(op):
+            if op[0] == "conv":
+                _, name, src, dst, c_off, x_off = op
+                l, _ = self._by_name[name]
+                return [(src, x_off, x_off + l.c_in)], [(dst, c_off, c_off + l.c_out)]
+            _, src, dst, *_ = op
+            c = self.bufs[src].shape[-1]
+            return [(src, 0, c)], [(dst, 0, c)]
+        writers: Dict[str, list] = {}   # buffer -> [(c0, c1, op index)]
+        self.deps: List[List[int]] = []
+        for i, op in enumerate(self.ops):
+            reads, writes = ranges(op)
+            d = set()
+            for buf, c0, c1 in reads:
+                for w0, w1, j in writers.get(buf, []):
+                    if w0 < c1 and c0 < w1:
+                        d.add(j)
+            for buf, c0, c1 in writes:
+                writers.setdefault(buf, []).append((c0, c1, i))
+            self.deps.append(sorted(d))
+        self.stream_of: List[int] = []
+        last = [-1] * max(1, n_streams)      # last op issued on each stream
+        used = [0] * len(last)
+        for i, d in enumerate(self.deps):
+            pick = next((s for s in range(len(last)) if last[s] in d), None)
+            if pick is None:
+                pick = min(range(len(last)), key=lambda s: used[s])
+            self.stream_of.append(pick)
+            last[pick] = i
+            used[pick] = i + 1
+        self.streams = [None] + [torch.cuda.Stream() for _ in range(len(last) - 1)]
+        self.events = [torch.cuda.Event() for _ in self.ops]
 
     def kept_rate(self) -> float:
         if self.mode == "dense":
@@ -193,22 +234,37 @@ class S3DStack:
         return calls
 
     def forward(self, x: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """One pass.  Ops run on the current stream and up to n_streams - 1
+        side streams, forked from it and joined back at the end (so the pass
+        can be captured in one HIP graph)."""
         if x is not None:
             self.x.copy_(x)
-        for op in self.ops:
+        main = torch.cuda.current_stream()
+        streams = [main] + self.streams[1:]
+        for st in streams[1:]:
+            st.wait_stream(main)
+        for i, op in enumerate(self.ops):
+            st = streams[self.stream_of[i]]
+            for j in self.deps[i]:
+                if self.stream_of[j] != self.stream_of[i]:
+                    st.wait_event(self.events[j])
             if op[0] == "conv":
                 _, name, src, dst, c_off, x_off = op
                 _, conv = self._by_name[name]
-                conv(self.bufs[src], None, out=self.bufs[dst], c_off=c_off, x_off=x_off)
+                conv(self.bufs[src], None, out=self.bufs[dst], c_off=c_off, x_off=x_off, stream=st)
             else:
-                _, src, dst, k, st, pd = op
-                layers.maxpool3d(self.bufs[src], k, st, self.dtype, out=self.bufs[dst], pad=pd)
+                _, src, dst, k, stv, pd = op
+                layers.maxpool3d(self.bufs[src], k, stv, self.dtype, out=self.bufs[dst], pad=pd,
+                                 stream=st)
+            self.events[i].record(st)
+        for st in streams[1:]:
+            main.wait_stream(st)
         return self.bufs[self.out_name]
 
 
 def make_stack(net: str, batch: int = 1, dtype: str = "bf16", mode: str = "kgs",
-               rate: float = 3.0, fuse_pool: bool = True, group=(4, 4)):
-    """The named stack (c3d, r2plus1d or s3d)."""
+               rate: float = 3.0, fuse_pool: bool = True, group=(4, 4), streams: int = 4):
+    """The named stack (c3d, r2plus1d or s3d; ``streams`` applies to s3d)."""
     if net == "s3d":
-        return S3DStack(batch, dtype, mode, rate, group=group)
+        return S3DStack(batch, dtype, mode, rate, group=group, n_streams=streams)
     return Stack(net, batch, dtype, mode, rate, fuse_pool=fuse_pool, group=group)
