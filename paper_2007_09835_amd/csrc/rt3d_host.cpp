@@ -154,7 +154,7 @@ constexpr int kMaxHalo = 96 * 1024;    // LDS bytes for the staged brick
 
 // Choose the output brick: fewest launched voxel slots (least waste at the
 // volume's edges), then the smallest halo (least staging traffic).
-Tiling choose_tiling(const Geom &g) {
+Tiling choose_tiling(const Geom &g, int slots = kSlots) {
   Tiling best{};
   long best_cost = -1, best_halo = 0;
   // Channels per LDS chunk: 32 (16-bit) or 16 (fp32), narrower when the
@@ -170,10 +170,10 @@ Tiling choose_tiling(const Geom &g) {
   if ((row / 16) % 2 == 0) row += 16;
   // Bricks hold whole pooling windows (their origins are then multiples of
   // the window too), so the fused pooling never crosses workgroups.
-  for (int bw = g.qw; bw <= std::max(g.qw, std::min(g.wo, kSlots)); bw += g.qw)
-    for (int bh = g.qh; bh <= std::max(g.qh, std::min(g.ho, kSlots / bw)); bh += g.qh)
-      for (int bt = g.qt; bt <= std::max(g.qt, std::min(g.to, kSlots / (bw * bh))); bt += g.qt) {
-        if (bt * bh * bw > kSlots) continue;
+  for (int bw = g.qw; bw <= std::max(g.qw, std::min(g.wo, slots)); bw += g.qw)
+    for (int bh = g.qh; bh <= std::max(g.qh, std::min(g.ho, slots / bw)); bh += g.qh)
+      for (int bt = g.qt; bt <= std::max(g.qt, std::min(g.to, slots / (bw * bh))); bt += g.qt) {
+        if (bt * bh * bw > slots) continue;
         const int ht = (bt - 1) * g.st + g.kt;
         const int hh = (bh - 1) * g.sh + g.kh;
         const int hw = (bw - 1) * g.sw + g.kw;
@@ -186,7 +186,7 @@ Tiling choose_tiling(const Geom &g) {
         // for the 16-byte fp32 reads).
         const int modulus = g.es == 2 ? 16 : 8;
         int conflict = 1;
-        for (int f = 0; f < kSlots / 16; ++f) {
+        for (int f = 0; f < slots / 16; ++f) {
           int hits[16] = {0};
           for (int n = 0; n < 16; ++n) {
             const int sl = 16 * f + n;
@@ -196,11 +196,11 @@ Tiling choose_tiling(const Geom &g) {
             conflict = std::max(conflict, ++hits[v % modulus]);
           }
         }
-        const long cost = nb * kSlots * (3 + conflict);
+        const long cost = nb * slots * (3 + conflict);
         if (best_cost < 0 || cost < best_cost || (cost == best_cost && halo < best_halo)) {
           best_cost = cost;
           best_halo = halo;
-          best = Tiling{bt, bh, bw, ht, hh, hw, cc, row, kSlots, (g.c_in + cc - 1) / cc};
+          best = Tiling{bt, bh, bw, ht, hh, hw, cc, row, slots, (g.c_in + cc - 1) / cc};
         }
       }
   // 16-bit layers with a small halo (few kernel taps) take wider channel
@@ -279,15 +279,11 @@ rt3d_status canon_index(const rt3d_conv3d_desc *d, const uint8_t *mask, Canon &c
   return ok();
 }
 
-// Small-input-channel path (kVarSmall*16): 16-bit, c_in <= 4 (one channel
-// block), kernels up to 3x3x3 with stride 1 (at most 4 K-steps of 8 items and
-// 12 halo lines of <= 192 elements per brick, the kernel's register budget),
-// and no pooling or the 1x2x2 window (pooled in registers).  Disable with
-// RT3D_SMALL_KERNEL=0.
-// The small-channel kernel: c_in <= 4 (one 4-channel block per tap), a
-// halo of at most 12 lines (kt * (sh + kh)) of at most 256 elements
-// ((31 sw + kw) * c_in), at most 64 taps (8 K-steps of 8), and pooling that
-// is either absent or 1x2x2 (the brick's two rows and adjacent lanes).
+// Small-input-channel path (kVarSmall*16): 16-bit, c_in <= 4 (one 4-channel
+// block per tap), a halo of at most 12 lines (kt * (sh + kh)) of at most 256
+// elements ((31 sw + kw) * c_in), at most 64 taps (8 K-steps of 8), and
+// pooling that is either absent or 1x2x2 (the brick's two rows and adjacent
+// lanes).  Disable with RT3D_SMALL_KERNEL=0.
 bool small_ok(const Geom &g) {
   if (const char *env = std::getenv("RT3D_SMALL_KERNEL"))
     if (std::atoi(env) == 0) return false;
@@ -312,6 +308,28 @@ Tiling small_tiling(const Geom &g) {
   t.slots = 64;
   t.nchunks = 1;
   return t;
+}
+
+// Voxel slots per workgroup of the 16-bit item kernels: 128 (8 fragments of
+// 16 per wave) or 64 (4 fragments).  Wide bricks reuse each weight fragment
+// over more voxels and stage less halo per output; narrow bricks double the
+// workgroups, which pays when 128-slot bricks times 16-filter tiles give
+// fewer waves than the GPU has SIMDs (the layer would otherwise need deep
+// channel splits and their reduction pass).  Measured on MI355X over the
+// C3D and R(2+1)D layers at batch 1.  Benchmark switch: RT3D_SLOTS=64|128.
+int brick_slots(const Geom &g) {
+  if (g.es != 2) return kSlots;
+  if (const char *env = std::getenv("RT3D_SLOTS")) {
+    const int v = std::atoi(env);
+    if (v == 64 || v == 128) return v;
+  }
+  const long voxels = static_cast<long>(std::max(g.n, 1)) * g.to * g.ho * g.wo;
+  const long waves = (voxels + kSlots - 1) / kSlots * ((g.c_out + 15) / 16);
+  return waves < 1024 ? 64 : kSlots;
+}
+
+Tiling layer_tiling(const Geom &g) {
+  return small_ok(g) ? small_tiling(g) : choose_tiling(g, brick_slots(g));
 }
 
 // mask of the 4x4 kernel block (p4, q4) at position pos (groups of 8 or 16
@@ -737,7 +755,7 @@ rt3d_status plan_kgs(const rt3d_conv3d_desc *d, const uint8_t *mask, const uint8
   }
   const Geom g = geom_of(d);
   const bool small = small_ok(g);
-  tl = small ? small_tiling(g) : choose_tiling(g);
+  tl = layer_tiling(g);
   if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
   Mask4 m4{mask, c.Q, ks, d->g_m / 4, d->g_n / 4};
   static const uint8_t zero = 0;
@@ -847,7 +865,7 @@ Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint32_t variant, u
   // with constants fitted to per-wave timestamps and per-layer traces of the
   // C3D and R(2+1)D layers on MI355X.
   const size_t halo = static_cast<size_t>(tl.ht) * tl.hh * tl.hw * tl.row;
-  int per_cu = conv_resident(static_cast<int>(variant), d->dtype, p.mfw, halo);
+  int per_cu = conv_resident(static_cast<int>(variant), d->dtype, p.mfw, tl.slots / 16, halo);
   if (per_cu <= 0) {
     (void)hipGetLastError();
     per_cu = 2;
@@ -922,6 +940,7 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   a.y_off = d->y_c_off;
   a.x_pitch = d->x_c_total != 0 ? d->x_c_total : d->c_in;
   a.x_off = d->x_c_off;
+  a.nf = tl.slots / 16;
   a.res = residual;
   a.bias = bias;
   a.step_ptr = reinterpret_cast<const uint32_t *>(b + p.step_ptr_off);
@@ -1193,7 +1212,7 @@ rt3d_status rt3d_dense_pack_size(const rt3d_conv3d_desc *d, uint64_t *bytes) {
   if (!bytes) return fail(RT3D_ERR_INVALID_ARG, "bytes must be non-NULL");
   const Geom g = geom_of(d);
   const bool small = small_ok(g);
-  const Tiling tl = small ? small_tiling(g) : choose_tiling(g);
+  const Tiling tl = layer_tiling(g);
   if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
   std::vector<uint8_t> scratch(static_cast<size_t>(g.c_out) * g.c_in * g.ks * g.es, 0);
   Layout L;
@@ -1210,7 +1229,7 @@ rt3d_status rt3d_dense_pack(const rt3d_conv3d_desc *d, const void *w_dense, void
     return fail(RT3D_ERR_INVALID_ARG, "w_dense, blob and info must be non-NULL");
   const Geom g = geom_of(d);
   const bool small = small_ok(g);
-  const Tiling tl = small ? small_tiling(g) : choose_tiling(g);
+  const Tiling tl = layer_tiling(g);
   if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
   Layout L;
   build_items_layout(g, tl, static_cast<const uint8_t *>(w_dense), nullptr, L, small);

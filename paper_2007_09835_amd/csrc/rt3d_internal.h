@@ -85,7 +85,7 @@ struct ConvArgs {
   int32_t steps_max;  // most K-steps of one wave tile (the plan's tile_steps)
   int32_t x_pitch;    // channels per voxel of x (>= c_in: a slice of a wider tensor)
   int32_t x_off;      // first channel of x this layer reads
-  int32_t pad2;
+  int32_t nf;         // 16-slot voxel fragments per wave (slots / 16)
 };
 
 // Launch shape chosen at forward time from the batch size.
@@ -116,9 +116,9 @@ struct GroupArgs {
 };
 
 // Kernel launchers (rt3d_kernels.hip).  Return hipSuccess or the launch error.
-// Workgroups of the conv kernel for (variant, dtype, mfw) that fit on one CU
+// Workgroups of the conv kernel for (variant, dtype, mfw, nf) that fit on one CU
 // with `lds` bytes of dynamic LDS each; 0 when the runtime cannot say.
-int conv_resident(int variant, int dtype, int mfw, size_t lds);
+int conv_resident(int variant, int dtype, int mfw, int nf, size_t lds);
 int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream);
 int launch_small16(const ConvArgs &a, int dtype, int mfw, void *stream);
 size_t small_lds_bytes(const ConvArgs &a);

@@ -1544,7 +1544,7 @@ __global__ __launch_bounds__(256) void reg_finalize_kernel(const float *partial,
 size_t halo_bytes(const ConvArgs &a) {
   const size_t halo = static_cast<size_t>(a.ht) * a.hh * a.hw * a.row;
   if (a.splits > 1) return halo;  // partials are stored from registers
-  const size_t tile = static_cast<size_t>(128) * a.tile_row;  // epilogue tile: 128 voxel slots
+  const size_t tile = static_cast<size_t>(16 * a.nf) * a.tile_row;  // epilogue tile: the slots
   return halo > tile ? halo : tile;
 }
 
@@ -1584,19 +1584,25 @@ int resident(K kernel, size_t lds) {
 
 }  // namespace
 
-int conv_resident(int variant, int dtype, int mfw, size_t lds) {
+int conv_resident(int variant, int dtype, int mfw, int nf, size_t lds) {
   switch (variant) {
     case kVarDenseItems16:
     case kVarKgsUnion16:
-      if (dtype == RT3D_BF16) {
-        if (mfw == 1) return resident(items16_kernel<__bf16, 1, 8, true>, lds);
-        if (mfw == 2) return resident(items16_kernel<__bf16, 2, 8, true>, lds);
-        if (mfw == 4) return resident(items16_kernel<__bf16, 4, 8, true>, lds);
-      } else {
-        if (mfw == 1) return resident(items16_kernel<_Float16, 1, 8, true>, lds);
-        if (mfw == 2) return resident(items16_kernel<_Float16, 2, 8, true>, lds);
-        if (mfw == 4) return resident(items16_kernel<_Float16, 4, 8, true>, lds);
-      }
+#define RT3D_RES16(T)                                                                  \
+  do {                                                                                 \
+    if (nf == 4) {                                                                     \
+      if (mfw == 1) return resident(items16_kernel<T, 1, 4, true>, lds);               \
+      if (mfw == 2) return resident(items16_kernel<T, 2, 4, true>, lds);               \
+      if (mfw == 4) return resident(items16_kernel<T, 4, 4, true>, lds);               \
+    } else {                                                                           \
+      if (mfw == 1) return resident(items16_kernel<T, 1, 8, true>, lds);               \
+      if (mfw == 2) return resident(items16_kernel<T, 2, 8, true>, lds);               \
+      if (mfw == 4) return resident(items16_kernel<T, 4, 8, true>, lds);               \
+    }                                                                                  \
+  } while (0)
+      if (dtype == RT3D_BF16) RT3D_RES16(__bf16);
+      else RT3D_RES16(_Float16);
+#undef RT3D_RES16
       return 0;
     case kVarDenseItemsF32:
       if (mfw == 1) return resident(items_f32_kernel<1, 8>, lds);
@@ -1669,8 +1675,14 @@ int small_resident(const ConvArgs &a, int dtype, int mfw) {
 int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream) {
   const bool fast = a.c_in % 8 == 0 && a.x_pitch % 8 == 0 && a.x_off % 8 == 0;
 #define RT3D_ITEMS16(T, M)                                                         \
-  return fast ? launch_conv(items16_kernel<T, M, 8, true>, a, stream)              \
-              : launch_conv(items16_kernel<T, M, 8, false>, a, stream)
+  do {                                                                             \
+    if (a.nf == 4)                                                                 \
+      return fast ? launch_conv(items16_kernel<T, M, 4, true>, a, stream)          \
+                  : launch_conv(items16_kernel<T, M, 4, false>, a, stream);        \
+    return fast ? launch_conv(items16_kernel<T, M, 8, true>, a, stream)            \
+                : launch_conv(items16_kernel<T, M, 8, false>, a, stream);          \
+  } while (0)
+  if (a.nf != 4 && a.nf != 8) return hipErrorInvalidValue;
   if (dtype == RT3D_BF16) {
     if (mfw == 1) RT3D_ITEMS16(__bf16, 1);
     if (mfw == 2) RT3D_ITEMS16(__bf16, 2);
