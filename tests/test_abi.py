@@ -141,6 +141,35 @@ def test_dense_pack_sizes_and_info():
     assert rt3d.rt3d_conv3d_workspace_size(desc, info) == 0
 
 
+def _brick_slots(desc):
+    """Voxel slots per workgroup of the layer's plan (Tiling.slots: the
+    ninth int32 of the plan)."""
+    w = _weights(np.random.default_rng(1), (desc.c_out, desc.c_in, desc.kt, desc.kh, desc.kw),
+                 {0: "f32", 1: "bf16", 2: "f16"}[desc.dtype])
+    _, info = rt3d.rt3d_dense_pack(desc, w)
+    return int(np.frombuffer(bytes(info.plan), dtype=np.int32)[8])
+
+
+def test_brick_width_follows_the_layer_size(monkeypatch):
+    """16-bit layers whose 128-slot bricks times 16-filter tiles give fewer
+    than 1024 waves (one per SIMD of the GPU) get 64-slot bricks; larger
+    layers and fp32 keep 128; RT3D_SLOTS overrides the choice at pack time."""
+    monkeypatch.delenv("RT3D_SLOTS", raising=False)
+    big = rt3d.make_desc(1, 64, 128, (16, 56, 56), dtype="bf16")        # 392 bricks x 8 tiles
+    small = rt3d.make_desc(1, 256, 256, (8, 28, 28), dtype="bf16")      # 49 x 16 = 784 waves
+    edge = rt3d.make_desc(1, 64, 64, (16, 56, 56), dtype="f16")         # 392 x 4 = 1568 waves
+    f32 = rt3d.make_desc(1, 256, 256, (8, 28, 28), dtype="f32")
+    assert _brick_slots(big) == 128
+    assert _brick_slots(small) == 64
+    assert _brick_slots(edge) == 128
+    assert _brick_slots(f32) == 128
+    monkeypatch.setenv("RT3D_SLOTS", "128")
+    assert _brick_slots(small) == 128
+    monkeypatch.setenv("RT3D_SLOTS", "64")
+    assert _brick_slots(big) == 64
+    assert _brick_slots(f32) == 128
+
+
 def _expect_status(status, fn, *args):
     with pytest.raises(rt3d.Rt3dError) as ei:
         fn(*args)
