@@ -433,6 +433,18 @@ __device__ __forceinline__ float4 add4(float4 x, float4 y) {
   return make_float4(x.x + y.x, x.y + y.y, x.z + y.z, x.w + y.w);
 }
 
+// v of lane l ^ 1: a quad permutation (1, 0, 3, 2) on the DPP path, without
+// the LDS round trip of a general shuffle.  Lanes l and l ^ 1 must be both
+// active.
+__device__ __forceinline__ float swap_pair(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ float4 swap_pairs4(float4 v) {
+  return make_float4(swap_pair(v.x), swap_pair(v.y), swap_pair(v.z), swap_pair(v.w));
+}
+
 __device__ __forceinline__ float4 shfl_xor4(float4 v, int m) {
   return make_float4(__shfl_xor(v.x, m), __shfl_xor(v.y, m), __shfl_xor(v.z, m),
                      __shfl_xor(v.w, m));
@@ -905,7 +917,7 @@ __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
 #pragma unroll
         for (int jw = 0; jw < 2; ++jw) {
           float4 m = max4(v[jw], v[jw + 2]);
-          m = max4(m, shfl_xor4(m, 1));
+          m = max4(m, swap_pairs4(m));  // lanes n, n ^ 1 share g: both active
           const int ow = b.ow0 + 16 * jw + n;
           const int ph = b.oh0 >> 1, pw = ow >> 1;
           if ((n & 1) == 0 && b.ot0 < a.pto && ph < a.pho && pw < a.pwo)
