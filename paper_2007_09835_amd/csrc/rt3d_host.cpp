@@ -490,6 +490,32 @@ void pair_items(std::vector<Item> &its, const Geom &g, const Tiling &tl, PassCos
   }
 }
 
+// KGS wave-tile width for the 16-bit item kernel: 1 (16 filters walk the
+// union of their four 4x4 blocks' items) or 4 (64 filters walk the union of
+// sixteen blocks, each B fragment feeding four MFMAs, as in the dense
+// kernel).  The wide union executes more zero-weight items but costs about
+// 1/1.4 as much per item (measured over the C3D layers at batch 32: the
+// narrow union runs at ~1.4x the dense kernel's time per executed item), so
+// it wins when the narrow union already covers most items.  It is only
+// considered where the dense kernel itself runs 64-filter tiles (256 filters
+// or more) and the layer gives every SIMD a 64-filter wave without channel
+// splits (at batch 1 the narrow tiles' extra waves matter more).
+int kgs_tile_width(const Geom &g, const Tiling &tl, const Mask4 *m4) {
+  if (g.es != 2 || !m4 || g.c_out < 256) return 1;
+  const long voxels = static_cast<long>(std::max(g.n, 1)) * g.to * g.ho * g.wo;
+  const long bricks = (voxels + tl.slots - 1) / tl.slots;
+  if (bricks * ((g.c_out + 63) / 64) < 1024) return 1;
+  double narrow = 0, wide = 0;
+  const int p4_count = (g.c_out + 3) / 4;
+  for (int ch = 0; ch < tl.nchunks; ++ch) {
+    for (int p4 = 0; p4 < p4_count; p4 += 4)
+      narrow += static_cast<double>(chunk_items(g, m4, tl.cc, ch, p4, 4).size());
+    for (int p4 = 0; p4 < p4_count; p4 += 16)
+      wide += 4.0 * static_cast<double>(chunk_items(g, m4, tl.cc, ch, p4, 16).size());
+  }
+  return wide < 1.4 * narrow ? 4 : 1;
+}
+
 // 16-bit MFMA item layout (variants kVarDenseItems16, kVarKgsUnion16) and
 // the f32 16x16x4 dense layout (kVarDenseItemsF32).
 void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const Mask4 *m4,
@@ -516,9 +542,12 @@ void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
       const int v = std::atoi(env);
       if (v == 1 || v == 2 || v == 4) mfw = v;
     }
-  } else if (const char *env = std::getenv("RT3D_KGS_MFW")) {
-    const int v = std::atoi(env);
-    if (v == 1 || v == 2 || v == 4) mfw = v;
+  } else if (!small) {
+    mfw = kgs_tile_width(g, tl, m4);
+    if (const char *env = std::getenv("RT3D_KGS_MFW")) {
+      const int v = std::atoi(env);
+      if (v == 1 || v == 2 || v == 4) mfw = v;
+    }
   }
   if (small) {
     // Up to 32 filters per wave: wider tiles hold 4x the weights in

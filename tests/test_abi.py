@@ -170,6 +170,30 @@ def test_brick_width_follows_the_layer_size(monkeypatch):
     assert _brick_slots(f32) == 128
 
 
+def test_kgs_tile_width_follows_union_size(monkeypatch):
+    """KGS layers with 256+ filters and a 64-filter wave per SIMD walk the
+    union of 16 kernel groups (64-filter tiles) when the 16-filter union
+    already covers most items; sparser masks and batch-1 layers keep
+    16-filter tiles.  Plan fields: mfw is the eleventh int32."""
+    monkeypatch.delenv("RT3D_KGS_MFW", raising=False)
+    monkeypatch.delenv("RT3D_SLOTS", raising=False)
+    rng = np.random.default_rng(3)
+    w = _weights(rng, (256, 256, 3, 3, 3), "bf16")
+
+    def mfw(n, keep):
+        desc = rt3d.make_desc(n, 256, 256, (8, 28, 28), dtype="bf16")
+        mask = np.zeros((64, 64, 27), np.uint8)
+        for p in range(64):
+            for q in range(64):
+                mask[p, q, rng.choice(27, keep, replace=False)] = 1
+        _, info = rt3d.rt3d_kgs_pack(desc, w, mask)
+        return int(np.frombuffer(bytes(info.plan), dtype=np.int32)[10])
+
+    assert mfw(32, 13) == 4   # 16-filter union ~93% of items: the wide union is cheaper
+    assert mfw(32, 5) == 1    # ~56%: the narrow union is cheaper
+    assert mfw(1, 13) == 1    # batch 1: too few 64-filter waves
+
+
 def _expect_status(status, fn, *args):
     with pytest.raises(rt3d.Rt3dError) as ei:
         fn(*args)
