@@ -71,6 +71,9 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+SPIN_CYCLES = 400000   # ~0.2 ms of GPU spin, longer than the host's enqueue of one launch
+
+
 def time_region(torch, fn, steps, stream):
     """Run fn() `steps` times between two events on `stream`; ms per call."""
     torch.cuda.synchronize()
@@ -84,12 +87,29 @@ def time_region(torch, fn, steps, stream):
     return e0.elapsed_time(e1) / steps
 
 
+def graph_of(torch, fn, reps):
+    """A HIP graph holding `reps` back-to-back calls of fn (captured on the
+    current stream after one eager call, which allocates any workspace)."""
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(reps):
+            fn()
+    g.replay()
+    torch.cuda.synchronize()
+    return g
+
+
 def per_layer_ms(torch, stack, reps, stream):
-    """Average duration of each layer's conv kernel, launched back to back."""
+    """Average duration of each layer's conv launch (kernel and split
+    reduction), from graph replays of `reps` back-to-back launches: the
+    host's per-call cost stays out of the measurement."""
     out = []
     for _, fn in stack.layer_calls():
-        fn()
-        out.append(time_region(torch, fn, reps, stream))
+        g = graph_of(torch, fn, reps)
+        out.append(time_region(torch, g.replay, 5, stream) / reps)
+        del g
     return out
 
 
@@ -212,13 +232,16 @@ def pct(xs, q):
 def latency(torch, fn, iters, stream, flush=None):
     """Per-launch latency (ms) over `iters` launches, each bracketed by its
     own events; with `flush`, 1 GiB is written before every launch (outside
-    the events) so L2 and the 256 MB MALL start cold."""
+    the events) so L2 and the 256 MB MALL start cold.  A spin kernel queued
+    ahead of the first event keeps the GPU busy while the host enqueues the
+    launch, so the interval holds GPU time only."""
     times = []
     fn()
     torch.cuda.synchronize()
     for _ in range(iters):
         if flush is not None:
             flush()
+        torch.cuda._sleep(SPIN_CYCLES)
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)
