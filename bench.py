@@ -49,6 +49,8 @@ def parse():
     p.add_argument("--report", default=None, help="write per-layer results to this JSON file")
     p.add_argument("--profile-layer", default=None,
                    help="only launch this layer's sparse conv --layer-reps times (for rocprofv3)")
+    p.add_argument("--layer-graph", action="store_true",
+                   help="--profile-layer: launch from a HIP graph of --layer-reps launches")
     p.add_argument("--profile-reweight", default=None, metavar="LAYER",
                    help="launch only the reweight pass over this C3D layer's weights "
                         "(bf16, all outputs) --layer-reps times, for rocprofv3")
@@ -154,7 +156,12 @@ def profile_layer(args, torch, stream):
                torch.empty(conv.out_shape(args.batch), dtype=sparse.x.dtype, device="cuda"))
     fn = lambda: conv(inp, res, out=out_buf)
     fn()
-    ms = time_region(torch, fn, args.layer_reps, stream)
+    if args.layer_graph:
+        # as the stack measurement launches it: back to back inside a HIP graph
+        g = graph_of(torch, fn, args.layer_reps)
+        ms = time_region(torch, g.replay, 1, stream) / args.layer_reps
+    else:
+        ms = time_region(torch, fn, args.layer_reps, stream)
     info = conv.info
     kept = (args.batch * l.voxels_out * info.kept_weights if conv.sparse
             else l.dense_macs(args.batch))
