@@ -38,6 +38,8 @@ def parse():
     p.add_argument("--mode", default="kgs", choices=["kgs", "vanilla"])
     p.add_argument("--group", default="4x4", help="kernel group size g_MxG_N of the masks")
     p.add_argument("--no-graph", action="store_true", help="launch eagerly instead of a HIP graph")
+    p.add_argument("--clock-warmup", type=float, default=0.5, metavar="SECONDS",
+                   help="keep the GPU busy this long before the warmup steps (clock ramp-up)")
     p.add_argument("--streams", type=int, default=4,
                    help="S3D: streams for independent Inception branches (1 = in order)")
     p.add_argument("--separate-pool", action="store_true",
@@ -144,18 +146,27 @@ def measured_traffic(layer):
 def profile_layer(args, torch, stream):
     """Launch one layer of the sparse stack back to back (and optionally a
     plain copy of known size) so rocprofv3 sees only these kernels."""
+    from paper_2007_09835_amd import synth
     from paper_2007_09835_amd.stack import make_stack
     sparse = make_stack(args.net, args.batch, args.dtype, args.mode, args.rate,
                         fuse_pool=not args.separate_pool, group=group_of(args))
     idx = [l.name for l in sparse.layers].index(args.profile_layer)
     l, conv = sparse.layers[idx], sparse.convs[idx]
-    inp = torch.randn(conv.desc_for(args.batch).n, l.t, l.h, l.w, l.c_in, device="cuda").abs()
-    inp = inp.to(sparse.x.dtype)
-    res = torch.zeros_like(sparse.bufs[l.name]) if l.residual_from else None
-    out_buf = (sparse.bufs[l.name] if l.name in sparse.bufs else
-               torch.empty(conv.out_shape(args.batch), dtype=sparse.x.dtype, device="cuda"))
-    fn = lambda: conv(inp, res, out=out_buf)
+    # The layer's own input in a pass over the benchmark clip (the stack
+    # measurement's data: MFMA power, and so the clock, depend on the values).
+    l0 = sparse.layers[0]
+    sparse.x.copy_(synth.to_dtype(synth.clip_input("bench-clip", args.batch, "uniform01", l0.c_in,
+                                                   l0.t, l0.h, l0.w), args.dtype)
+                   .permute(0, 2, 3, 4, 1).contiguous().cuda())
+    sparse.forward()
+    fn = dict((c[0].name, c[1]) for c in sparse.layer_calls())[l.name]
     fn()
+    # Keep the GPU busy for --clock-warmup seconds first: the clocks ramp up
+    # under load, and the stack measurement runs after the same warm-up.
+    t_end = time.perf_counter() + args.clock_warmup
+    while time.perf_counter() < t_end:
+        sparse.forward()
+        torch.cuda.synchronize()
     if args.layer_graph:
         # as the stack measurement launches it: back to back inside a HIP graph
         g = graph_of(torch, fn, args.layer_reps)
@@ -360,6 +371,10 @@ def suite(args, torch, stream):
 
     scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")   # 1 GiB
     flush = lambda: scratch.fill_(1.0)
+    t_end = time.perf_counter() + args.clock_warmup   # clock ramp-up before any measurement
+    while time.perf_counter() < t_end:
+        flush()
+        torch.cuda.synchronize()
     iters = max(args.steps, 50)
     out = {"configs": {}}
     md = ["# Measurement suite (MI355X, one GPU)", "",
@@ -614,6 +629,14 @@ def main():
 
     run_sparse = runner(sparse)
     run_dense = runner(dense)
+    # GPU clocks ramp up over the first fraction of a second under load: keep
+    # the GPU busy for --clock-warmup seconds before the W warmup steps (all of
+    # it outside the timed region).
+    t_end = time.perf_counter() + args.clock_warmup
+    while time.perf_counter() < t_end:
+        run_sparse()
+        run_dense()
+        torch.cuda.synchronize()
     for _ in range(args.warmup):
         run_sparse()
         run_dense()
