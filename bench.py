@@ -579,7 +579,10 @@ def main():
     if args.profile_reweight:
         layer = next(l for l in synth.c3d_layers() if l.name == args.profile_reweight)
         r = reweight_layer(torch, layer, "bf16", True)
-        r["fn"]()
+        t_end = time.perf_counter() + args.clock_warmup   # clock ramp-up
+        while time.perf_counter() < t_end:
+            r["fn"]()
+            torch.cuda.synchronize()
         ms = time_region(torch, r["fn"], args.layer_reps, stream)
         out = {"reweight_layer": layer.name, "launches": args.layer_reps, "ms_per_launch": ms,
                "algorithmic_bytes": r["bytes"], "gbps": r["bytes"] / (ms * 1e-3) / 1e9}
