@@ -39,7 +39,7 @@ def parse():
     p.add_argument("--group", default="4x4", help="kernel group size g_MxG_N of the masks")
     p.add_argument("--no-graph", action="store_true", help="launch eagerly instead of a HIP graph")
     p.add_argument("--clock-warmup", type=float, default=0.5, metavar="SECONDS",
-                   help="keep the GPU busy this long before the warmup steps (clock ramp-up)")
+                   help="load the GPU this long before measuring (clock ramp-up)")
     p.add_argument("--streams", type=int, default=4,
                    help="S3D: streams for independent Inception branches (1 = in order)")
     p.add_argument("--separate-pool", action="store_true",
@@ -76,6 +76,22 @@ def log(*a):
 
 
 SPIN_CYCLES = 400000   # ~0.2 ms of GPU spin, longer than the host's enqueue of one launch
+
+
+def clock_warmup(torch, seconds):
+    """Keep the GPU under load for `seconds` before measuring: its clocks ramp
+    up over the first fraction of a second of work.  Large bf16 matrix
+    products give the load with few kernel launches (short profiler traces)."""
+    if seconds <= 0:
+        return
+    a = torch.ones(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    b = torch.ones(8192, 8192, device="cuda", dtype=torch.bfloat16)
+    t_end = time.perf_counter() + seconds
+    while time.perf_counter() < t_end:
+        for _ in range(4):
+            torch.mm(a, b)
+        torch.cuda.synchronize()
+    del a, b
 
 
 def time_region(torch, fn, steps, stream):
@@ -161,12 +177,7 @@ def profile_layer(args, torch, stream):
     sparse.forward()
     fn = dict((c[0].name, c[1]) for c in sparse.layer_calls())[l.name]
     fn()
-    # Keep the GPU busy for --clock-warmup seconds first: the clocks ramp up
-    # under load, and the stack measurement runs after the same warm-up.
-    t_end = time.perf_counter() + args.clock_warmup
-    while time.perf_counter() < t_end:
-        sparse.forward()
-        torch.cuda.synchronize()
+    clock_warmup(torch, args.clock_warmup)   # as before the stack measurement
     if args.layer_graph:
         # as the stack measurement launches it: back to back inside a HIP graph
         g = graph_of(torch, fn, args.layer_reps)
@@ -371,10 +382,7 @@ def suite(args, torch, stream):
 
     scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")   # 1 GiB
     flush = lambda: scratch.fill_(1.0)
-    t_end = time.perf_counter() + args.clock_warmup   # clock ramp-up before any measurement
-    while time.perf_counter() < t_end:
-        flush()
-        torch.cuda.synchronize()
+    clock_warmup(torch, args.clock_warmup)
     iters = max(args.steps, 50)
     out = {"configs": {}}
     md = ["# Measurement suite (MI355X, one GPU)", "",
@@ -579,10 +587,7 @@ def main():
     if args.profile_reweight:
         layer = next(l for l in synth.c3d_layers() if l.name == args.profile_reweight)
         r = reweight_layer(torch, layer, "bf16", True)
-        t_end = time.perf_counter() + args.clock_warmup   # clock ramp-up
-        while time.perf_counter() < t_end:
-            r["fn"]()
-            torch.cuda.synchronize()
+        clock_warmup(torch, args.clock_warmup)
         ms = time_region(torch, r["fn"], args.layer_reps, stream)
         out = {"reweight_layer": layer.name, "launches": args.layer_reps, "ms_per_launch": ms,
                "algorithmic_bytes": r["bytes"], "gbps": r["bytes"] / (ms * 1e-3) / 1e9}
@@ -632,14 +637,7 @@ def main():
 
     run_sparse = runner(sparse)
     run_dense = runner(dense)
-    # GPU clocks ramp up over the first fraction of a second under load: keep
-    # the GPU busy for --clock-warmup seconds before the W warmup steps (all of
-    # it outside the timed region).
-    t_end = time.perf_counter() + args.clock_warmup
-    while time.perf_counter() < t_end:
-        run_sparse()
-        run_dense()
-        torch.cuda.synchronize()
+    clock_warmup(torch, args.clock_warmup)   # outside the timed region
     for _ in range(args.warmup):
         run_sparse()
         run_dense()
