@@ -310,22 +310,25 @@ Tiling small_tiling(const Geom &g) {
   return t;
 }
 
-// Voxel slots per workgroup of the 16-bit item kernels: 128 (8 fragments of
-// 16 per wave) or 64 (4 fragments).  Wide bricks reuse each weight fragment
+// Voxel slots per workgroup of the item kernels: 128 (8 fragments of 16 per
+// wave; two slots per lane in the exact fp32 kernel) or 64 (4 fragments; one
+// slot per lane).  Wide bricks reuse each weight fragment
 // over more voxels and stage less halo per output; narrow bricks double the
 // workgroups, which pays when 128-slot bricks times 16-filter tiles give
 // fewer waves than the GPU has SIMDs (the layer would otherwise need deep
 // channel splits and their reduction pass).  Measured on MI355X over the
-// C3D and R(2+1)D layers at batch 1.  Benchmark switch: RT3D_SLOTS=64|128.
+// C3D and R(2+1)D layers at batch 1 (and on the single fp32 layers).
+// Benchmark switch: RT3D_SLOTS=64|128.
 int brick_slots(const Geom &g) {
-  if (g.es != 2) return kSlots;
   if (const char *env = std::getenv("RT3D_SLOTS")) {
     const int v = std::atoi(env);
     if (v == 64 || v == 128) return v;
   }
   const long voxels = static_cast<long>(std::max(g.n, 1)) * g.to * g.ho * g.wo;
   const long waves = (voxels + kSlots - 1) / kSlots * ((g.c_out + 15) / 16);
-  return waves < 1024 ? 64 : kSlots;
+  // fp32 waves carry 8x the MFMA time per item (16x16x4 at 1/16 of the
+  // 16-bit rate): narrow bricks only pay below one wave per CU.
+  return waves < (g.es == 4 ? 256 : 1024) ? 64 : kSlots;
 }
 
 Tiling layer_tiling(const Geom &g) {

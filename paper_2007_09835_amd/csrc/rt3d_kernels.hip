@@ -451,6 +451,19 @@ __device__ __forceinline__ float4 shfl_xor4(float4 v, int m) {
 }
 
 
+// r[k] <- r[(k + by) % R] for a wave-uniform 0 <= by < R.
+template <int R, typename X>
+__device__ __forceinline__ void rotate_ring(X (&r)[R], int by) {
+  static_for<R - 1>([&](auto kc) {
+    constexpr int K = decltype(kc)::value + 1;
+    if (by == K) {
+      X t[R];
+      static_for<R>([&](auto ic) { t[ic] = r[(decltype(ic)::value + K) % R]; });
+      static_for<R>([&](auto ic) { r[ic] = t[ic]; });
+    }
+  });
+}
+
 // Walks voxel slots (t, h, w) of a bt x bh x bw box in steps of `step`
 // slots with carries instead of divisions (step is at most 64).
 struct BoxIter {
@@ -1107,39 +1120,89 @@ __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
   const uint32_t *sp = a.step_ptr + static_cast<long>(active ? wt : 0) * (a.nchunks + 1);
   const float *A = static_cast<const float *>(a.a);
 
+  // Software pipeline over the wave's items (as in the 16-bit item kernel):
+  // the weight value, LDS offset and keep bits of item i+D are in flight
+  // from global memory, and the B operands of item i+1 are read from LDS,
+  // while the MFMAs of item i run.  The item stream of the split runs across
+  // chunk boundaries with clamped indices; only B waits for a chunk's halo.
+  constexpr int D = 8;
+  float ra[D];
+  uint32_t roff[D], rkeep[D];
+  float4 rb[2][SUB];
+  auto fetch = [&](int slot, uint32_t it) {
+    ra[slot] = A[static_cast<long>(it) * 64 + lane];
+    roff[slot] = a.items[it];
+    rkeep[slot] = a.keep[it];
+  };
+  auto load_b = [&](int slot, uint32_t off) {
+    #pragma unroll
+    for (int s = 0; s < SUB; ++s) rb[slot][s] = *reinterpret_cast<const float4 *>(lds + vb[s] + off);
+  };
+  auto mma = [&](int bs, int as) {
+    const uint32_t keep = uniform(rkeep[as]);
+    const float av = ra[as];
+    static_for<4>([&](auto gc) {
+      constexpr int G = decltype(gc)::value;
+      if (keep & (1u << G)) {
+        #pragma unroll
+        for (int s = 0; s < SUB; ++s) {
+          acc[G][s] = mfma441<4 * G + 0>(av, rb[bs][s].x, acc[G][s]);
+          acc[G][s] = mfma441<4 * G + 1>(av, rb[bs][s].y, acc[G][s]);
+          acc[G][s] = mfma441<4 * G + 2>(av, rb[bs][s].z, acc[G][s]);
+          acc[G][s] = mfma441<4 * G + 3>(av, rb[bs][s].w, acc[G][s]);
+        }
+      }
+    });
+  };
+
   int ch0, ch1;
   split_range(a, wg.split, ch0, ch1);
+  const uint32_t S0 = uniform(sp[ch0]), S1 = uniform(sp[ch1]);
+  const bool work = active && S1 > S0;
+  const uint32_t LAST = work ? S1 - 1 : S0;
   Stager<4, 8> st;
   st.init(a, b);
   if (st.ok && ch0 < ch1) st.issue(a, ch0 * a.cc);
+  if (work) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) fetch(d, min(S0 + d, LAST));
+  }
   for (int ch = ch0; ch < ch1; ++ch) {
     __syncthreads();  // every wave is done with the previous chunk
     if (st.ok) st.commit(lds, a);
     else stage_halo<4>(lds, a, b, ch * a.cc);
     __syncthreads();
     if (st.ok && ch + 1 < ch1) st.issue(a, (ch + 1) * a.cc);  // overlaps this chunk's MFMAs
-    if (!active) continue;
-    const uint32_t it_end = uniform(sp[ch + 1]);
-    for (uint32_t it = uniform(sp[ch]); it < it_end; ++it) {
-      const uint32_t off = uniform(a.items[it]);
-      const uint32_t keep = uniform(a.keep[it]);
-      const float av = A[static_cast<long>(it) * 64 + lane];
-      float4 bv[SUB];
-      #pragma unroll
-      for (int s = 0; s < SUB; ++s) bv[s] = *reinterpret_cast<const float4 *>(lds + vb[s] + off);
-      static_for<4>([&](auto gc) {
-        constexpr int G = decltype(gc)::value;
-        if (keep & (1u << G)) {
-          #pragma unroll
-          for (int s = 0; s < SUB; ++s) {
-            acc[G][s] = mfma441<4 * G + 0>(av, bv[s].x, acc[G][s]);
-            acc[G][s] = mfma441<4 * G + 1>(av, bv[s].y, acc[G][s]);
-            acc[G][s] = mfma441<4 * G + 2>(av, bv[s].z, acc[G][s]);
-            acc[G][s] = mfma441<4 * G + 3>(av, bv[s].w, acc[G][s]);
-          }
-        }
+    if (!work) continue;
+    const uint32_t i_beg = uniform(sp[ch]), i_end = uniform(sp[ch + 1]);
+    if (i_beg == i_end) continue;
+    // Ring slots are relative to the chunk's first item: slot i % D for
+    // weights, offsets and keep bits, i % 2 for B.
+    load_b(0, uniform(roff[0]));
+    uint32_t i = i_beg;
+    for (; i + D <= i_end; i += D) {
+      static_for<D>([&](auto dc) {
+        constexpr int K = decltype(dc)::value;
+        load_b((K + 1) & 1, uniform(roff[(K + 1) % D]));
+        mma(K & 1, K);
+        fetch(K, min(i + K + D, LAST));
+        __builtin_amdgcn_sched_barrier(0);
       });
     }
+    const uint32_t rem = i_end - i;  // tail: 0..D-1 items
+    static_for<D - 1>([&](auto dc) {
+      constexpr int K = decltype(dc)::value;
+      if (K < rem) {
+        if (K + 1 < rem) load_b((K + 1) & 1, uniform(roff[(K + 1) % D]));
+        mma(K & 1, K);
+        fetch(K, min(i + K + D, LAST));
+      }
+    });
+    // The rings hold items i_end.. at slots (n + k) % D: rotate them to slot 0.
+    const int n = static_cast<int>(i_end - i_beg);
+    rotate_ring(ra, n % D);
+    rotate_ring(roff, n % D);
+    rotate_ring(rkeep, n % D);
   }
   if (a.splits > 1) {
     if (active) {
@@ -1617,12 +1680,18 @@ int conv_resident(int variant, int dtype, int mfw, int nf, size_t lds) {
 #undef RT3D_RES16
       return 0;
     case kVarDenseItemsF32:
-      if (mfw == 1) return resident(items_f32_kernel<1, 8>, lds);
-      if (mfw == 2) return resident(items_f32_kernel<2, 8>, lds);
-      if (mfw == 4) return resident(items_f32_kernel<4, 8>, lds);
+      if (nf == 4) {
+        if (mfw == 1) return resident(items_f32_kernel<1, 4>, lds);
+        if (mfw == 2) return resident(items_f32_kernel<2, 4>, lds);
+        if (mfw == 4) return resident(items_f32_kernel<4, 4>, lds);
+      } else {
+        if (mfw == 1) return resident(items_f32_kernel<1, 8>, lds);
+        if (mfw == 2) return resident(items_f32_kernel<2, 8>, lds);
+        if (mfw == 4) return resident(items_f32_kernel<4, 8>, lds);
+      }
       return 0;
     case kVarKgsExactF32:
-      return resident(kgs_exact_f32_kernel<2>, lds);
+      return nf == 4 ? resident(kgs_exact_f32_kernel<1>, lds) : resident(kgs_exact_f32_kernel<2>, lds);
     default:
       return 0;
   }
@@ -1709,6 +1778,13 @@ int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream) {
 }
 
 int launch_items_f32(const ConvArgs &a, int mfw, void *stream) {
+  if (a.nf == 4) {
+    if (mfw == 1) return launch_conv(items_f32_kernel<1, 4>, a, stream);
+    if (mfw == 2) return launch_conv(items_f32_kernel<2, 4>, a, stream);
+    if (mfw == 4) return launch_conv(items_f32_kernel<4, 4>, a, stream);
+    return hipErrorInvalidValue;
+  }
+  if (a.nf != 8) return hipErrorInvalidValue;
   if (mfw == 1) return launch_conv(items_f32_kernel<1, 8>, a, stream);
   if (mfw == 2) return launch_conv(items_f32_kernel<2, 8>, a, stream);
   if (mfw == 4) return launch_conv(items_f32_kernel<4, 8>, a, stream);
@@ -1732,6 +1808,8 @@ int launch_reduce_splits(const ConvArgs &a, int dtype, void *stream) {
 }
 
 int launch_kgs_exact_f32(const ConvArgs &a, void *stream) {
+  if (a.nf == 4) return launch_conv(kgs_exact_f32_kernel<1>, a, stream);  // 64 slots: one per lane
+  if (a.nf != 8) return hipErrorInvalidValue;
   return launch_conv(kgs_exact_f32_kernel<2>, a, stream);
 }
 

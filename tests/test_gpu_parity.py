@@ -91,17 +91,19 @@ def test_dense_small_shapes(si, dtype):
     check_full(case, f"dense {tag} {dtype}")
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("slots", ["64", "128"])
 @pytest.mark.parametrize("sparse", [True, False])
 @pytest.mark.parametrize("si", [0, 1, 2, 7])
-def test_both_brick_widths(si, sparse, slots, monkeypatch):
-    """The 16-bit item kernel with 4 and with 8 voxel fragments per wave
-    (64- and 128-slot bricks) on the same layers."""
+def test_both_brick_widths(si, sparse, slots, dtype, monkeypatch):
+    """The item kernels with 64- and 128-slot bricks (16-bit: 4 or 8 voxel
+    fragments per wave; exact fp32 KGS: one or two slots per lane) on the
+    same layers."""
     monkeypatch.setenv("RT3D_SLOTS", slots)
     tag, n, c_in, c_out, thw, k, stride, pad, keep = SHAPES[si]
     mask = masked(tag, c_out, c_in, k, min(keep, k[0] * k[1] * k[2])) if sparse else None
-    case = LayerCase(tag + "w" + slots, n, c_in, c_out, thw, k, stride, pad, "bf16", mask)
-    check_full(case, f"{'kgs' if sparse else 'dense'} {tag} slots={slots}")
+    case = LayerCase(tag + "w" + slots, n, c_in, c_out, thw, k, stride, pad, dtype, mask)
+    check_full(case, f"{'kgs' if sparse else 'dense'} {tag} {dtype} slots={slots}")
 
 
 # First-layer shapes (c_in <= 4, kernels up to 3x3x3, stride 1) run on the
