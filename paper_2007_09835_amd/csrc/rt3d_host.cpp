@@ -1003,8 +1003,10 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   a.nbricks = static_cast<int32_t>(static_cast<long>(a.n) * a.nbt * a.nbh * a.nbw);
   a.ntg = (a.wave_tiles + a.wpw - 1) / a.wpw;
   a.grid = 0;  // one workgroup per tile
-  // The kernels divide workgroup ids and (pooled) voxel indices with a
-  // 24-bit reciprocal method.
+  // The kernels divide workgroup ids, (pooled) voxel indices and chunk
+  // ranges (split * nchunks) with a 24-bit reciprocal method.
+  if (tl.nchunks >= 4096)
+    return fail(RT3D_ERR_UNSUPPORTED, "4096 or more input-channel chunks");
   if (a.total_vox >= (1L << 24))
     return fail(RT3D_ERR_UNSUPPORTED, "2^24 or more output voxels per launch");
   if (static_cast<long>(a.n) * a.nbt * a.nbh * a.nbw * a.ntg * a.splits >= (1L << 24))

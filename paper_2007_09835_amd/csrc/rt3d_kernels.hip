@@ -145,6 +145,17 @@ __device__ __forceinline__ Slot slot_at(const ConvArgs &a, const Brick &b, int t
   return o;
 }
 
+// LDS byte offset of voxel slot (tt, hh, ww)'s (0,0,0) tap: the part of
+// slot_at the K loop needs, without branches.  Slots outside the output read
+// slot 0's row (their results are never stored).
+__device__ __forceinline__ int slot_lds(const ConvArgs &a, const Brick &b, int tt, int hh, int ww) {
+  const bool valid = (tt < a.bt) & (b.ot0 + tt < a.to) & (b.oh0 + hh < a.ho) & (b.ow0 + ww < a.wo);
+  tt = valid ? tt : 0;
+  hh = valid ? hh : 0;
+  ww = valid ? ww : 0;
+  return (((tt * a.st) * a.hh + hh * a.sh) * a.hw + ww * a.sw) * a.row;
+}
+
 // (t, h, w) of voxel slots s, s + stride, s + 2*stride, ... of the brick:
 // one divmod pair to start, then carries only (VALU time in the prologue
 // and epilogue is otherwise dominated by divisions).
@@ -249,14 +260,11 @@ struct Stager {
 #pragma unroll
     for (int k = 0; k < MAXI; ++k) {
       const int idx = threadIdx.x + k * blockDim.x;
-      int v = -2;
-      if (idx < total) {
-        const int zt = b.zt0 + xt, zh = b.zh0 + xh, zw = b.zw0 + xw;
-        v = (zt >= 0 && zt < a.t && zh >= 0 && zh < a.h && zw >= 0 && zw < a.w)
-                ? ((b.nb * a.t + zt) * a.h + zh) * a.w + zw
-                : -1;
-      }
-      vox[k] = v;
+      const int zt = b.zt0 + xt, zh = b.zh0 + xh, zw = b.zw0 + xw;
+      const bool in = (static_cast<unsigned>(zt) < static_cast<unsigned>(a.t)) &
+                      (static_cast<unsigned>(zh) < static_cast<unsigned>(a.h)) &
+                      (static_cast<unsigned>(zw) < static_cast<unsigned>(a.w));
+      vox[k] = idx < total ? (in ? ((b.nb * a.t + zt) * a.h + zh) * a.w + zw : -1) : -2;
       xw += sx.r;
       const int cw = xw >= a.hw ? 1 : 0;
       xw -= cw * a.hw;
@@ -336,10 +344,11 @@ struct Stager {
 template <typename T>
 __device__ __forceinline__ float to_f32(T v) { return static_cast<float>(v); }
 
-// Channel chunks handled by this workgroup's split.
+// Channel chunks handled by this workgroup's split (the host keeps nchunks
+// below 4096, so the products stay in the 24-bit division's range).
 __device__ __forceinline__ void split_range(const ConvArgs &a, int split, int &ch0, int &ch1) {
-  ch0 = static_cast<int>((static_cast<long>(split) * a.nchunks) / a.splits);
-  ch1 = static_cast<int>((static_cast<long>(split + 1) * a.nchunks) / a.splits);
+  ch0 = uniform(divmod(split * a.nchunks, a.splits).q);
+  ch1 = uniform(divmod((split + 1) * a.nchunks, a.splits).q);
 }
 
 // ---------------------------------------------------------------------------
@@ -566,7 +575,7 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
     sw.init(a, lane & 15, 16);
 #pragma unroll
     for (int j = 0; j < NF; ++j) {
-      vb[j] = slot_at(a, b, sw.t, sw.h, sw.w).lds;
+      vb[j] = slot_lds(a, b, sw.t, sw.h, sw.w);
       sw.next(a);
     }
   }
@@ -971,7 +980,7 @@ __global__ __launch_bounds__(256) void items_f32_kernel(ConvArgs a) {
     sw.init(a, lane & 15, 16);
 #pragma unroll
     for (int j = 0; j < NF; ++j) {
-      vb[j] = slot_at(a, b, sw.t, sw.h, sw.w).lds;
+      vb[j] = slot_lds(a, b, sw.t, sw.h, sw.w);
       sw.next(a);
     }
   }
@@ -1106,7 +1115,7 @@ __global__ __launch_bounds__(256) void kgs_exact_f32_kernel(ConvArgs a) {
     sw.init(a, lane, 64);
 #pragma unroll
     for (int s = 0; s < SUB; ++s) {
-      vb[s] = slot_at(a, b, sw.t, sw.h, sw.w).lds;
+      vb[s] = slot_lds(a, b, sw.t, sw.h, sw.w);
       sw.next(a);
     }
   }
