@@ -23,6 +23,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "KGS conv3d dense-equiv TFLOP/s + ms/clip (C3D 16x112x112); speedup vs dense"
 PEAK_TFLOPS = {"bf16": 2500.0, "f16": 2500.0, "f32": 157.3}   # dense MFMA, MI355X spec
+HBM_GBPS = 8000.0                                                   # HBM3E, MI355X spec
 
 
 def parse():
@@ -119,6 +120,27 @@ def graph_of(torch, fn, reps):
     g.replay()
     torch.cuda.synchronize()
     return g
+
+
+def layer_roofline(l, conv, batch, ms):
+    """Roofline of one conv launch: algorithmic FLOPs (kept MACs x 2) and
+    bytes (input read once, kept weights once, bias, output written once,
+    residual read once), the bound they give at the MI355X peaks, and the
+    fraction of it the measured time `ms` reaches (roofline time / time)."""
+    es = 4 if conv.dtype == "f32" else 2
+    d = conv.desc_for(batch)
+    kept = batch * l.voxels_out * conv.info.kept_weights if conv.sparse else l.dense_macs(batch)
+    q = max(d.qt, 1) * max(d.qh, 1) * max(d.qw, 1)
+    out_elems = batch * l.voxels_out // q * l.c_out
+    nbytes = es * (batch * l.t * l.h * l.w * l.c_in + conv.info.kept_weights + out_elems) + 4 * l.c_out
+    if l.residual_from:
+        nbytes += es * batch * l.voxels_out * l.c_out
+    flops = 2.0 * kept
+    t_mma = flops / (PEAK_TFLOPS[conv.dtype] * 1e12)
+    t_hbm = nbytes / (HBM_GBPS * 1e9)
+    t_roof = max(t_mma, t_hbm)
+    return {"flops": flops, "bytes": nbytes, "bound": "mfma" if t_mma >= t_hbm else "hbm",
+            "roofline_ms": t_roof * 1e3, "frac": t_roof / (ms * 1e-3)}
 
 
 def per_layer_ms(torch, stack, reps, stream):
@@ -488,6 +510,8 @@ def suite(args, torch, stream):
             res[name] = {"warm": latency(torch, g.replay, iters, stream),
                          "cold": latency(torch, g.replay, max(iters // 5, 10), stream, flush),
                          "layers": per_layer_ms(torch, st, 20, stream)}
+            res[name]["roofline"] = [layer_roofline(l, c, batch, ms) for l, c, ms in
+                                     zip(st.layers, st.convs, res[name]["layers"])]
         return sp, res
 
     md += ["## Configs 3-5: stacks (bf16, HIP graph per pass)", "",
@@ -521,9 +545,14 @@ def suite(args, torch, stream):
         if "batch 32" not in e["label"] and "R(2+1)D" not in e["label"] and "S3D" not in e["label"]:
             continue
         md += ["### %s: per layer (ms per launch, warm)" % e["label"], "",
-               "| layer | R | KGS | dense | speedup | speedup / R |", "|---|---|---|---|---|---|"]
-        for name, r, ks, ds in zip(e["layers"], e["layer_rates"], e["kgs"]["layers"], e["dense"]["layers"]):
-            md.append("| %s | %.2f | %.4f | %.4f | %.2f | %.2f |" % (name, r, ks, ds, ds / ks, ds / ks / r))
+               "| layer | R | KGS | dense | speedup | speedup / R | KGS exec TF | KGS roofline frac | dense roofline frac |",
+               "|---|---|---|---|---|---|---|---|---|"]
+        for name, r, ks, ds, kr, dr in zip(e["layers"], e["layer_rates"], e["kgs"]["layers"],
+                                           e["dense"]["layers"], e["kgs"]["roofline"],
+                                           e["dense"]["roofline"]):
+            md.append("| %s | %.2f | %.4f | %.4f | %.2f | %.2f | %.0f | %.3f (%s) | %.3f (%s) |" % (
+                name, r, ks, ds, ds / ks, ds / ks / r, kr["flops"] / (ks * 1e-3) / 1e12,
+                kr["frac"], kr["bound"], dr["frac"], dr["bound"]))
         md.append("")
     out["configs"]["stacks"] = stacks
 
@@ -670,13 +699,16 @@ def main():
             "dense_equiv_tflops": 2 * macs_dense / lay_s[i] / 1e9,
             "executed_tflops": 2 * kept / lay_s[i] / 1e9,
             "dense_kernel_tflops": 2 * macs_dense / lay_d[i] / 1e9,
+            "roofline_sparse": layer_roofline(l, sparse.convs[i], args.batch, lay_s[i]),
+            "roofline_dense": layer_roofline(dense.layers[i], dense.convs[i], args.batch, lay_d[i]),
         })
         row = rows[-1]
-        log("%-10s %5d->%-5d R=%.2f  kgs %.4f ms (%.0f/%.0f TF eq/exec)  dense %.4f ms (%.0f TF)"
-            "  speedup %.2f (%.2f R)" % (l.name, l.c_in, l.c_out, r, lay_s[i],
-                                         row["dense_equiv_tflops"], row["executed_tflops"],
-                                         lay_d[i], row["dense_kernel_tflops"], row["speedup"],
-                                         row["speedup_over_rate"]))
+        log("%-10s %5d->%-5d R=%.2f  kgs %.4f ms (%.0f/%.0f TF eq/exec, %.3f of %s roofline)  "
+            "dense %.4f ms (%.0f TF, %.3f)  speedup %.2f (%.2f R)" % (
+                l.name, l.c_in, l.c_out, r, lay_s[i], row["dense_equiv_tflops"],
+                row["executed_tflops"], row["roofline_sparse"]["frac"],
+                row["roofline_sparse"]["bound"], lay_d[i], row["dense_kernel_tflops"],
+                row["roofline_dense"]["frac"], row["speedup"], row["speedup_over_rate"]))
 
     # Dominant kernel: the sparse-stack layer with the largest duration.
     dom = max(range(len(rows)), key=lambda i: rows[i]["ms_sparse"])
