@@ -139,7 +139,10 @@ rt3d_status rt3d_conv3d_out_shape(const rt3d_conv3d_desc *desc,
  * A blob (KGS or dense) is tied to every desc field except n and flags: the
  * kernel layout is planned for the layer's input extent, strides and
  * padding, so one blob serves any batch size and any epilogue flags, and a
- * forward call with other extents fails with RT3D_ERR_BLOB_MISMATCH.  Device
+ * forward call with other extents fails with RT3D_ERR_BLOB_MISMATCH.  The
+ * layout's tile shapes are chosen for desc->n at pack time (the voxel brick
+ * and the filter-tile width depend on how much parallelism the batch gives);
+ * a blob packed for one batch size runs correctly at any other.  Device
  * pointers (x, y, residual, bias, blob, workspace) must be 16-byte aligned. */
 rt3d_status rt3d_kgs_pack_size(const rt3d_conv3d_desc *desc, const uint8_t *mask,
                                uint64_t *bytes);

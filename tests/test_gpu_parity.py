@@ -261,6 +261,28 @@ def test_fused_pool_epilogue(pi):
     check_full(case, f"pooled {tag} {dtype} {'kgs' if sparse else 'dense'}")
 
 
+def test_blob_packed_for_another_batch_size():
+    """The tile shapes are chosen for the batch size given at pack time (64-
+    or 128-slot bricks, 16- or 64-filter KGS tiles); a blob packed for one
+    batch size gives the same results at another."""
+    def repack(case, c_in, c_out, thw, k, stride, pad, batch):
+        case.conv = layers.Conv3d(c_in, c_out, thw, k, stride, pad, case.w_t,
+                                  case.b64.astype(np.float32), case.mask, case.dtype,
+                                  batch=batch)
+
+    # packed for batch 1 (64-slot bricks), run at batch 3
+    mask = masked("rb1", 48, 32, (3, 3, 3), 9)
+    case = LayerCase("rb1", 3, 32, 48, (4, 10, 12), (3, 3, 3), (1, 1, 1), (1, 1, 1), "bf16", mask)
+    repack(case, 32, 48, (4, 10, 12), (3, 3, 3), (1, 1, 1), (1, 1, 1), 1)
+    check_full(case, "batch-1 blob at batch 3")
+    # packed for batch 32 (64-filter KGS tiles on a wide layer), run at batch 1
+    mask = masked("rb32", 256, 256, (3, 3, 3), 13)
+    case = LayerCase("rb32", 1, 256, 256, (8, 28, 28), (3, 3, 3), (1, 1, 1), (1, 1, 1), "bf16",
+                     mask)
+    repack(case, 256, 256, (8, 28, 28), (3, 3, 3), (1, 1, 1), (1, 1, 1), 32)
+    check_sampled(case, "batch-32 blob at batch 1", count=1500)
+
+
 def test_runs_are_deterministic():
     mask = masked("det", 64, 64, (3, 3, 3), 9)
     case = LayerCase("det", 1, 64, 64, (4, 14, 14), (3, 3, 3), (1, 1, 1), (1, 1, 1), "bf16", mask)
