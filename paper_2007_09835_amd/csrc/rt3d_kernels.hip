@@ -710,6 +710,33 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
     }
     return;
   }
+  if (NF == 4 && MFW <= 2 && a.qt * a.qh * a.qw == 1) {
+    // No pooling: a lane's accumulator holds 4 consecutive filters of one
+    // voxel slot, so the epilogue runs on registers and stores straight to
+    // y (no LDS tile, no barriers).  Narrow tiles only: in the wider ones
+    // the extra live registers would cost the second wave per SIMD.
+    if (active) {
+      float4 bb[MFW];
+#pragma unroll
+      for (int i = 0; i < MFW; ++i) bb[i] = load_bias4(a, wt * 16 * MFW + 16 * i + 4 * g);
+      SlotWalk sw;
+      sw.init(a, lane & 15, 16);
+#pragma unroll
+      for (int j = 0; j < NF; ++j) {
+        const Slot sl = slot_at(a, b, sw.t, sw.h, sw.w);
+        sw.next(a);
+        if (!sl.valid) continue;
+#pragma unroll
+        for (int i = 0; i < MFW; ++i) {
+          const int m0 = wt * 16 * MFW + 16 * i + 4 * g;
+          if (m0 >= a.c_out) continue;
+          const float4 raw = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+          put4<T>(a, sl.out, m0, activate4<T>(a, sl.out, m0, raw, bb[i]));
+        }
+      }
+    }
+    return;
+  }
   const int m_wg0 = wg.tg * a.wpw * 16 * MFW;
   __syncthreads();  // the halo is no longer needed: reuse LDS for the tile
   if (active) {
@@ -1062,6 +1089,33 @@ __global__ __launch_bounds__(256) void items_f32_kernel(ConvArgs a) {
 #pragma unroll
         for (int i = 0; i < MFW; ++i)
           put_partial(a, sl, wt * 16 * MFW + 16 * i + 4 * g, wg.split, acc[i][j]);
+      }
+    }
+    return;
+  }
+  if (NF == 4 && MFW <= 2 && a.qt * a.qh * a.qw == 1) {
+    // No pooling: a lane's accumulator holds 4 consecutive filters of one
+    // voxel slot, so the epilogue runs on registers and stores straight to
+    // y (no LDS tile, no barriers).  Narrow tiles only: in the wider ones
+    // the extra live registers would cost the second wave per SIMD.
+    if (active) {
+      float4 bb[MFW];
+#pragma unroll
+      for (int i = 0; i < MFW; ++i) bb[i] = load_bias4(a, wt * 16 * MFW + 16 * i + 4 * g);
+      SlotWalk sw;
+      sw.init(a, lane & 15, 16);
+#pragma unroll
+      for (int j = 0; j < NF; ++j) {
+        const Slot sl = slot_at(a, b, sw.t, sw.h, sw.w);
+        sw.next(a);
+        if (!sl.valid) continue;
+#pragma unroll
+        for (int i = 0; i < MFW; ++i) {
+          const int m0 = wt * 16 * MFW + 16 * i + 4 * g;
+          if (m0 >= a.c_out) continue;
+          const float4 raw = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+          put4<float>(a, sl.out, m0, activate4<float>(a, sl.out, m0, raw, bb[i]));
+        }
       }
     }
     return;
