@@ -283,6 +283,22 @@ def test_blob_packed_for_another_batch_size():
     check_sampled(case, "batch-32 blob at batch 1", count=1500)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("sparse", [True, False])
+@pytest.mark.parametrize("shape", [((4, 4, 32), 32, 48), ((4, 6, 34), 40, 36)])
+def test_pooled_register_epilogue(shape, sparse, dtype):
+    """2x2x2 pooling done on the accumulator registers (2x2x16 bricks of 64
+    slots: the four w-rows of a brick and adjacent lanes form the windows),
+    including a ragged second brick along w (34 = 16 + 16 + 2)."""
+    thw, c_in, c_out = shape
+    mask = masked("prp", c_out, c_in, (3, 3, 3), 9) if sparse else None
+    case = LayerCase("prp%d" % c_in, 1, c_in, c_out, thw, (3, 3, 3), (1, 1, 1), (1, 1, 1), dtype,
+                     mask, pool=(2, 2, 2))
+    plan = np.frombuffer(bytes(case.conv.info.plan), dtype=np.int32)
+    assert tuple(plan[:3]) == (2, 2, 16) and plan[8] == 64, plan[:9]
+    check_full(case, f"pooled registers {thw} {'kgs' if sparse else 'dense'} {dtype}")
+
+
 def test_runs_are_deterministic():
     mask = masked("det", 64, 64, (3, 3, 3), 9)
     case = LayerCase("det", 1, 64, 64, (4, 14, 14), (3, 3, 3), (1, 1, 1), (1, 1, 1), "bf16", mask)
