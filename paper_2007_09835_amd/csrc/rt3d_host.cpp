@@ -316,7 +316,9 @@ Tiling small_tiling(const Geom &g) {
 // over more voxels and stage less halo per output; narrow bricks double the
 // workgroups, which pays when 128-slot bricks times 16-filter tiles give
 // fewer waves than the GPU has SIMDs (the layer would otherwise need deep
-// channel splits and their reduction pass).  Measured on MI355X over the
+// channel splits and their reduction pass), and for unpooled 16-bit layers
+// well beyond that (their epilogue is then done in registers, without the
+// LDS tile and its barriers).  Measured on MI355X over the
 // C3D and R(2+1)D layers at batch 1 (and on the single fp32 layers).
 // Benchmark switch: RT3D_SLOTS=64|128.
 int brick_slots(const Geom &g) {
@@ -327,8 +329,12 @@ int brick_slots(const Geom &g) {
   const long voxels = static_cast<long>(std::max(g.n, 1)) * g.to * g.ho * g.wo;
   const long waves = (voxels + kSlots - 1) / kSlots * ((g.c_out + 15) / 16);
   // fp32 waves carry 8x the MFMA time per item (16x16x4 at 1/16 of the
-  // 16-bit rate): narrow bricks only pay below one wave per CU.
-  return waves < (g.es == 4 ? 256 : 1024) ? 64 : kSlots;
+  // 16-bit rate): narrow bricks only pay below one wave per CU.  16-bit
+  // layers without pooling keep their narrow-tile epilogue in registers, so
+  // narrow bricks pay there up to about eight 128-slot waves per SIMD.
+  const bool pooled = g.qt * g.qh * g.qw > 1;
+  const long limit = g.es == 4 ? 256 : (pooled ? 1024 : 8192);
+  return waves < limit ? 64 : kSlots;
 }
 
 Tiling layer_tiling(const Geom &g) {

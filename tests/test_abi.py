@@ -151,26 +151,29 @@ def _brick_slots(desc):
 
 
 def test_brick_width_follows_the_layer_size(monkeypatch):
-    """Layers whose 128-slot bricks times 16-filter tiles give fewer than 1024
-    waves (one per SIMD of the GPU; 256 for fp32, whose waves carry more MFMA
-    time) get 64-slot bricks, larger layers keep 128; RT3D_SLOTS overrides
-    the choice at pack time."""
+    """64-slot bricks when 128-slot bricks times 16-filter tiles give fewer
+    than 1024 waves (one per SIMD of the GPU) for pooled 16-bit layers, 8192
+    for unpooled 16-bit layers (their narrow-tile epilogue runs in
+    registers) and 256 for fp32; larger layers keep 128; RT3D_SLOTS
+    overrides the choice at pack time."""
     monkeypatch.delenv("RT3D_SLOTS", raising=False)
-    big = rt3d.make_desc(1, 64, 128, (16, 56, 56), dtype="bf16")        # 392 bricks x 8 tiles
-    small = rt3d.make_desc(1, 256, 256, (8, 28, 28), dtype="bf16")      # 49 x 16 = 784 waves
-    edge = rt3d.make_desc(1, 64, 64, (16, 56, 56), dtype="f16")         # 392 x 4 = 1568 waves
-    f32 = rt3d.make_desc(1, 256, 256, (8, 28, 28), dtype="f32")         # 784 waves
-    f32_small = rt3d.make_desc(1, 16, 32, (8, 28, 28), dtype="f32")     # 49 x 2 = 98 waves
-    assert _brick_slots(big) == 128
-    assert _brick_slots(small) == 64
-    assert _brick_slots(edge) == 128
+    pooled_big = rt3d.make_desc(1, 64, 128, (16, 56, 56), dtype="bf16", pool=(2, 2, 2))  # 3136
+    pooled_small = rt3d.make_desc(1, 256, 256, (8, 28, 28), dtype="bf16", pool=(2, 2, 2))  # 784
+    unpooled = rt3d.make_desc(1, 64, 128, (16, 56, 56), dtype="bf16")       # 3136 waves
+    unpooled_big = rt3d.make_desc(4, 64, 128, (16, 56, 56), dtype="f16")    # 12544 waves
+    f32 = rt3d.make_desc(1, 256, 256, (8, 28, 28), dtype="f32")             # 784 waves
+    f32_small = rt3d.make_desc(1, 16, 32, (8, 28, 28), dtype="f32")         # 49 x 2 = 98 waves
+    assert _brick_slots(pooled_big) == 128
+    assert _brick_slots(pooled_small) == 64
+    assert _brick_slots(unpooled) == 64
+    assert _brick_slots(unpooled_big) == 128
     assert _brick_slots(f32) == 128
     assert _brick_slots(f32_small) == 64
     monkeypatch.setenv("RT3D_SLOTS", "128")
-    assert _brick_slots(small) == 128
+    assert _brick_slots(pooled_small) == 128
     assert _brick_slots(f32_small) == 128
     monkeypatch.setenv("RT3D_SLOTS", "64")
-    assert _brick_slots(big) == 64
+    assert _brick_slots(pooled_big) == 64
     assert _brick_slots(f32) == 64
 
 
