@@ -280,17 +280,20 @@ rt3d_status canon_index(const rt3d_conv3d_desc *d, const uint8_t *mask, Canon &c
 }
 
 // Small-input-channel path (kVarSmall*16): 16-bit, c_in <= 4 (one 4-channel
-// block per tap), a halo of at most 12 lines (kt * (sh + kh)) of at most 256
-// elements ((31 sw + kw) * c_in), at most 64 taps (8 K-steps of 8), and
-// pooling that is either absent or 1x2x2 (the brick's two rows and adjacent
-// lanes).  Disable with RT3D_SMALL_KERNEL=0.
+// block per tap), a halo of at most 12 lines (kt * (sh + kh)) of at most 253
+// elements ((31 sw + kw) * c_in: one 8-byte word per lane, from the aligned
+// word at or before the line start), w * c_in % 4 == 0 (every halo line of a
+// brick then starts at the same offset within its word), at most 64 taps (8
+// K-steps of 8), and pooling that is either absent or 1x2x2 (the brick's two
+// rows and adjacent lanes).  The input must also stay below 2^31 - 8 bytes (its buffer
+// resource extent), checked at launch.  Disable with RT3D_SMALL_KERNEL=0.
 bool small_ok(const Geom &g) {
   if (const char *env = std::getenv("RT3D_SMALL_KERNEL"))
     if (std::atoi(env) == 0) return false;
   const bool pool_ok = (g.qt == 1 && g.qh == 1 && g.qw == 1) || (g.qt == 1 && g.qh == 2 && g.qw == 2);
   const int lines = g.kt * (g.sh + g.kh);
   const int line_elems = (31 * g.sw + g.kw) * g.c_in;
-  return g.es == 2 && g.c_in <= 4 && lines <= 12 && line_elems <= 256 &&
+  return g.es == 2 && g.c_in <= 4 && lines <= 12 && line_elems <= 253 && g.w * g.c_in % 4 == 0 &&
          g.kt * g.kh * g.kw <= 64 && pool_ok;
 }
 
@@ -1015,6 +1018,9 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
     return fail(RT3D_ERR_UNSUPPORTED, "4096 or more input-channel chunks");
   if (a.total_vox >= (1L << 24))
     return fail(RT3D_ERR_UNSUPPORTED, "2^24 or more output voxels per launch");
+  if ((info->variant == kVarSmallDense16 || info->variant == kVarSmallKgs16) &&
+      static_cast<long>(g.n) * g.t * g.h * g.w * g.c_in * 2 >= (1L << 31) - 8)
+    return fail(RT3D_ERR_UNSUPPORTED, "input of 2^31 - 8 bytes or more on the small-channel kernel");
   if (static_cast<long>(a.n) * a.nbt * a.nbh * a.nbw * a.ntg * a.splits >= (1L << 24))
     return fail(RT3D_ERR_UNSUPPORTED, "layer needs 2^24 or more workgroups");
   int e;

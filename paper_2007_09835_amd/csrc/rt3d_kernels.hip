@@ -798,13 +798,13 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
 
 constexpr int kSmallLines = 12;      // halo lines (t, h) per brick: kt * (sh + kh) <= 12
 
-// LL = halo-line elements per lane (hw * c_in <= 64 * LL).  RES: the layer
-// adds a residual (a separate instantiation keeps the common epilogue short).
-// STEPS: K-steps held in registers (4: kernels up to 32 taps; 8: up to 64,
-// e.g. the 1x7x7 stem convs).
-template <typename T, int MFW, int LL, bool RES, int STEPS>
+// RES: the layer adds a residual (a separate instantiation keeps the common
+// epilogue short).  STEPS: K-steps held in registers (4: kernels up to 32
+// taps; 8: up to 64, e.g. the 1x7x7 stem convs).  EPL: halo elements per
+// lane and line (2: one dword load, lines up to 127 elements; 4: one 8-byte
+// load, up to 253).
+template <typename T, int MFW, bool RES, int STEPS, int EPL>
 __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
-  constexpr int kSmallLineLoads = LL;
   using V8 = std::conditional_t<std::is_same_v<T, __bf16>, bf16x8, f16x8>;
   constexpr int NF = 4;
   extern __shared__ __align__(16) uint8_t lds[];
@@ -812,7 +812,9 @@ __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
   const int g = lane >> 4;
   const int wave = static_cast<int>(threadIdx.x) >> 6;
   const int rows = a.ht * a.hh * a.hw;
-  const int buf_bytes = ((rows * 8 + 15) & ~15) + 16;  // + a 16-byte sink for unused lanes
+  // + a sink for elements outside the line: a 2-byte slot per lane, so that
+  // the writes that land there do not collide in one bank
+  const int buf_bytes = ((rows * 8 + 15) & ~15) + 128;
   uint8_t *mine = lds + wave * 2 * buf_bytes;
   for (int i = lane; i < 2 * buf_bytes / 16; i += 64)
     reinterpret_cast<uint4 *>(mine)[i] = make_uint4(0, 0, 0, 0);
@@ -868,65 +870,73 @@ __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
     vb[j] = (hh * a.sh * a.hw + ww * a.sw) * 8;
   }
 
-  // Halo staging: line L = (xt, xh) holds hw voxels x c_in channels that are
-  // contiguous in the channels-last input; lane takes elements lane + 64k.
-  int ex[kSmallLineLoads], ec[kSmallLineLoads];
+  // Halo staging.  Line L = (xt, xh) of a brick holds hw voxels x c_in
+  // channels, contiguous in the channels-last input from element
+  // E0 = (((n t + xt) h + xh) w + zw0) c_in.  A lane loads the aligned word
+  // of EPL elements (E0 / EPL) + lane, i.e. line elements
+  // e = EPL lane + u - E0 % EPL, u < EPL, so one load per lane covers a line
+  // of up to 64 EPL - EPL + 1 elements; w c_in % 4 == 0 (host) gives every
+  // line of a brick the same shift (zw0 c_in) % EPL and makes the input a
+  // whole number of 8-byte words.  The loads go through a buffer resource
+  // whose extent is the input: words before or past it, and whole lines
+  // outside the clip (given an out-of-range offset), read as zero without
+  // touching memory.  Element u of a lane lands at LDS byte pend[u] of its
+  // line (voxel e / c_in, 8-byte rows of 4 channels), with bit 0 set when the
+  // voxel is a padding column (a zero is staged), or in the lane's sink slot
+  // when e is outside the line (pend[u] < 0).
+  using W = std::conditional_t<EPL == 4, uint2, uint32_t>;
   const int line_len = a.hw * a.c_in;
-#pragma unroll
-  for (int k = 0; k < kSmallLineLoads; ++k) {
-    const DivMod d = divmod(lane + 64 * k, a.c_in);
-    ex[k] = d.q;
-    ec[k] = d.r;
-  }
+  const long xbytes = static_cast<long>(a.n) * a.t * a.h * a.w * a.c_in * 2;  // < 2^31 - 8 (host)
+  const __amdgpu_buffer_rsrc_t xres =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(a.x), 0, static_cast<int>(xbytes), 0x00020000);
   const int nlines = a.ht * a.hh;
-  uint16_t sv[kSmallLines][kSmallLineLoads];
-  unsigned long long okbits = 0;  // element (L, k) is inside the input (else it stages a zero)
-  static_assert(kSmallLines * kSmallLineLoads <= 64, "ok bits");
-  const uint16_t *xin = static_cast<const uint16_t *>(a.x);
-  // Staging is branch-free: every lane loads from a clamped in-range address
-  // and selects zero where the element is padding, and writes go to a sink
-  // past the halo rows where the lane has no element, so all loads issue
-  // back to back and the LDS writes wait once.
+  const int sink = buf_bytes - 128 + 2 * lane;
+  W sv[kSmallLines];
+  int pend[EPL];
   auto issue = [&](int br) {
     const Brick b = decode_brick(a, br);
-    // Column offsets within a line are the same for every line of the
-    // brick; each line's base address is uniform (scalar registers), so a
-    // load is a scalar base plus one 32-bit lane offset.
-    int eo[kSmallLineLoads];
-    unsigned colok = 0;
-#pragma unroll
-    for (int k = 0; k < kSmallLineLoads; ++k) {
-      const int zw = b.zw0 + ex[k];
-      colok |= (lane + 64 * k < line_len && zw >= 0 && zw < a.w ? 1u : 0u) << k;
-      eo[k] = min(max(zw, 0), a.w - 1) * a.c_in + ec[k];
-    }
-    unsigned long long bits = 0;
 #pragma unroll
     for (int L = 0; L < kSmallLines; ++L) {
       const DivMod lt = divmod(L, a.hh);
       const int zt = b.zt0 + lt.q, zh = b.zh0 + lt.r;
       const bool line_ok = L < nlines && zt >= 0 && zt < a.t && zh >= 0 && zh < a.h;
-      const int ztc = min(max(zt, 0), a.t - 1), zhc = min(max(zh, 0), a.h - 1);
-      const int row = uniform((b.nb * a.t + ztc) * a.h + zhc);  // < 2^31: checked on the host
-      const uint16_t *lp = xin + static_cast<long>(row) * (a.w * a.c_in);
-#pragma unroll
-      for (int k = 0; k < kSmallLineLoads; ++k)
-        sv[L][k] = lp[static_cast<unsigned>(eo[k])];  // selected at commit
-      if (line_ok) bits |= static_cast<unsigned long long>(colok) << (L * kSmallLineLoads);
+      const int e0 = uniform((((b.nb * a.t + zt) * a.h + zh) * a.w + b.zw0) * a.c_in);
+      const int base = line_ok ? 2 * EPL * (e0 >> (EPL == 4 ? 2 : 1)) : static_cast<int>(0x80000000u);
+      if constexpr (EPL == 4)
+        sv[L] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(xres, base + 8 * lane, 0, 0));
+      else
+        sv[L] = __builtin_amdgcn_raw_buffer_load_b32(xres, base + 4 * lane, 0, 0);
     }
-    okbits = bits;
+    const int shift = (b.zw0 * a.c_in) & (EPL - 1);
+#pragma unroll
+    for (int u = 0; u < EPL; ++u) {
+      const int e = EPL * lane + u - shift;
+      const DivMod d = divmod(max(e, 0), a.c_in);
+      const bool pad = static_cast<unsigned>(b.zw0 + d.q) >= static_cast<unsigned>(a.w);
+      pend[u] = static_cast<unsigned>(e) < static_cast<unsigned>(line_len) ? d.q * 8 + d.r * 2 + (pad ? 1 : 0)
+                                                                           : -2;
+    }
   };
 
   auto commit = [&](uint8_t *buf) {
 #pragma unroll
-    for (int L = 0; L < kSmallLines; ++L)
-#pragma unroll
-      for (int k = 0; k < kSmallLineLoads; ++k) {
-        const bool mine_el = L < nlines && lane + 64 * k < line_len;
-        const int off = mine_el ? (L * a.hw + ex[k]) * 8 + ec[k] * 2 : buf_bytes - 16;
-        const bool ok = (okbits >> (L * kSmallLineLoads + k)) & 1ull;
-        *reinterpret_cast<uint16_t *>(buf + off) = ok ? sv[L][k] : uint16_t{0};
+    for (int L = 0; L < kSmallLines; ++L) {
+      uint32_t half[EPL];
+      if constexpr (EPL == 4) {
+        half[0] = sv[L].x & 0xffffu;
+        half[1] = sv[L].x >> 16;
+        half[2] = sv[L].y & 0xffffu;
+        half[3] = sv[L].y >> 16;
+      } else {
+        half[0] = sv[L] & 0xffffu;
+        half[1] = sv[L] >> 16;
       }
+#pragma unroll
+      for (int u = 0; u < EPL; ++u) {
+        const int o = L < nlines && pend[u] >= 0 ? L * a.hw * 8 + (pend[u] & ~1) : sink;
+        *reinterpret_cast<uint16_t *>(buf + o) = static_cast<uint16_t>((pend[u] & 1) ? 0u : half[u]);
+      }
+    }
   };
   auto wave_sync = [] {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -1793,8 +1803,8 @@ int conv_resident(int variant, int dtype, int mfw, int nf, size_t lds) {
 
 size_t small_lds_bytes(const ConvArgs &a) {
   const size_t buf =
-      ((static_cast<size_t>(a.ht) * a.hh * a.hw * 8 + 15) & ~static_cast<size_t>(15)) + 16;
-  return 4 * 2 * buf;  // four waves, two halo buffers each (rows + a 16-byte sink)
+      ((static_cast<size_t>(a.ht) * a.hh * a.hw * 8 + 15) & ~static_cast<size_t>(15)) + 128;
+  return 4 * 2 * buf;  // four waves, two halo buffers each (rows + a 2-byte sink slot per lane)
 }
 
 template <typename K>
@@ -1807,29 +1817,28 @@ int launch_small(K kernel, const ConvArgs &a, void *stream) {
   return hipGetLastError();
 }
 
-int small_line_loads(const ConvArgs &a) { return a.hw * a.c_in <= 128 ? 2 : 3; }  // 4 with 8 steps
-
-#define RT3D_SMALL_LL(T, M, FN, ...)                                                     \
+#define RT3D_SMALL_EPL(T, M, S, FN, ...)                                                 \
   do {                                                                                   \
-    if (steps8)                                                                          \
-      return res ? FN((small_kernel<T, M, 4, true, 8>), __VA_ARGS__)                     \
-                 : FN((small_kernel<T, M, 4, false, 8>), __VA_ARGS__);                   \
-    if (ll == 2)                                                                         \
-      return res ? FN((small_kernel<T, M, 2, true, 4>), __VA_ARGS__)                     \
-                 : FN((small_kernel<T, M, 2, false, 4>), __VA_ARGS__);                   \
-    return res ? FN((small_kernel<T, M, 3, true, 4>), __VA_ARGS__)                       \
-               : FN((small_kernel<T, M, 3, false, 4>), __VA_ARGS__);                     \
+    if (epl2)                                                                            \
+      return res ? FN((small_kernel<T, M, true, S, 2>), __VA_ARGS__)                     \
+                 : FN((small_kernel<T, M, false, S, 2>), __VA_ARGS__);                   \
+    return res ? FN((small_kernel<T, M, true, S, 4>), __VA_ARGS__)                       \
+               : FN((small_kernel<T, M, false, S, 4>), __VA_ARGS__);                     \
+  } while (0)
+#define RT3D_SMALL_STEPS(T, M, FN, ...)                                                  \
+  do {                                                                                   \
+    if (steps8) RT3D_SMALL_EPL(T, M, 8, FN, __VA_ARGS__);                                \
+    RT3D_SMALL_EPL(T, M, 4, FN, __VA_ARGS__);                                            \
   } while (0)
 #define RT3D_SMALL_MFW(T, FN, ...)                                                       \
   do {                                                                                   \
-    if (mfw == 1) RT3D_SMALL_LL(T, 1, FN, __VA_ARGS__);                                  \
-    if (mfw == 2) RT3D_SMALL_LL(T, 2, FN, __VA_ARGS__);                                  \
+    if (mfw == 1) RT3D_SMALL_STEPS(T, 1, FN, __VA_ARGS__);                               \
+    if (mfw == 2) RT3D_SMALL_STEPS(T, 2, FN, __VA_ARGS__);                               \
   } while (0)
-// Kernels with more than 4 K-steps (up to 8) use 4 line loads per lane.
 #define RT3D_SMALL_DISPATCH(FN, ...)                                                     \
   do {                                                                                   \
-    const int ll = small_line_loads(a);                                                  \
     const bool steps8 = a.steps_max > 4;                                                 \
+    const bool epl2 = a.hw * a.c_in <= 127;                                              \
     const bool res = a.res != nullptr;                                                   \
     if (dtype == RT3D_BF16) RT3D_SMALL_MFW(__bf16, FN, __VA_ARGS__);                      \
     else RT3D_SMALL_MFW(_Float16, FN, __VA_ARGS__);                                      \

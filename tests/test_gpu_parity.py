@@ -106,20 +106,26 @@ def test_both_brick_widths(si, sparse, slots, dtype, monkeypatch):
     check_full(case, f"{'kgs' if sparse else 'dense'} {tag} {dtype} slots={slots}")
 
 
-# First-layer shapes (c_in <= 4, kernels up to 3x3x3, stride 1) run on the
+# First-layer shapes (c_in <= 4, w * c_in % 4 == 0) run on the
 # small-input-channel kernel: wave-private bricks of 1x2x32 voxels, weights in
-# registers, optional 1x2x2 pooling in registers.
+# registers, halo lines staged by one 8-byte buffer load per lane (words
+# before the input's first byte read as zero), optional 1x2x2 pooling in
+# registers.  Widths leave a ragged last brick.
 SMALL_CIN = [
     # tag, n, c_in, c_out, thw, k, pad, pool, dtype, sparse, residual
-    ("c1", 1, 3, 64, (4, 10, 70), (3, 3, 3), (1, 1, 1), (1, 2, 2), "bf16", False, False),
-    ("c2", 2, 3, 40, (3, 7, 45), (3, 3, 3), (1, 1, 1), (1, 1, 1), "f16", True, False),
+    ("c1", 1, 3, 64, (4, 10, 72), (3, 3, 3), (1, 1, 1), (1, 2, 2), "bf16", False, False),
+    ("c2", 2, 3, 40, (3, 7, 44), (3, 3, 3), (1, 1, 1), (1, 1, 1), "f16", True, False),
     ("c3", 1, 4, 20, (2, 6, 33), (1, 3, 3), (0, 1, 1), (1, 1, 1), "bf16", False, True),
-    ("c4", 1, 1, 16, (5, 5, 9), (3, 3, 3), (0, 1, 1), (1, 2, 2), "bf16", True, False),
+    ("c4", 1, 1, 16, (5, 5, 12), (3, 3, 3), (0, 1, 1), (1, 2, 2), "bf16", True, False),
     ("c5", 3, 2, 64, (3, 9, 40), (3, 1, 3), (1, 0, 1), (1, 2, 2), "f16", False, True),
     # 1x7x7 stride (1,2,2) stems (S3D 3->64, R(2+1)D 3->45: 8 K-steps) and a 5x5 tap window
-    ("c6", 1, 3, 64, (3, 13, 75), (1, 7, 7), (0, 3, 3), (1, 1, 1), "bf16", False, False),
-    ("c7", 2, 3, 45, (2, 9, 66), (1, 7, 7), (0, 3, 3), (1, 1, 1), "f16", True, False),
+    ("c6", 1, 3, 64, (3, 13, 76), (1, 7, 7), (0, 3, 3), (1, 1, 1), "bf16", False, False),
+    ("c7", 2, 3, 45, (2, 9, 68), (1, 7, 7), (0, 3, 3), (1, 1, 1), "f16", True, False),
     ("c8", 1, 2, 20, (2, 8, 40), (1, 5, 5), (0, 2, 2), (1, 2, 2), "bf16", False, True),
+    # w * c_in % 4 != 0: halo lines would start at different offsets within
+    # their 8-byte words, so these run on the item kernel
+    ("c9", 1, 3, 32, (3, 6, 45), (3, 3, 3), (1, 1, 1), (1, 2, 2), "bf16", True, False),
+    ("c10", 2, 1, 16, (2, 5, 9), (1, 3, 3), (0, 1, 1), (1, 1, 1), "f16", False, False),
 ]
 SMALL_CIN_STRIDE = {"c6": (1, 2, 2), "c7": (1, 2, 2)}
 
@@ -130,7 +136,8 @@ def test_small_input_channel_layers(ci):
     mask = masked(tag, c_out, c_in, k, max(1, (k[0] * k[1] * k[2]) // 3)) if sparse else None
     case = LayerCase(tag, n, c_in, c_out, thw, k, SMALL_CIN_STRIDE.get(tag, (1, 1, 1)), pad, dtype,
                      mask, residual=residual, pool=pool)
-    assert case.conv.info.variant in (5, 6), case.conv.info.variant
+    small = thw[2] * c_in % 4 == 0
+    assert (case.conv.info.variant in (5, 6)) == small, case.conv.info.variant
     check_full(case, f"small c_in {tag} {dtype} {'kgs' if sparse else 'dense'}")
 
 
