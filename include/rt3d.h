@@ -181,7 +181,11 @@ rt3d_status rt3d_conv3d_workspace_size(const rt3d_conv3d_desc *desc,
  * [M] array or NULL (zero bias); residual must be non-NULL exactly when
  * RT3D_RESIDUAL is set.  y must not overlap x, residual or the blob.  Only
  * kept (group, position) pairs are multiplied; a vanilla-pruned group costs
- * nothing.  Asynchronous on `stream`. */
+ * nothing.  Asynchronous on `stream`.  Per-call limits (RT3D_ERR_UNSUPPORTED,
+ * checked before any launch; the same for rt3d_conv3d_dense_fwd): fewer
+ * than 2^24 output voxels and 2^24 workgroups, and for layers packed onto
+ * the small-input-channel kernel (c_in <= 4) an input x of fewer than
+ * 2^31 - 8 bytes. */
 rt3d_status rt3d_kgs_conv3d_fwd(const rt3d_conv3d_desc *desc, const rt3d_pack_info *info,
                                 const void *blob_dev, const void *x, const float *bias,
                                 const void *residual, void *y,
