@@ -887,6 +887,9 @@ __global__ __launch_bounds__(256) void small_kernel(ConvArgs a) {
   using W = std::conditional_t<EPL == 4, uint2, uint32_t>;
   const int line_len = a.hw * a.c_in;
   const long xbytes = static_cast<long>(a.n) * a.t * a.h * a.w * a.c_in * 2;  // < 2^31 - 8 (host)
+  // Raw buffer (stride 0): the range check compares each word's byte offset
+  // with the extent; the last descriptor word selects the 32-bit data format
+  // that untyped loads use on this architecture.
   const __amdgpu_buffer_rsrc_t xres =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(a.x), 0, static_cast<int>(xbytes), 0x00020000);
   const int nlines = a.ht * a.hh;
