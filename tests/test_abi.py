@@ -335,3 +335,27 @@ def test_group_reweight_error_paths():
     assert call(good, reg=256, ws=512, ws_bytes=2) == rt3d.RT3D_ERR_BUFFER_TOO_SMALL
     # nothing requested: nothing launched
     assert call(good) == rt3d.RT3D_OK
+
+
+def test_small_channel_kernel_choice():
+    """The small-input-channel kernel takes layers with c_in <= 4 whose halo
+    lines fit one word per lane (at most 253 elements) and whose rows hold a
+    multiple of 4 elements (w * c_in % 4 == 0: every line of a brick starts at
+    the same offset within its word); the rest run on the item kernel.  Pack
+    is host-only, so the choice is visible without a GPU."""
+    rng = np.random.default_rng(7)
+
+    def variant(c_in, w, k=(3, 3, 3), stride=(1, 1, 1), pad=(1, 1, 1)):
+        desc = rt3d.make_desc(1, c_in, 32, (4, 6, w), k, stride, pad, dtype="bf16")
+        _, info = rt3d.rt3d_dense_pack(desc, _weights(rng, (32, c_in) + tuple(k), "bf16"))
+        return info.variant
+
+    assert variant(3, 44) == 5          # 132 elements per row
+    assert variant(3, 45) == 1          # 135: lines start at different word offsets
+    assert variant(1, 12) == 5
+    assert variant(1, 9) == 1
+    # line elements (31 sw + kw) c_in: 252 fits, 256 does not
+    assert variant(4, 40, (1, 1, 1), (1, 2, 2), (0, 0, 0)) == 5
+    assert variant(4, 40, (1, 2, 2), (1, 2, 2), (0, 0, 0)) == 1
+    # stems: 1x7x7 stride (1, 2, 2) on RGB, 207 elements per line
+    assert variant(3, 224, (1, 7, 7), (1, 2, 2), (0, 3, 3)) == 5
