@@ -510,13 +510,17 @@ void pair_items(std::vector<Item> &its, const Geom &g, const Tiling &tl, PassCos
 // narrow union runs at ~1.4x the dense kernel's time per executed item), so
 // it wins when the narrow union already covers most items.  It is only
 // considered where the dense kernel itself runs 64-filter tiles (256 filters
-// or more) and the layer gives every SIMD a 64-filter wave without channel
-// splits (at batch 1 the narrow tiles' extra waves matter more).
+// or more) and either the layer gives every SIMD a 64-filter wave without
+// channel splits, or its reduction is deep (K = c_in taps >= 8192) with at
+// least 512 narrow waves (C3D conv4b-conv5b at batch 8-32, measured); at
+// batch 1 the narrow tiles' extra waves matter more.
 int kgs_tile_width(const Geom &g, const Tiling &tl, const Mask4 *m4) {
   if (g.es != 2 || !m4 || g.c_out < 256) return 1;
   const long voxels = static_cast<long>(std::max(g.n, 1)) * g.to * g.ho * g.wo;
   const long bricks = (voxels + tl.slots - 1) / tl.slots;
-  if (bricks * ((g.c_out + 63) / 64) < 1024) return 1;
+  const bool deep = static_cast<long>(g.c_in) * g.kt * g.kh * g.kw >= 8192 &&
+                    bricks * ((g.c_out + 15) / 16) >= 512;
+  if (bricks * ((g.c_out + 63) / 64) < 1024 && !deep) return 1;
   double narrow = 0, wide = 0;
   const int p4_count = (g.c_out + 3) / 4;
   for (int ch = 0; ch < tl.nchunks; ++ch) {

@@ -200,6 +200,24 @@ def test_kgs_tile_width_follows_union_size(monkeypatch):
     assert mfw(32, 5) == 1    # ~56%: the narrow union is cheaper
     assert mfw(1, 13) == 1    # batch 1: too few 64-filter waves
 
+    # Deep reductions (512 input channels x 27 taps) take the wide union with
+    # fewer voxels, from 512 narrow (16-filter) waves: C3D conv5a at batch 32
+    # (2x7x7 outputs, 25 bricks x 32 tiles), not at batch 8 (7 x 32).
+    w5 = _weights(rng, (512, 512, 3, 3, 3), "bf16")
+
+    def mfw5(n, keep):
+        desc = rt3d.make_desc(n, 512, 512, (2, 7, 7), dtype="bf16")
+        mask = np.zeros((128, 128, 27), np.uint8)
+        for p in range(128):
+            for q in range(128):
+                mask[p, q, rng.choice(27, keep, replace=False)] = 1
+        _, info = rt3d.rt3d_kgs_pack(desc, w5, mask)
+        return int(np.frombuffer(bytes(info.plan), dtype=np.int32)[10])
+
+    assert mfw5(32, 9) == 4
+    assert mfw5(8, 9) == 1
+    assert mfw5(32, 5) == 1   # the narrow union is still cheaper when sparse
+
 
 def _expect_status(status, fn, *args):
     with pytest.raises(rt3d.Rt3dError) as ei:
