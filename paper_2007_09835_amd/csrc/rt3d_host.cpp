@@ -503,9 +503,9 @@ void pair_items(std::vector<Item> &its, const Geom &g, const Tiling &tl, PassCos
 }
 
 // KGS wave-tile width for the 16-bit item kernel: 1 (16 filters walk the
-// union of their four 4x4 blocks' items) or 4 (64 filters walk the union of
-// sixteen blocks, each B fragment feeding four MFMAs, as in the dense
-// kernel).  The wide union executes more zero-weight items but costs about
+// union of their four 4x4 blocks' items), 2 (see below) or 4 (64 filters
+// walk the union of sixteen blocks, each B fragment feeding four MFMAs, as
+// in the dense kernel).  The wide union executes more zero-weight items but costs about
 // 1/1.4 as much per item (measured over the C3D layers at batch 32: the
 // narrow union runs at ~1.4x the dense kernel's time per executed item), so
 // it wins when the narrow union already covers most items.  It is only
@@ -514,9 +514,18 @@ void pair_items(std::vector<Item> &its, const Geom &g, const Tiling &tl, PassCos
 // channel splits, or its reduction is deep (K = c_in taps >= 8192) with at
 // least 512 narrow waves (C3D conv4b-conv5b at batch 8-32, measured); at
 // batch 1 the narrow tiles' extra waves matter more.
+//
+// Spatial-only 1x3x3 layers on 64-slot bricks with at least 1.25M outputs
+// (voxels x filters) take 32-filter tiles instead (the union of eight
+// blocks): measured at batch 1 on R(2+1)D layers 2-3 (-8% to -23%) and the
+// S3D 64->192 layer (-7%), while 3x3x3, temporal and smaller layers ran
+// slower with them.
 int kgs_tile_width(const Geom &g, const Tiling &tl, const Mask4 *m4) {
-  if (g.es != 2 || !m4 || g.c_out < 256) return 1;
   const long voxels = static_cast<long>(std::max(g.n, 1)) * g.to * g.ho * g.wo;
+  if (g.es == 2 && m4 && tl.slots == 64 && g.kt == 1 && g.kh * g.kw == 9 &&
+      voxels * g.c_out >= 1250000)
+    return 2;
+  if (g.es != 2 || !m4 || g.c_out < 256) return 1;
   const long bricks = (voxels + tl.slots - 1) / tl.slots;
   const bool deep = static_cast<long>(g.c_in) * g.kt * g.kh * g.kw >= 8192 &&
                     bricks * ((g.c_out + 15) / 16) >= 512;

@@ -218,6 +218,22 @@ def test_kgs_tile_width_follows_union_size(monkeypatch):
     assert mfw5(8, 9) == 1
     assert mfw5(32, 5) == 1   # the narrow union is still cheaper when sparse
 
+    # Spatial-only 1x3x3 layers with 1.25M+ outputs on 64-slot bricks: the
+    # union of eight blocks (R(2+1)D layer 2: 64 -> 144 at 16x56x56)
+    w2 = _weights(rng, (144, 64, 1, 3, 3), "bf16")
+
+    def mfw2(n, c_out, thw):
+        desc = rt3d.make_desc(n, 64, c_out, thw, (1, 3, 3), (1, 1, 1), (0, 1, 1), dtype="bf16")
+        mask = np.zeros(((c_out + 3) // 4, 16, 9), np.uint8)
+        for p in range(mask.shape[0]):
+            for q in range(16):
+                mask[p, q, rng.choice(9, 4, replace=False)] = 1
+        _, info = rt3d.rt3d_kgs_pack(desc, w2[:c_out], mask)
+        return int(np.frombuffer(bytes(info.plan), dtype=np.int32)[10])
+
+    assert mfw2(1, 144, (16, 56, 56)) == 2
+    assert mfw2(1, 144, (8, 28, 28)) == 1    # 0.9M outputs
+
 
 def _expect_status(status, fn, *args):
     with pytest.raises(rt3d.Rt3dError) as ei:
