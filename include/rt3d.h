@@ -33,7 +33,18 @@
  *     a kernel surface at the next synchronisation of that stream.
  *   - Ownership: the caller owns every buffer.  The library never allocates
  *     caller-visible memory, never frees or retains a pointer past a call,
- *     and keeps no state except a thread-local error message.
+ *     and keeps no state except a thread-local error message and a per-device
+ *     cache of runtime queries (compute-unit count, kernel occupancy).
+ *   - Tuning switch (benchmarks only; leave unset): the environment variable
+ *     RT3D_TUNE="key=value,..." overrides planner choices.  Pack-time keys
+ *     change the kernel layout written into a blob: slots=64|128 (voxel slots
+ *     per workgroup), kgs_mfw=1|2|4 and dense_mfw=1|2|4 (16-filter MFMA rows
+ *     per wave tile), small_mfw=1|2 and small_kernel=0 (the small-input-channel
+ *     kernel), kgs_map=0|1 (16-bit KGS mapping: 0 = union of the tile's kept
+ *     items, 1 = disjoint item pairs on the 2:4 sparse MFMA).  Launch-time
+ *     keys change the launch of a forward call: splits=N (input-channel
+ *     splits) and wg_order=0|1 (workgroup order).  Results stay within the
+ *     documented accuracy under every setting.
  *   - Errors: all arguments are validated before anything is launched; on
  *     error nothing is written to the outputs and rt3d_last_error_detail()
  *     describes the failure.
@@ -179,9 +190,16 @@ rt3d_status rt3d_conv3d_workspace_size(const rt3d_conv3d_desc *desc,
  * nothing is read or written and the device pointers may be NULL.  x, y, residual
  * are device pointers in the channels-last layout; bias is a device float32
  * [M] array or NULL (zero bias); residual must be non-NULL exactly when
- * RT3D_RESIDUAL is set.  y must not overlap x, residual or the blob.  Only
- * kept (group, position) pairs are multiplied; a vanilla-pruned group costs
- * nothing.  Asynchronous on `stream`.  Per-call limits (RT3D_ERR_UNSUPPORTED,
+ * RT3D_RESIDUAL is set.  y must not overlap x, residual or the blob.  Work
+ * skipped: a (4-channel block, kernel position) item that no kernel group
+ * of a wave's filter tile keeps is never read or multiplied (so a vanilla-
+ * pruned group costs nothing when its tile-mates prune the same channels).
+ * How a kept item is multiplied depends on the mapping chosen at pack time:
+ * the exact fp32 kernel issues one 4x4 MFMA per kept (group, item); the
+ * 16-bit union mapping multiplies the tile's other groups at that item by
+ * zero weights; the 16-bit pair mapping packs two items whose kept groups
+ * are disjoint into one 2:4 sparse MFMA slot and streams kept weights only.
+ * Asynchronous on `stream`.  Per-call limits (RT3D_ERR_UNSUPPORTED,
  * checked before any launch; the same for rt3d_conv3d_dense_fwd): fewer
  * than 2^24 output voxels and 2^24 workgroups, and for layers packed onto
  * the small-input-channel kernel (c_in <= 4) an input x of fewer than
@@ -223,7 +241,8 @@ rt3d_status rt3d_maxpool3d_fwd(int32_t n, int32_t c, int32_t t, int32_t h, int32
  *
  * The pruning algorithms of Section 4 penalise the norm of kernel groups: the
  * regularization-based algorithm adds lambda * sum ||W^G||_g to the training
- * loss (eq. (3)), and the reweighted algorithm (eq. (4)) multiplies each norm
+ * loss (eq. (1); per kernel position, eq. (2)), and the reweighted algorithm
+ * (eq. (3)) multiplies each norm
  * by a penalty factor P that is reset after every iteration to
  * 1 / (||W^G||_g^2 + eps), so that large groups are penalised less and small
  * ones more; after a few iterations the groups whose norm has converged to
@@ -263,7 +282,7 @@ rt3d_status rt3d_group_workspace_size(const rt3d_group_desc *desc, uint64_t *byt
  * all ones) and norm n_u:
  *   norms[u]    = n_u                                     (float32 [units])
  *   pen_next[u] = 1 / (n_u^2 + eps)   (the reweighting update; float32 [units])
- *   *reg        = lambda * sum_u P_u * n_u   (the penalty term of eq. (4);
+ *   *reg        = lambda * sum_u P_u * n_u   (the penalty term of eq. (3);
  *                                             one float32 in device memory)
  *   mask        = 1 where n_u > tau, else 0, for every kernel position the
  *                 unit covers: uint8 [P][Q][K_s], the layout rt3d_kgs_pack

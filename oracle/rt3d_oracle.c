@@ -20,7 +20,7 @@
  *     partial.
  *   - Section 4 (regularization-based and reweighted pruning): the l1 / l2
  *     norm of a group's weights at one kernel position (KGS) or over the
- *     whole group (vanilla), the penalty term of eq. (4) and the update of
+ *     whole group (vanilla), the penalty term of eq. (3) and the update of
  *     its penalty factors.
  *
  * Conventions (the paper is silent on them; readings recorded in the design
@@ -342,13 +342,13 @@ int oracle_maxpool3d(int n, int c, int t, int h, int w, int kt, int kh, int kw,
  * groups of g_m x g_n kernels, P = ceil(c_out/g_m) by Q = ceil(c_in/g_n)
  * (trailing groups partial).  A "unit" u is what one norm covers:
  *   scope 0 (KGS):     one kernel position of one group, u = (p*Q + q)*ks + pos
- *                      (the norm in the caption of Fig. 2 / eq. (3));
- *   scope 1 (vanilla): a whole group, u = p*Q + q (the group norm of eq. (2)).
+ *                      (the norm in the caption of Fig. 2 / eq. (2));
+ *   scope 1 (vanilla): a whole group, u = p*Q + q (the group norm of eq. (1)).
  * norm = 1 or 2 selects the l1 or l2 norm of the unit's weights:
  *   n_u = (sum over the unit of |w|^norm)^(1/norm).
  * With P_u the current penalty factors (pen; NULL means all ones) the call
  * evaluates
- *   reg        = lambda * sum_u P_u * n_u        (penalty term of eq. (4))
+ *   reg        = lambda * sum_u P_u * n_u        (penalty term of eq. (3))
  *   pen_next_u = 1 / (n_u^2 + eps)               (reweighting update, Section 4)
  *   mask       = n_u > tau for every kernel position of the unit (pruning the
  *                units whose norm has converged to zero), layout [P][Q][ks]

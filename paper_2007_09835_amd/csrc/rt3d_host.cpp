@@ -6,7 +6,11 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
+#include <map>
+#include <mutex>
 #include <numeric>
+#include <tuple>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -37,6 +41,21 @@ rt3d_status ok() {
 }
 
 int esize_of(int dtype) { return dtype == RT3D_F32 ? 4 : 2; }
+
+// Benchmark-only overrides of planner choices, all read from one variable,
+// RT3D_TUNE="key=value,key=value" (keys and effects are listed in
+// include/rt3d.h).  Returns -1 when the key is absent.  Unset in normal use.
+int tune(const char *key) {
+  const char *env = std::getenv("RT3D_TUNE");
+  if (!env) return -1;
+  const size_t n = std::strlen(key);
+  for (const char *p = env; *p;) {
+    while (*p == ',' || *p == ' ') ++p;
+    if (std::strncmp(p, key, n) == 0 && p[n] == '=') return std::atoi(p + n + 1);
+    while (*p && *p != ',') ++p;
+  }
+  return -1;
+}
 
 uint64_t align_up(uint64_t v, uint64_t a) { return (v + a - 1) / a * a; }
 
@@ -286,10 +305,9 @@ rt3d_status canon_index(const rt3d_conv3d_desc *d, const uint8_t *mask, Canon &c
 // brick then starts at the same offset within its word), at most 64 taps (8
 // K-steps of 8), and pooling that is either absent or 1x2x2 (the brick's two
 // rows and adjacent lanes).  The input must also stay below 2^31 - 8 bytes (its buffer
-// resource extent), checked at launch.  Disable with RT3D_SMALL_KERNEL=0.
+// resource extent), checked at launch.  Tuning switch small_kernel=0 disables it.
 bool small_ok(const Geom &g) {
-  if (const char *env = std::getenv("RT3D_SMALL_KERNEL"))
-    if (std::atoi(env) == 0) return false;
+  if (tune("small_kernel") == 0) return false;
   const bool pool_ok = (g.qt == 1 && g.qh == 1 && g.qw == 1) || (g.qt == 1 && g.qh == 2 && g.qw == 2);
   const int lines = g.kt * (g.sh + g.kh);
   const int line_elems = (31 * g.sw + g.kw) * g.c_in;
@@ -323,10 +341,10 @@ Tiling small_tiling(const Geom &g) {
 // well beyond that (their epilogue is then done in registers, without the
 // LDS tile and its barriers).  Measured on MI355X over the
 // C3D and R(2+1)D layers at batch 1 (and on the single fp32 layers).
-// Benchmark switch: RT3D_SLOTS=64|128.
+// Tuning switch slots=64|128.
 int brick_slots(const Geom &g) {
-  if (const char *env = std::getenv("RT3D_SLOTS")) {
-    const int v = std::atoi(env);
+  {
+    const int v = tune("slots");
     if (v == 64 || v == 128) return v;
   }
   const long voxels = static_cast<long>(std::max(g.n, 1)) * g.to * g.ho * g.wo;
@@ -562,26 +580,20 @@ void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
     mfw = voxels >= 2000 ? 4 : 2;
   }
   if (dense) {
-    // Benchmark A/B switch for the dense wave-tile width (1, 2 or 4).
-    if (const char *env = std::getenv("RT3D_DENSE_MFW")) {
-      const int v = std::atoi(env);
-      if (v == 1 || v == 2 || v == 4) mfw = v;
-    }
+    // Tuning switch dense_mfw=1|2|4.
+    const int v = tune("dense_mfw");
+    if (v == 1 || v == 2 || v == 4) mfw = v;
   } else if (!small) {
     mfw = kgs_tile_width(g, tl, m4);
-    if (const char *env = std::getenv("RT3D_KGS_MFW")) {
-      const int v = std::atoi(env);
-      if (v == 1 || v == 2 || v == 4) mfw = v;
-    }
+    const int v = tune("kgs_mfw");
+    if (v == 1 || v == 2 || v == 4) mfw = v;
   }
   if (small) {
     // Up to 32 filters per wave: wider tiles hold 4x the weights in
     // registers and drop residency to one wave per SIMD.
     mfw = g.c_out > 16 ? 2 : 1;
-    if (const char *env = std::getenv("RT3D_SMALL_MFW")) {
-      const int v = std::atoi(env);
-      if (v == 1 || v == 2) mfw = v;
-    }
+    const int v = tune("small_mfw");
+    if (v == 1 || v == 2) mfw = v;
   }
   const int wt_count = (g.c_out + 16 * mfw - 1) / (16 * mfw);
   L.variant = small ? (dense ? kVarSmallDense16 : kVarSmallKgs16)
@@ -647,6 +659,195 @@ void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
     L.step_ptr[static_cast<size_t>(wt) * (tl.nchunks + 1) + tl.nchunks] = step;
     L.plan.tile_steps = std::max<int32_t>(L.plan.tile_steps, static_cast<int32_t>(step - first_step));
   }
+}
+
+// ---------------------------------------------------------------------------
+// Pair mapping (kVarKgsPair16): two items per 2:4 sparse MFMA slot
+// ---------------------------------------------------------------------------
+
+struct ItemPair {
+  Item x, y;  // y.ql < 0: no partner (an offset-0 read that no group keeps)
+};
+
+// Pairs the items of one 16-filter tile and chunk so that no kernel group of
+// the tile keeps both items of a pair: a filter row then has at most two
+// nonzero weights in every quad (X.c0, X.c1, Y.c0, Y.c1) and (X.c2, X.c3,
+// Y.c2, Y.c3), the 2:4 pattern the sparse MFMA multiplies at twice the dense
+// rate.  Greedy, most constrained items first: an item kept by all four
+// groups has no partner; one kept by three groups can only take an item kept
+// by the fourth group alone; one kept by two groups takes the complementary
+// two groups first, then an item of either other group alone; items kept by
+// one group pair across groups, largest buckets first.  Every item lands in
+// exactly one pair.
+std::vector<ItemPair> pair_up(const std::vector<Item> &items) {
+  std::vector<Item> b[16];
+  for (const Item &it : items) b[it.keep & 15u].push_back(it);
+  std::vector<ItemPair> out;
+  out.reserve(items.size());
+  const Item none{-1, 0, 0};
+  auto take = [&](int m) {
+    const Item it = b[m].back();
+    b[m].pop_back();
+    return it;
+  };
+  while (!b[15].empty()) out.push_back({take(15), none});
+  for (const int m : {7, 11, 13, 14}) {
+    const int c = 15 & ~m;
+    while (!b[m].empty() && !b[c].empty()) out.push_back({take(m), take(c)});
+    while (!b[m].empty()) out.push_back({take(m), none});
+  }
+  for (const int m : {3, 5, 6})
+    while (!b[m].empty() && !b[15 & ~m].empty()) out.push_back({take(m), take(15 & ~m)});
+  for (const int m : {3, 5, 6, 9, 10, 12}) {
+    const int c = 15 & ~m, s1 = c & -c, s2 = c & ~s1;
+    while (!b[m].empty()) {
+      const int pick = b[s1].size() >= b[s2].size() ? s1 : s2;
+      if (b[pick].empty()) out.push_back({take(m), none});
+      else out.push_back({take(m), take(pick)});
+    }
+  }
+  for (;;) {
+    int s[4] = {1, 2, 4, 8};
+    std::sort(s, s + 4, [&](int u, int v) { return b[u].size() > b[v].size(); });
+    if (b[s[1]].empty()) break;
+    out.push_back({take(s[0]), take(s[1])});
+  }
+  for (const int m : {1, 2, 4, 8})
+    while (!b[m].empty()) out.push_back({take(m), none});
+  // Ascending by position, then channel block: neighbouring pairs read
+  // nearby halo rows.
+  std::stable_sort(out.begin(), out.end(), [](const ItemPair &u, const ItemPair &v) {
+    return u.x.pos != v.x.pos ? u.x.pos < v.x.pos : u.x.ql < v.x.ql;
+  });
+  return out;
+}
+
+// Lays out a padded pair list (a multiple of 8 pairs) step by step.  In a
+// step, lane groups g and g + 1 (g even) read pairs (g, g + 1) and (g + 4,
+// g + 5) in the same LDS passes, so the list is regrouped into couples of
+// pairs whose items are read together with few bank conflicts (greedy over a
+// window; a couple may swap the roles X and Y of its second pair).
+void couple_pairs(std::vector<ItemPair> &prs, const Geom &g, const Tiling &tl, PassCost &cost) {
+  const size_t n = prs.size();
+  auto off = [&](const Item &it) { return it.ql < 0 ? 0u : item_offset(g, tl, it.ql, it.pos); };
+  std::vector<char> used(n, 0);
+  std::vector<ItemPair> out;
+  out.reserve(n);
+  constexpr size_t kWindow = 32;
+  for (size_t i = 0; i < n; ++i) {
+    if (used[i]) continue;
+    used[i] = 1;
+    const uint32_t px = off(prs[i].x), py = off(prs[i].y);
+    size_t best = n;
+    bool best_swap = false;
+    int best_cost = 1 << 30;
+    for (size_t j = i + 1, looked = 0; j < n && looked < kWindow; ++j) {
+      if (used[j]) continue;
+      ++looked;
+      const uint32_t qx = off(prs[j].x), qy = off(prs[j].y);
+      const int straight = cost(px, qx) + cost(py, qy);
+      const int swapped = cost(px, qy) + cost(py, qx);
+      const int c = std::min(straight, swapped);
+      if (c < best_cost) {
+        best_cost = c;
+        best = j;
+        best_swap = swapped < straight;
+        if (c == 2) break;
+      }
+    }
+    out.push_back(prs[i]);
+    if (best < n) {
+      used[best] = 1;
+      ItemPair q = prs[best];
+      if (best_swap) std::swap(q.x, q.y);
+      out.push_back(q);
+    }
+  }
+  // Consecutive couples fill each step's positions (0,1) (2,3) (4,5) (6,7):
+  // lane groups 0/1 and 2/3 share a pass, pairs 0-3 are read by reads 0-1
+  // and pairs 4-7 by reads 2-3.
+  prs.swap(out);
+}
+
+// Pair layout: per 16-filter tile and chunk the paired items, 8 pairs per
+// K-step; per step 16 LDS offsets (lane group g: X and Y of pairs g and
+// g + 4), the step's kept 4x4 weight blocks, 32 bytes each ([row][channel])
+// in (pair, group) order, and per (lane group g, kernel group) a descriptor
+// {byte offset of the block of pair 2g, of pair 2g + 1 (2^31 when the group
+// keeps neither item), index register, 0}.  The index register holds two
+// bits per compressed A element: (0, 1, 0, 1) = 0x44 selects X's channels of
+// a pair's two quads, (2, 3, 2, 3) = 0xEE selects Y's; pair 2g sits in bits
+// 0-7, pair 2g + 1 in bits 8-15.
+void build_pairs_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const Mask4 *m4,
+                        Layout &L) {
+  const int wt_count = (g.c_out + 15) / 16;
+  L.variant = kVarKgsPair16;
+  L.plan.mfw = 1;
+  L.plan.wave_tiles = wt_count;
+  L.plan.items_per_step = 16;
+  L.step_ptr.assign(static_cast<size_t>(wt_count) * (tl.nchunks + 1), 0);
+  L.item_ptr.assign(wt_count, 0);
+  WeightSource src{w, g, m4};
+  PassCost cost(g, tl);
+  auto off = [&](const Item &it) { return it.ql < 0 ? 0u : item_offset(g, tl, it.ql, it.pos); };
+  const Item none{-1, 0, 0};
+  uint32_t step = 0, blocks = 0;
+  for (int wt = 0; wt < wt_count; ++wt) {
+    const uint32_t first = step;
+    L.item_ptr[wt] = first;
+    for (int ch = 0; ch < tl.nchunks; ++ch) {
+      L.step_ptr[static_cast<size_t>(wt) * (tl.nchunks + 1) + ch] = step;
+      std::vector<ItemPair> prs = pair_up(chunk_items(g, m4, tl.cc, ch, wt * 4, 4));
+      while (prs.size() % 8) prs.push_back({none, none});
+      couple_pairs(prs, g, tl, cost);
+      for (size_t s0 = 0; s0 < prs.size(); s0 += 8, ++step) {
+        const ItemPair *sp = &prs[s0];
+        for (int lg = 0; lg < 4; ++lg) {
+          L.items.push_back(off(sp[lg].x));
+          L.items.push_back(off(sp[lg].y));
+          L.items.push_back(off(sp[lg + 4].x));
+          L.items.push_back(off(sp[lg + 4].y));
+        }
+        uint32_t keep = 0, side = 0;
+        for (int j = 0; j < 8; ++j)
+          for (int gi = 0; gi < 4; ++gi) {
+            const bool kx = (sp[j].x.keep >> gi) & 1u, ky = (sp[j].y.keep >> gi) & 1u;
+            if (kx || ky) keep |= 1u << (4 * j + gi);
+            if (ky) side |= 1u << (4 * j + gi);
+          }
+        for (int lg = 0; lg < 4; ++lg)
+          for (int gi = 0; gi < 4; ++gi) {
+            uint32_t off[2], idx = 0;
+            for (int h = 0; h < 2; ++h) {
+              const int b = 4 * (2 * lg + h) + gi;
+              const uint32_t below = static_cast<uint32_t>(__builtin_popcount(keep & ((1u << b) - 1u)));
+              off[h] = ((keep >> b) & 1u) ? (blocks + below) * 32u : 0x80000000u;
+              idx |= (((side >> b) & 1u) ? 0xEEu : 0x44u) << (8 * h);
+            }
+            L.keep.push_back(off[0]);
+            L.keep.push_back(off[1]);
+            L.keep.push_back(idx);
+            L.keep.push_back(0);
+          }
+        for (int b = 0; b < 32; ++b) {
+          if (!((keep >> b) & 1u)) continue;
+          const int j = b >> 2, gi = b & 3;
+          const Item &it = ((side >> b) & 1u) ? sp[j].y : sp[j].x;
+          const size_t base = L.a.size();
+          L.a.resize(base + 16 * static_cast<size_t>(g.es));
+          for (int r = 0; r < 4; ++r)
+            for (int c = 0; c < 4; ++c)
+              src.copy(L.a.data() + base + (r * 4 + c) * g.es, wt * 16 + 4 * gi + r,
+                       4 * (ch * (tl.cc / 4) + it.ql) + c, it.pos);
+          ++blocks;
+        }
+      }
+    }
+    L.step_ptr[static_cast<size_t>(wt) * (tl.nchunks + 1) + tl.nchunks] = step;
+    L.plan.tile_steps = std::max<int32_t>(L.plan.tile_steps, static_cast<int32_t>(step - first));
+  }
+  // check_desc bounds a layer to 1e9 weights, so the kept blocks (16 weights
+  // each) end below byte 2^31: every kept offset stays below the not-kept mark.
 }
 
 // Exact f32 KGS layout (kVarKgsExactF32): per 16-filter tile and chunk, the
@@ -793,6 +994,19 @@ void write_blob(uint8_t *out, const rt3d_pack_info &info, const Canon *c, const 
   if (!L.a.empty()) std::memcpy(out + s.a, L.a.data(), L.a.size());
 }
 
+// 16-bit KGS mapping: pairs (2:4 sparse MFMA over 64-slot bricks) or the
+// union of a tile's kept items.  Tuning switch kgs_map=0 (union) or 1
+// (pairs).  The union is the default: on MI355X a K-step's cost follows its
+// LDS read instructions and address arithmetic, and a pair step reads every
+// item of the union as well (two 8-byte reads per pair per voxel fragment)
+// plus the register moves that interleave them, so halving the MFMAs does
+// not pay (measured on every C3D layer at batch 1 and 32).
+bool use_pairs(const Geom &g, const Mask4 *m4) {
+  (void)m4;
+  if (g.es != 2) return false;
+  return tune("kgs_map") == 1;
+}
+
 // Build everything for a KGS pack (w may be null when only sizing).
 rt3d_status plan_kgs(const rt3d_conv3d_desc *d, const uint8_t *mask, const uint8_t *w,
                      Canon &c, Layout &L, Tiling &tl, bool &vanilla) {
@@ -828,9 +1042,15 @@ rt3d_status plan_kgs(const rt3d_conv3d_desc *d, const uint8_t *mask, const uint8
       build_exact_f32_layout(g, tl, wsrc, &m4, L);
     }
   } else {
+    std::vector<uint8_t> scratch;
     if (!w) {
-      std::vector<uint8_t> scratch(static_cast<size_t>(g.c_out) * g.c_in * ks * g.es, 0);
-      build_items_layout(g, tl, scratch.data(), &m4, L, small);
+      scratch.assign(static_cast<size_t>(g.c_out) * g.c_in * ks * g.es, 0);
+      wsrc = scratch.data();
+    }
+    if (!small && use_pairs(g, &m4)) {
+      tl = choose_tiling(g, 64);
+      if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
+      build_pairs_layout(g, tl, wsrc, &m4, L);
     } else {
       build_items_layout(g, tl, wsrc, &m4, L, small);
     }
@@ -851,7 +1071,7 @@ rt3d_status check_info(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, bo
   if (info->desc_hash != desc_hash(d))
     return fail(RT3D_ERR_BLOB_MISMATCH, "blob was packed for a different layer description");
   const bool is_sparse = info->variant == kVarKgsUnion16 || info->variant == kVarKgsExactF32 ||
-                         info->variant == kVarSmallKgs16;
+                         info->variant == kVarSmallKgs16 || info->variant == kVarKgsPair16;
   if (is_sparse != sparse)
     return fail(RT3D_ERR_BLOB_MISMATCH, sparse ? "dense blob passed to the KGS forward"
                                                : "KGS blob passed to the dense forward");
@@ -888,16 +1108,76 @@ double xcd_fill_bytes(long nb, long nt, long ns, int order, double a_unit, doubl
   return total;
 }
 
+// Device queries are answered once per device and cached: the forward
+// calls plan their launch on every call, and the runtime's occupancy and
+// attribute queries would otherwise cost host time each time.
+constexpr int kMaxDevices = 64;
+
+int current_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  return dev;
+}
+
 // Compute units of the current device (256 when no device answers).
 int device_cus() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+  static std::atomic<int> cache[kMaxDevices];
+  const int dev = current_device();
+  int cus = cache[dev].load(std::memory_order_relaxed);
+  if (cus > 0) return cus;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       cus <= 0) {
     (void)hipGetLastError();
     return 256;
   }
+  cache[dev].store(cus, std::memory_order_relaxed);
   return cus;
+}
+
+// Resident workgroups per CU of a conv kernel at an LDS size (cached per
+// device and kernel configuration; 0 when the runtime cannot say).
+int cached_resident(int variant, int dtype, int mfw, int nf, size_t lds) {
+  static std::mutex mu;
+  static std::map<std::tuple<int, int, int, int, int, size_t>, int> cache;
+  const auto key = std::make_tuple(current_device(), variant, dtype, mfw, nf, lds);
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    const auto it = cache.find(key);
+    if (it != cache.end()) return it->second;
+  }
+  const int n = conv_resident(variant, dtype, mfw, nf, lds);
+  if (n <= 0) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  cache[key] = n;
+  return n;
+}
+
+// Resident workgroups per CU of the small-input-channel kernel chosen for
+// these arguments (cached like cached_resident).
+int cached_small_resident(const ConvArgs &a, int dtype, int mfw) {
+  static std::mutex mu;
+  static std::map<std::tuple<int, int, int, int, int, int, size_t>, int> cache;
+  const auto key = std::make_tuple(current_device(), dtype, mfw, a.steps_max > 4 ? 1 : 0,
+                                   a.hw * a.c_in <= 127 ? 1 : 0, a.res ? 1 : 0, small_lds_bytes(a));
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    const auto it = cache.find(key);
+    if (it != cache.end()) return it->second;
+  }
+  const int n = small_resident(a, dtype, mfw);
+  if (n <= 0) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  cache[key] = n;
+  return n;
 }
 
 Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint32_t variant, uint64_t ws_cap,
@@ -918,17 +1198,24 @@ Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint32_t variant, u
   //   bytes written and read back / kPartialBytesPerCycle),
   // with constants fitted to per-wave timestamps and per-layer traces of the
   // C3D and R(2+1)D layers on MI355X.
+  // LDS per workgroup as the launch requests it: split launches keep only
+  // the halo (partials are stored from registers); unsplit ones also reuse
+  // it as the epilogue tile of 16 * nf voxel slots x 64 * mfw filters.
   const size_t halo = static_cast<size_t>(tl.ht) * tl.hh * tl.hw * tl.row;
-  int per_cu = conv_resident(static_cast<int>(variant), d->dtype, p.mfw, tl.slots / 16, halo);
-  if (per_cu <= 0) {
-    (void)hipGetLastError();
-    per_cu = 2;
-  }
+  const size_t tile = static_cast<size_t>(tl.slots) * (static_cast<size_t>(L.wpw) * 16 * p.mfw * 4 + 16);
+  int per_cu_split = cached_resident(static_cast<int>(variant), d->dtype, p.mfw, tl.slots / 16, halo);
+  int per_cu_whole =
+      cached_resident(static_cast<int>(variant), d->dtype, p.mfw, tl.slots / 16, std::max(halo, tile));
+  if (per_cu_split <= 0) per_cu_split = 2;
+  if (per_cu_whole <= 0) per_cu_whole = per_cu_split;
   const long cus = device_cus();
   const long total_vox_ = static_cast<long>(g.n) * g.to * g.ho * g.wo;
   const double partial_bytes = 2.0 * static_cast<double>(total_vox_) * ((g.c_out + 3) / 4 * 4) * 4;
   constexpr double kFixed = 12000, kReduce = 9600, kShare = 0.2, kPartialBytesPerCycle = 4200;
-  const double step_cycles = p.mfw == 1 ? 380.0 : (p.mfw == 2 ? 555.0 : 815.0);
+  // Pair steps read twice the items of a union step (an estimate until
+  // measured per layer).
+  const double step_cycles = variant == kVarKgsPair16 ? 600.0
+                             : (p.mfw == 1 ? 380.0 : (p.mfw == 2 ? 555.0 : 815.0));
   const double chunk_steps = p.tile_steps > 0 ? static_cast<double>(p.tile_steps) / tl.nchunks : 24.0;
   // A chunk costs its K-steps, but no less than the exposed latency of its
   // halo load, plus the barriers and LDS commit around it.
@@ -939,6 +1226,7 @@ Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint32_t variant, u
   for (int s = 1; s <= tl.nchunks; ++s) {
     if (s > 1 && (tl.nchunks + s - 1) / s == (tl.nchunks + s - 2) / (s - 1)) continue;  // same chunks per WG
     const long n = wgs * s;
+    const long per_cu = s > 1 ? per_cu_split : per_cu_whole;
     const long per = std::min<long>((n + cus - 1) / cus, per_cu);          // workgroups per CU at once
     const long rounds = (n + cus * per - 1) / (cus * per);
     const double t = rounds * (kFixed + ((tl.nchunks + s - 1) / s) * chunk_cycles *
@@ -949,7 +1237,7 @@ Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint32_t variant, u
       splits = s;
     }
   }
-  if (const char *env = std::getenv("RT3D_SPLITS")) splits = std::max(1, std::min(tl.nchunks, std::atoi(env)));
+  if (tune("splits") > 0) splits = std::max(1, std::min(tl.nchunks, tune("splits")));
   const long total_vox = static_cast<long>(g.n) * g.to * g.ho * g.wo;
   const uint64_t per_split = static_cast<uint64_t>(total_vox) * ((g.c_out + 3) / 4 * 4) * 4;
   while (splits > 1 && per_split * splits > ws_cap) --splits;
@@ -961,7 +1249,7 @@ Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint32_t variant, u
                     xcd_fill_bytes(bricks, ntg, splits, 0, a_unit, x_unit)
                 ? 1
                 : 0;
-  if (const char *env = std::getenv("RT3D_WG_ORDER")) L.order = std::atoi(env) ? 1 : 0;
+  if (tune("wg_order") >= 0) L.order = tune("wg_order") ? 1 : 0;
   return L;
 }
 
@@ -1002,6 +1290,7 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   a.items = reinterpret_cast<const uint32_t *>(b + p.items_off);
   a.keep = reinterpret_cast<const uint32_t *>(b + p.keep_off);
   a.a = b + p.a_off;
+  a.a_bytes = static_cast<int32_t>(std::min<uint64_t>(info->packed_bytes - p.a_off, 0x7fffffffu));
   a.n = g.n; a.c_in = g.c_in; a.c_out = g.c_out; a.t = g.t; a.h = g.h; a.w = g.w;
   a.to = g.to; a.ho = g.ho; a.wo = g.wo;
   a.st = g.st; a.sh = g.sh; a.sw = g.sw; a.pt = g.pt; a.ph = g.ph; a.pw = g.pw;
@@ -1040,18 +1329,18 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   switch (info->variant) {
     case kVarDenseItems16:
     case kVarKgsUnion16:
-      e = launch_items16(a, d->dtype, p.mfw, stream);
+      e = launch_items16(a, d->dtype, p.mfw, false, stream);
+      break;
+    case kVarKgsPair16:
+      e = launch_items16(a, d->dtype, p.mfw, true, stream);
       break;
     case kVarSmallDense16:
     case kVarSmallKgs16: {
       // Waves walk (wave tile, brick) pairs: as many workgroups as fit
       // resident, with a wave count that is a multiple of the wave tiles.
       const long waves = static_cast<long>(a.nbricks) * a.wave_tiles;
-      int per_cu = small_resident(a, d->dtype, p.mfw);
-      if (per_cu <= 0) {
-        (void)hipGetLastError();
-        per_cu = 1;
-      }
+      int per_cu = cached_small_resident(a, d->dtype, p.mfw);
+      if (per_cu <= 0) per_cu = 1;
       long grid = std::min<long>((waves + 3) / 4, static_cast<long>(device_cus()) * per_cu);
       const long unit = a.wave_tiles / std::gcd(a.wave_tiles, 4);
       grid = std::max<long>(unit, grid / unit * unit);

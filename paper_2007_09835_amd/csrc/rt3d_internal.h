@@ -9,7 +9,7 @@
 namespace rt3d {
 
 constexpr uint64_t kMagic = 0x314b4e3344335452ull;  // "RT3D3NK1" little-endian
-constexpr uint32_t kVersion = 1;
+constexpr uint32_t kVersion = 2;
 constexpr uint64_t kAlign = 256;                    // section alignment in a blob
 
 // Kernel mappings (the `variant` field of rt3d_pack_info).
@@ -20,6 +20,8 @@ enum Variant : uint32_t {
   kVarKgsExactF32 = 4,   // KGS, 4x4x1 f32 MFMA, exact per 4x4 kernel block
   kVarSmallDense16 = 5,  // dense, c_in <= 4: wave-private bricks, weights in registers
   kVarSmallKgs16 = 6,    // KGS, c_in <= 4: as above over the union of the wave tile's items
+  kVarKgsPair16 = 7,     // KGS, 2:4 sparse 16x16x64 MFMA over pairs of items no group keeps
+                         // both of; compact weight stream (kept 4x4 blocks only)
 };
 
 // Voxel tiling shared by every conv kernel: a workgroup computes a brick of
@@ -47,7 +49,8 @@ struct Plan {
   uint64_t item_ptr_off;   // u32 [wave_tiles]
   uint64_t items_off;      // u32 [...] LDS byte offset of each item
   uint64_t a_off;          // dtype [...], MFMA operand order
-  uint64_t keep_off;       // u32 [...] (exact f32 variant: kept-group bits per item)
+  uint64_t keep_off;       // u32 [...] (exact f32 variant: kept-group bits per item;
+                           // pair variant: uint4 per step {keep, side, first block, 0})
 };
 static_assert(sizeof(Plan) <= sizeof(((rt3d_pack_info *)0)->plan), "plan does not fit");
 
@@ -86,6 +89,7 @@ struct ConvArgs {
   int32_t x_pitch;    // channels per voxel of x (>= c_in: a slice of a wider tensor)
   int32_t x_off;      // first channel of x this layer reads
   int32_t nf;         // 16-slot voxel fragments per wave (slots / 16)
+  int32_t a_bytes;    // bytes of the weight stream (pair variant: its buffer extent)
 };
 
 // Launch shape chosen at forward time from the batch size.
@@ -119,7 +123,7 @@ struct GroupArgs {
 // Workgroups of the conv kernel for (variant, dtype, mfw, nf) that fit on one CU
 // with `lds` bytes of dynamic LDS each; 0 when the runtime cannot say.
 int conv_resident(int variant, int dtype, int mfw, int nf, size_t lds);
-int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream);
+int launch_items16(const ConvArgs &a, int dtype, int mfw, bool pair, void *stream);
 int launch_small16(const ConvArgs &a, int dtype, int mfw, void *stream);
 size_t small_lds_bytes(const ConvArgs &a);
 int small_resident(const ConvArgs &a, int dtype, int mfw);

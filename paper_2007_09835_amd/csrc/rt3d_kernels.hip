@@ -30,6 +30,9 @@ namespace {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
+typedef __attribute__((__vector_size__(16 * sizeof(__bf16)))) __bf16 bf16x16;
+typedef __attribute__((__vector_size__(16 * sizeof(_Float16)))) _Float16 f16x16;
+typedef __attribute__((__vector_size__(8 * sizeof(unsigned)))) unsigned u32x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(4 * sizeof(unsigned)))) unsigned u32x4;
 
@@ -549,14 +552,38 @@ __device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, co
 // a range of channel chunks (split-K) when the layer alone cannot fill the
 // GPU.  Dense layers give every wave tile the
 // full item list (and MFW > 1 shares each B fragment across filter rows);
-// KGS layers give each 16-filter tile the union of the items its four kernel
-// groups keep, with the pruned entries of that union stored as zero weights.
+// KGS layers give each 16-filter tile either the union of the items its four
+// kernel groups keep, with the pruned entries of that union stored as zero
+// weights, or (PAIR) the pair mapping below.
+//
+// PAIR: v_smfmac_f32_16x16x64_{bf16,f16}, 2:4 structured-sparse A.  A K-step
+// is 8 pairs of items (64 reduction slots); the planner pairs two items only
+// when no kernel group of the tile keeps both, so in every quad of four
+// consecutive reduction slots a filter row has at most two nonzero weights,
+// and a step multiplies up to 16 items in the time of one dense 16x16x32
+// MFMA.  Reduction slots of pair j (items X, Y): quad 2j = (X.c0, X.c1, Y.c0,
+// Y.c1), quad 2j+1 = (X.c2, X.c3, Y.c2, Y.c3).  Lane layouts (measured on
+// gfx950): A (compressed, 8 values) lane m + 16*ga, element e -> quad
+// 4*ga + e/2, so lane group ga holds pairs 2ga and 2ga+1 of its filter row;
+// B lane n + 16*gb, element e -> slot 8*gb + e (e < 8) or 32 + 8*gb + e - 8,
+// so lane group gb reads pairs gb and gb+4 (four 8-byte LDS reads); the
+// 2-bit index of element e sits at bits 2e of the index register (ABID 0).
+// Weights stream compact: one 32-byte 4x4 block per kept (pair, group).  Per
+// step and (lane group, kernel group) the planner stores the byte offsets of
+// the blocks of the lane group's two pairs and their index register; a group
+// that keeps neither item of a pair gets an offset beyond the buffer's
+// extent, which loads zeros without touching memory, so pruned weights never
+// leave HBM.
 // ---------------------------------------------------------------------------
 
 // FAST: c_in is a multiple of 8 (branch-free halo staging).
-template <typename T, int MFW, int NF, bool FAST>
+template <typename T, int MFW, int NF, bool FAST, bool PAIR = false>
 __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
+  static_assert(!PAIR || MFW == 1, "the pair mapping uses 16-filter tiles");
   using V8 = std::conditional_t<std::is_same_v<T, __bf16>, bf16x8, f16x8>;
+  using V16 = std::conditional_t<std::is_same_v<T, __bf16>, bf16x16, f16x16>;
+  using BV = std::conditional_t<PAIR, V16, V8>;     // B fragment of one step
+  using OFF = std::conditional_t<PAIR, uint4, uint2>;  // LDS offsets of a lane group's items
   // Software pipeline of a wave (step t = one K-step of 8 items):
   //   item offsets for step t+4 and the A operand for step t+2 are in flight
   //   from global memory, and the B fragments of step t+1 are read from LDS,
@@ -590,24 +617,60 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
   const uint32_t step0 = uniform(sp[0]);
   const uint32_t row0 = uniform(a.item_ptr[active ? wt : 0]);
   const V8 *A = static_cast<const V8 *>(a.a) + lane;
-  const uint2 *IT = reinterpret_cast<const uint2 *>(a.items) + g;  // 4 uint2 per step
+  // Union / dense: 8 item offsets per step, lane group g reads 2 of them;
+  // PAIR: 16 per step, lane group g reads the items of pairs g and g + 4.
+  const OFF *IT = reinterpret_cast<const OFF *>(a.items) + g;
 
-  uint2 roff[4];
+  OFF roff[4];
   V8 ra[2][MFW];
-  V8 rb[2][NF];
+  BV rb[2][NF];
+  // PAIR only: step descriptors (keep word, side word, first block) ride
+  // with the offsets; each A slot carries its 2-bit index register.
+  uint4 rdesc[PAIR ? 4 : 1];
+  uint32_t ridx[2] = {0u, 0u};
+  const uint32_t row8 = (lane & 3) * 8u;           // this lane's filter row within a block
+  const __amdgpu_buffer_rsrc_t ares =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(a.a), 0, static_cast<int>(a.a_bytes), 0x00020000);
+  // PAIR: this lane's descriptor {block offset of pair 2g, of pair 2g + 1,
+  // index register, 0} of step s is entry 16 s + 4 g + (kernel group).
+  const uint4 *KD = reinterpret_cast<const uint4 *>(a.keep) + 4 * g + ((lane & 15) >> 2);
   auto fetch_off = [&](int slot, uint32_t s) {
     roff[slot] = IT[(static_cast<long>(row0) + (s - step0)) * 4];
+    if constexpr (PAIR) rdesc[slot] = KD[static_cast<long>(s) * 16];
   };
-  auto fetch_a = [&](int slot, uint32_t s) {
-    #pragma unroll
-    for (int i = 0; i < MFW; ++i) ra[slot][i] = A[(static_cast<long>(s) * MFW + i) * 64];
+  // dslot: the offsets-ring slot that holds step s's descriptor (PAIR).
+  auto fetch_a = [&](int slot, uint32_t s, int dslot) {
+    if constexpr (PAIR) {
+      // This lane's filter row of the two blocks (offsets >= 2^31 read zeros).
+      const uint4 d = rdesc[dslot];
+      const uint2 lo = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(ares, static_cast<int>(d.x + row8), 0, 0));
+      const uint2 hi = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(ares, static_cast<int>(d.y + row8), 0, 0));
+      ra[slot][0] = __builtin_bit_cast(V8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+      ridx[slot] = d.z;
+    } else {
+      (void)dslot;
+      #pragma unroll
+      for (int i = 0; i < MFW; ++i) ra[slot][i] = A[(static_cast<long>(s) * MFW + i) * 64];
+    }
   };
-  auto load_b = [&](int slot, uint2 off) {
+  auto load_b = [&](int slot, OFF off) {
     #pragma unroll
     for (int j = 0; j < NF; ++j) {
-      const uint2 lo = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.x);
-      const uint2 hi = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.y);
-      rb[slot][j] = __builtin_bit_cast(V8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+      if constexpr (PAIR) {
+        // Operand order (X.c01, Y.c01, X.c23, Y.c23) per pair.  Two 8-byte
+        // reads per pair and register moves to interleave them: LDS time
+        // follows the number of read instructions more than their width, and
+        // four 4-byte reads per pair measured about twice as slow.
+        const uint2 x0 = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.x);
+        const uint2 y0 = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.y);
+        const uint2 x1 = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.z);
+        const uint2 y1 = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.w);
+        rb[slot][j] = __builtin_bit_cast(V16, u32x8{x0.x, y0.x, x0.y, y0.y, x1.x, y1.x, x1.y, y1.y});
+      } else {
+        const uint2 lo = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.x);
+        const uint2 hi = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.y);
+        rb[slot][j] = __builtin_bit_cast(V8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+      }
     }
   };
   auto mma = [&](int slot) {
@@ -615,10 +678,18 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
     for (int j = 0; j < NF; ++j)
       #pragma unroll
       for (int i = 0; i < MFW; ++i) {
-        if constexpr (std::is_same_v<T, __bf16>)
+        if constexpr (PAIR) {
+          if constexpr (std::is_same_v<T, __bf16>)
+            acc[i][j] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(ra[slot][i], rb[slot][j], acc[i][j],
+                                                                   static_cast<int>(ridx[slot]), 0, 0);
+          else
+            acc[i][j] = __builtin_amdgcn_smfmac_f32_16x16x64_f16(ra[slot][i], rb[slot][j], acc[i][j],
+                                                                  static_cast<int>(ridx[slot]), 0, 0);
+        } else if constexpr (std::is_same_v<T, __bf16>) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ra[slot][i], rb[slot][j], acc[i][j], 0, 0, 0);
-        else
+        } else {
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ra[slot][i], rb[slot][j], acc[i][j], 0, 0, 0);
+        }
       }
   };
 
@@ -639,7 +710,7 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
 #pragma unroll
     for (int d = 0; d < 4; ++d) fetch_off(d, min(S0 + d, LAST));
 #pragma unroll
-    for (int d = 0; d < 2; ++d) fetch_a(d, min(S0 + d, LAST));
+    for (int d = 0; d < 2; ++d) fetch_a(d, min(S0 + d, LAST), d);
   }
   for (int ch = ch0; ch < ch1; ++ch) {
     __syncthreads();  // every wave is done with the previous chunk
@@ -659,7 +730,7 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
         constexpr int D = decltype(dc)::value;
         load_b((D + 1) & 1, roff[(D + 1) & 3]);
         mma(D & 1);
-        fetch_a(D & 1, min(s + D + 2, LAST));
+        fetch_a(D & 1, min(s + D + 2, LAST), (D + 2) & 3);
         fetch_off(D, min(s + D + 4, LAST));
         // Keep the stages in place: without this fence the scheduler sinks
         // the prefetches next to their uses two steps later.
@@ -672,20 +743,15 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
       if (D < rem) {
         if (D + 1 < rem) load_b((D + 1) & 1, roff[(D + 1) & 3]);
         mma(D & 1);
-        fetch_a(D & 1, min(s + D + 2, LAST));
+        fetch_a(D & 1, min(s + D + 2, LAST), (D + 2) & 3);
         fetch_off(D, min(s + D + 4, LAST));
       }
     });
     // The rings now hold steps s_end.. at slots (n + k) & 3 and (n + k) & 1
     // (n = steps of this chunk): rotate them to slot 0 for the next chunk.
     const uint32_t n = s_end - s_beg;
-    const uint2 o0 = roff[0], o1 = roff[1], o2 = roff[2], o3 = roff[3];
-    switch (n & 3) {
-      case 1: roff[0] = o1; roff[1] = o2; roff[2] = o3; roff[3] = o0; break;
-      case 2: roff[0] = o2; roff[1] = o3; roff[2] = o0; roff[3] = o1; break;
-      case 3: roff[0] = o3; roff[1] = o0; roff[2] = o1; roff[3] = o2; break;
-      default: break;
-    }
+    rotate_ring(roff, static_cast<int>(n & 3));
+    if constexpr (PAIR) rotate_ring(rdesc, static_cast<int>(n & 3));
     if (n & 1) {
 #pragma unroll
       for (int i = 0; i < MFW; ++i) {
@@ -693,6 +759,9 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
         ra[0][i] = ra[1][i];
         ra[1][i] = t;
       }
+      const uint32_t ti = ridx[0];
+      ridx[0] = ridx[1];
+      ridx[1] = ti;
     }
   }
   if (a.splits > 1) {
@@ -1786,6 +1855,10 @@ int conv_resident(int variant, int dtype, int mfw, int nf, size_t lds) {
       else RT3D_RES16(_Float16);
 #undef RT3D_RES16
       return 0;
+    case kVarKgsPair16:
+      if (mfw != 1 || nf != 4) return 0;
+      if (dtype == RT3D_BF16) return resident(items16_kernel<__bf16, 1, 4, true, true>, lds);
+      return resident(items16_kernel<_Float16, 1, 4, true, true>, lds);
     case kVarDenseItemsF32:
       if (nf == 4) {
         if (mfw == 1) return resident(items_f32_kernel<1, 4>, lds);
@@ -1859,8 +1932,22 @@ int small_resident(const ConvArgs &a, int dtype, int mfw) {
   return 0;
 }
 
-int launch_items16(const ConvArgs &a, int dtype, int mfw, void *stream) {
+int launch_items16(const ConvArgs &a, int dtype, int mfw, bool pair, void *stream) {
   const bool fast = a.c_in % 8 == 0 && a.x_pitch % 8 == 0 && a.x_off % 8 == 0;
+  if (pair) {
+    // 64-slot bricks only: with eight fragments the doubled B ring would
+    // leave one wave per SIMD.
+    if (mfw != 1 || a.nf != 4) return hipErrorInvalidValue;
+#define RT3D_PAIR16(T)                                                                   \
+  do {                                                                                   \
+    return fast ? launch_conv(items16_kernel<T, 1, 4, true, true>, a, stream)            \
+                : launch_conv(items16_kernel<T, 1, 4, false, true>, a, stream);          \
+  } while (0)
+    if (dtype == RT3D_BF16) RT3D_PAIR16(__bf16);
+    if (dtype == RT3D_F16) RT3D_PAIR16(_Float16);
+#undef RT3D_PAIR16
+    return hipErrorInvalidValue;
+  }
 #define RT3D_ITEMS16(T, M)                                                         \
   do {                                                                             \
     if (a.nf == 4)                                                                 \

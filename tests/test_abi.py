@@ -154,9 +154,9 @@ def test_brick_width_follows_the_layer_size(monkeypatch):
     """64-slot bricks when 128-slot bricks times 16-filter tiles give fewer
     than 1024 waves (one per SIMD of the GPU) for pooled 16-bit layers, 8192
     for unpooled 16-bit layers (their narrow-tile epilogue runs in
-    registers) and 256 for fp32; larger layers keep 128; RT3D_SLOTS
+    registers) and 256 for fp32; larger layers keep 128; RT3D_TUNE=slots=N
     overrides the choice at pack time."""
-    monkeypatch.delenv("RT3D_SLOTS", raising=False)
+    monkeypatch.delenv("RT3D_TUNE", raising=False)
     pooled_big = rt3d.make_desc(1, 64, 128, (16, 56, 56), dtype="bf16", pool=(2, 2, 2))  # 3136
     pooled_small = rt3d.make_desc(1, 256, 256, (8, 28, 28), dtype="bf16", pool=(2, 2, 2))  # 784
     unpooled = rt3d.make_desc(1, 64, 128, (16, 56, 56), dtype="bf16")       # 3136 waves
@@ -169,10 +169,10 @@ def test_brick_width_follows_the_layer_size(monkeypatch):
     assert _brick_slots(unpooled_big) == 128
     assert _brick_slots(f32) == 128
     assert _brick_slots(f32_small) == 64
-    monkeypatch.setenv("RT3D_SLOTS", "128")
+    monkeypatch.setenv("RT3D_TUNE", "slots=128")
     assert _brick_slots(pooled_small) == 128
     assert _brick_slots(f32_small) == 128
-    monkeypatch.setenv("RT3D_SLOTS", "64")
+    monkeypatch.setenv("RT3D_TUNE", "slots=64")
     assert _brick_slots(pooled_big) == 64
     assert _brick_slots(f32) == 64
 
@@ -181,9 +181,10 @@ def test_kgs_tile_width_follows_union_size(monkeypatch):
     """KGS layers with 256+ filters and a 64-filter wave per SIMD walk the
     union of 16 kernel groups (64-filter tiles) when the 16-filter union
     already covers most items; sparser masks and batch-1 layers keep
-    16-filter tiles.  Plan fields: mfw is the eleventh int32."""
-    monkeypatch.delenv("RT3D_KGS_MFW", raising=False)
-    monkeypatch.delenv("RT3D_SLOTS", raising=False)
+    16-filter tiles.  Plan fields: mfw is the eleventh int32.  (Checked with
+    the union mapping forced: the planner prefers the pair mapping wherever
+    it saves K-steps and the union would use narrow tiles.)"""
+    monkeypatch.setenv("RT3D_TUNE", "kgs_map=0")
     rng = np.random.default_rng(3)
     w = _weights(rng, (256, 256, 3, 3, 3), "bf16")
 

@@ -12,7 +12,8 @@ import pytest
 import torch
 
 import oracle
-from harness import TOL, LayerCase, from_device_ndhwc, rel_l2, rounded, sample_indices, to_device_ndhwc
+from harness import (TOL, LayerCase, assert_within_bound, error_bound, from_device_ndhwc,
+                     kept_terms_per_filter, rel_l2, rounded, sample_indices, to_device_ndhwc)
 from paper_2007_09835_amd import build, layers, synth
 
 pytestmark = pytest.mark.gpu
@@ -29,22 +30,27 @@ def masked(tag, c_out, c_in, k, keep, g=(4, 4)):
 
 
 def check_full(case, label):
+    """relL2 against the bar, and every output within its own bound
+    (harness.error_bound: rounding + float32 accumulation)."""
     got = case.run_gpu()
     ref = case.oracle_full()
     err = rel_l2(got, ref)
     print(f"{label}: relL2={err:.3e} maxabs={np.abs(got - ref).max():.3e}", flush=True)
     assert got.shape == ref.shape
     assert err <= TOL[case.dtype], (label, err)
+    assert_within_bound(got, ref, case.bound_full(ref), label)
     return got, ref
 
 
 def check_sampled(case, label, count=3000):
     got = case.run_gpu()
+    assert case.pool == (1, 1, 1)
     idx = sample_indices(got.shape, count)
     ref = case.oracle_points(idx)
     err = rel_l2(got.ravel()[idx], ref)
     print(f"{label}: sampled relL2={err:.3e} ({len(idx)} outputs)", flush=True)
     assert err <= TOL[case.dtype], (label, err)
+    assert_within_bound(got.ravel()[idx], ref, case.bound_points(idx, ref), label)
     return got
 
 
@@ -99,7 +105,7 @@ def test_both_brick_widths(si, sparse, slots, dtype, monkeypatch):
     """The item kernels with 64- and 128-slot bricks (16-bit: 4 or 8 voxel
     fragments per wave; exact fp32 KGS: one or two slots per lane) on the
     same layers."""
-    monkeypatch.setenv("RT3D_SLOTS", slots)
+    monkeypatch.setenv("RT3D_TUNE", "slots=" + slots)
     tag, n, c_in, c_out, thw, k, stride, pad, keep = SHAPES[si]
     mask = masked(tag, c_out, c_in, k, min(keep, k[0] * k[1] * k[2])) if sparse else None
     case = LayerCase(tag + "w" + slots, n, c_in, c_out, thw, k, stride, pad, dtype, mask)
@@ -358,12 +364,14 @@ def test_fused_concatenation_writes_only_its_slice(dtype):
         case = LayerCase(tag, n, c_in, c_out, thw, k, (1, 1, 1), pad, dtype, mask)
         case.x_t, case.x64 = x_t, x_ref
         case.conv(x, out=y, c_off=off)
-        refs.append((off, c_out, case.oracle_full()))
+        ref = case.oracle_full()
+        refs.append((off, c_out, ref, case.bound_full(ref)))
     torch.cuda.synchronize()
     got = from_device_ndhwc(y)
     owned = np.zeros(c_total, bool)
-    for off, c_out, ref in refs:
+    for off, c_out, ref, bound in refs:
         assert rel_l2(got[:, off:off + c_out], ref) <= TOL[dtype]
+        assert_within_bound(got[:, off:off + c_out], ref, bound, f"slice {off}")
         owned[off:off + c_out] = True
     assert np.all(got[:, ~owned] == -7.0)
 
@@ -437,9 +445,10 @@ def test_c3d_batch32_layers(variant, li):
 # S3D-shaped stack: Inception blocks (fused concatenation), padded pools
 # ---------------------------------------------------------------------------
 
-def _s3d_oracle_op(op, stack, src64, layer_by_name):
+def _s3d_oracle_op(op, stack, src64, layer_by_name, absolute=False):
     """float64 result of one op of the S3D stack on the float64 input src64
-    ([n][c][t][h][w]); a conv returns its c_out channels."""
+    ([n][c][t][h][w]); a conv returns its c_out channels.  absolute: the
+    conv of |x|, |w| plus |bias| without activation (the error bound's sum)."""
     if op[0] == "pool":
         _, _, _, k, st, pd = op
         return oracle.maxpool3d(src64, k, st, pd)
@@ -449,10 +458,13 @@ def _s3d_oracle_op(op, stack, src64, layer_by_name):
     d = synth.layer_params("s3d", l)
     w64 = synth.to_dtype(d.w, stack.dtype).double().numpy()
     b64 = d.bias.astype(np.float32).astype(np.float64)
+    relu = l.relu
+    if absolute:
+        src64, w64, b64, relu = np.abs(src64), np.abs(w64), np.abs(b64), False
     mask = stack.masks[i]
     if mask is None:
-        return oracle.conv3d_dense(src64, w64, b64, None, l.stride, l.pad, l.relu)
-    return oracle.conv3d_kgs(src64, w64, mask, *l.g, b64, None, l.stride, l.pad, l.relu)
+        return oracle.conv3d_dense(src64, w64, b64, None, l.stride, l.pad, relu)
+    return oracle.conv3d_kgs(src64, w64, mask, *l.g, b64, None, l.stride, l.pad, relu)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -477,9 +489,14 @@ def test_s3d_small_clip_every_op(dtype):
         if op[0] == "pool":
             assert np.array_equal(host[dst], ref), op
         else:
-            off, c_out = op[4], layer_by_name[op[1]][1].c_out
+            i, l = layer_by_name[op[1]]
+            off, c_out = op[4], l.c_out
             err = rel_l2(host[dst][:, off:off + c_out], ref)
             assert err <= TOL[dtype], (op, err)
+            s_abs = _s3d_oracle_op(op, st, host[src], layer_by_name, absolute=True)
+            kt = kept_terms_per_filter(st.masks[i], l.g, l.c_in, l.ks, l.c_out)[None, :, None, None, None]
+            assert_within_bound(host[dst][:, off:off + c_out], ref,
+                                error_bound(ref, s_abs, kt, dtype), f"s3d small {op[1]}")
         if dtype == "f32":
             full = _s3d_oracle_op(op, st, chain[src], layer_by_name)
             if op[0] == "pool":
@@ -506,3 +523,57 @@ def test_s3d_layers_full_size(li):
     case = LayerCase("s3d-" + l.name, 1, l.c_in, l.c_out, (l.t, l.h, l.w), l.k, l.stride, l.pad,
                      "bf16", mask, x_kind="uniform01" if li == 0 else "halfnormal")
     check_sampled(case, f"s3d {l.name}")
+
+
+# ---------------------------------------------------------------------------
+# Pair mapping (2:4 sparse MFMA over pairs of items that no kernel group of a
+# 16-filter tile keeps both of; compact weight stream).  Not the planner's
+# default, so it is forced through the tuning switch.
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("si", range(len(SHAPES)))
+def test_pair_mapping_small_shapes(si, dtype, monkeypatch):
+    monkeypatch.setenv("RT3D_TUNE", "kgs_map=1")
+    tag, n, c_in, c_out, thw, k, stride, pad, keep = SHAPES[si]
+    mask = masked(tag, c_out, c_in, k, min(keep, k[0] * k[1] * k[2]))
+    case = LayerCase(tag + "p", n, c_in, c_out, thw, k, stride, pad, dtype, mask)
+    if c_in > 4:
+        assert case.conv.info.variant == 7
+    check_full(case, f"pairs {tag} {dtype}")
+
+
+@pytest.mark.parametrize("pi", [0, 1, 4, 7, 8])
+def test_pair_mapping_pooled_and_split(pi, monkeypatch):
+    monkeypatch.setenv("RT3D_TUNE", "kgs_map=1")
+    tag, n, c_in, c_out, thw, pool, dtype, sparse, residual = POOLED[pi]
+    mask = masked(tag, c_out, c_in, (3, 3, 3), 9)
+    case = LayerCase(tag + "p", n, c_in, c_out, thw, (3, 3, 3), (1, 1, 1), (1, 1, 1),
+                     "bf16" if dtype == "f32" else dtype, mask, residual=residual, pool=pool)
+    assert case.conv.info.variant == 7
+    check_full(case, f"pairs pooled {tag}")
+
+
+@pytest.mark.parametrize("gi", [1, 3, 4])
+def test_pair_mapping_group_sizes(gi, monkeypatch):
+    monkeypatch.setenv("RT3D_TUNE", "kgs_map=1")
+    tag, n, c_in, c_out, thw, k, stride, pad, g, keep = GROUPED[gi]
+    mask = masked(tag, c_out, c_in, k, keep, g)
+    case = LayerCase(tag + "p", n, c_in, c_out, thw, k, stride, pad, "bf16", mask, g=g)
+    check_full(case, f"pairs {tag} g={g}")
+
+
+@pytest.mark.parametrize("variant", ["kgs3", "vanilla3"])
+@pytest.mark.parametrize("li", [1, 3, 6])
+def test_pair_mapping_c3d_layers(li, variant, monkeypatch):
+    """Full-size C3D layers at batch 1 on the pair mapping, sampled outputs."""
+    monkeypatch.setenv("RT3D_TUNE", "kgs_map=1")
+    stack = synth.c3d_stack(3.0)
+    l = stack[li]
+    r = synth.rng_for("c3d-pair", variant, l.name, "mask")
+    mask = (synth.vanilla_mask(r, *l.groups, l.ks, 3.0) if variant == "vanilla3"
+            else synth.kgs_mask(r, *l.groups, l.ks, l.keep))
+    case = LayerCase(f"pair-{variant}-{l.name}", 1, l.c_in, l.c_out, (l.t, l.h, l.w), l.k,
+                     l.stride, l.pad, "bf16", mask)
+    assert case.conv.info.variant == 7
+    check_sampled(case, f"pairs c3d {variant} {l.name}", count=2000)

@@ -152,7 +152,7 @@ def test_penalty_defaults_update_and_mask():
     b = oracle.group_reweight(w, 4, 4, norm=2, scope=0, pen=np.ones((2, 1, 27)), lam=0.7,
                               eps=1e-3, tau=1.5)
     assert a["reg"] == b["reg"]
-    # with unit penalty factors eq. (4) is the plain group lasso of eq. (3)
+    # with unit penalty factors eq. (3) is the plain group lasso of eq. (2)
     assert a["reg"] == pytest.approx(0.7 * a["norms"].sum(), rel=1e-14)
     assert a["pen_next"][1, 0, 0] == 1.0 / 1e-3
     assert np.array_equal(a["mask"], (a["norms"] > 1.5).astype(np.uint8))
