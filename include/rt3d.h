@@ -209,6 +209,26 @@ rt3d_status rt3d_kgs_conv3d_fwd(const rt3d_conv3d_desc *desc, const rt3d_pack_in
                                 const void *residual, void *y,
                                 void *workspace, uint64_t workspace_bytes, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the KGS
+ * forward of rt3d_kgs_conv3d_fwd without a caller workspace.  Its split-K
+ * partial sums go to the library's own device array of RT3D_NOALLOC_SCRATCH
+ * bytes (32 MiB, held by every GPU the library runs on until the process
+ * ends); the call allocates nothing.  The launch is the one
+ * rt3d_kgs_conv3d_fwd makes with a workspace of at least
+ * rt3d_conv3d_workspace_size bytes, so the results are identical.  A layer
+ * whose split-K workspace at desc->n exceeds RT3D_NOALLOC_SCRATCH bytes is
+ * rejected with RT3D_ERR_UNSUPPORTED before anything is launched (call
+ * rt3d_kgs_conv3d_fwd with a workspace instead).  Every call on a GPU shares
+ * that GPU's array: calls that overlap in time on one GPU (other streams,
+ * other threads) race and must not be made; consecutive calls on one stream
+ * are safe (each writes every partial sum it reads, so nothing needs to
+ * start at zero).  Other arguments and errors as rt3d_kgs_conv3d_fwd. */
+#define RT3D_NOALLOC_SCRATCH (32u << 20)
+rt3d_status rt3d_kgs_conv3d_fwd_noalloc(const rt3d_conv3d_desc *desc, const rt3d_pack_info *info,
+                                        const void *blob_dev, const void *x, const float *bias,
+                                        const void *residual, void *y, void *stream);
+
 /* Bytes of the dense blob.  Host only. */
 rt3d_status rt3d_dense_pack_size(const rt3d_conv3d_desc *desc, uint64_t *bytes);
 

@@ -1554,6 +1554,32 @@ rt3d_status rt3d_kgs_conv3d_fwd(const rt3d_conv3d_desc *d, const rt3d_pack_info 
   return run_conv(d, info, blob_dev, x, bias, residual, y, workspace, workspace_bytes, stream, true);
 }
 
+rt3d_status rt3d_kgs_conv3d_fwd_noalloc(const rt3d_conv3d_desc *d, const rt3d_pack_info *info,
+                                        const void *blob_dev, const void *x, const float *bias,
+                                        const void *residual, void *y, void *stream) {
+  rt3d_status st = check_desc(d, true);
+  if (st != RT3D_OK) return st;
+  st = check_info(d, info, true);
+  if (st != RT3D_OK) return st;
+  if (d->n == 0) return ok();
+  Plan p;
+  std::memcpy(&p, info->plan, sizeof(p));
+  // The split count a caller workspace of any size would get: the launch is
+  // then the one rt3d_kgs_conv3d_fwd makes with that workspace.
+  const uint64_t need = plan_launch(d, p, info->variant, UINT64_MAX, info->packed_bytes - p.a_off).ws_bytes;
+  if (need > kScratchBytes)
+    return fail(RT3D_ERR_UNSUPPORTED,
+                "this launch needs %llu bytes of split-K scratch; the no-allocation entry point "
+                "holds %llu (use rt3d_kgs_conv3d_fwd with a caller workspace)",
+                static_cast<unsigned long long>(need), static_cast<unsigned long long>(kScratchBytes));
+  void *ws = nullptr;
+  if (need > 0) {
+    ws = noalloc_scratch();
+    if (!ws) return fail(RT3D_ERR_HIP, "the device address of the library's scratch is unavailable");
+  }
+  return run_conv(d, info, blob_dev, x, bias, residual, y, ws, need, stream, true);
+}
+
 rt3d_status rt3d_dense_pack_size(const rt3d_conv3d_desc *d, uint64_t *bytes) {
   rt3d_status st = check_desc(d, false);
   if (st != RT3D_OK) return st;

@@ -119,6 +119,11 @@ struct GroupArgs {
   float lambda, eps, tau, step;
 };
 
+// Bytes of the library's own split-K scratch (the no-allocation forward).
+constexpr uint64_t kScratchBytes = 32ull << 20;
+// Device address of the current device's scratch, NULL if it cannot be found.
+void *noalloc_scratch();
+
 // Kernel launchers (rt3d_kernels.hip).  Return hipSuccess or the launch error.
 // Workgroups of the conv kernel for (variant, dtype, mfw, nf) that fit on one CU
 // with `lds` bytes of dynamic LDS each; 0 when the runtime cannot say.

@@ -19,6 +19,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 
 #include <type_traits>
 #include <utility>
@@ -1833,7 +1834,37 @@ int resident(K kernel, size_t lds) {
   return n;
 }
 
+// Split-K scratch of the no-allocation forward entry point: every GPU the
+// library runs on holds one copy for the life of the process.
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
 }  // namespace
+
+// Device address of this device's copy of `scratch`, looked up once per
+// device with that device current (in host code the array's name is only a
+// stand-in, never a device address).  NULL when the lookup fails.
+void *noalloc_scratch() {
+  constexpr int kMaxDev = 64;
+  static std::mutex mu;
+  static void *ptr[kMaxDev] = {};
+  static bool looked[kMaxDev] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!looked[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) == hipSuccess) {
+      ptr[dev] = p;
+      looked[dev] = true;
+    } else {
+      (void)hipGetLastError();
+    }
+  }
+  return ptr[dev];
+}
 
 int conv_resident(int variant, int dtype, int mfw, int nf, size_t lds) {
   switch (variant) {

@@ -37,7 +37,7 @@ DTYPE_CODES = {"f32": RT3D_F32, "bf16": RT3D_BF16, "f16": RT3D_F16}
 EXPORTED = (
     "rt3d_status_string", "rt3d_last_error_detail", "rt3d_conv3d_out_shape",
     "rt3d_kgs_pack_size", "rt3d_kgs_pack", "rt3d_kgs_unpack", "rt3d_conv3d_workspace_size",
-    "rt3d_kgs_conv3d_fwd", "rt3d_dense_pack_size", "rt3d_dense_pack", "rt3d_conv3d_dense_fwd",
+    "rt3d_kgs_conv3d_fwd", "rt3d_kgs_conv3d_fwd_noalloc", "rt3d_dense_pack_size", "rt3d_dense_pack", "rt3d_conv3d_dense_fwd",
     "rt3d_maxpool3d_fwd", "rt3d_group_units", "rt3d_group_workspace_size", "rt3d_group_reweight",
 )
 
@@ -104,6 +104,7 @@ def load():
         "rt3d_kgs_unpack": ([D, I, vp, vp], ctypes.c_int),
         "rt3d_conv3d_workspace_size": ([D, I, P(u64)], ctypes.c_int),
         "rt3d_kgs_conv3d_fwd": ([D, I, vp, vp, vp, vp, vp, vp, u64, vp], ctypes.c_int),
+        "rt3d_kgs_conv3d_fwd_noalloc": ([D, I, vp, vp, vp, vp, vp, vp], ctypes.c_int),
         "rt3d_dense_pack_size": ([D, P(u64)], ctypes.c_int),
         "rt3d_dense_pack": ([D, vp, vp, u64, I], ctypes.c_int),
         "rt3d_conv3d_dense_fwd": ([D, I, vp, vp, vp, vp, vp, vp, u64, vp], ctypes.c_int),
@@ -232,6 +233,15 @@ def rt3d_kgs_conv3d_fwd(desc: Conv3dDesc, info: PackInfo, blob_dev, x, bias, res
         ctypes.byref(desc), ctypes.byref(info), _dev_ptr(blob_dev, "blob"), _dev_ptr(x, "x"),
         _dev_ptr(bias, "bias"), _dev_ptr(residual, "residual"), _dev_ptr(y, "y"),
         _dev_ptr(workspace, "workspace"), ws_bytes, _stream_ptr(stream)))
+
+
+def rt3d_kgs_conv3d_fwd_noalloc(desc: Conv3dDesc, info: PackInfo, blob_dev, x, bias, residual, y,
+                                stream=None) -> None:
+    """KGS forward whose split-K scratch is the library's own device array."""
+    _check(load().rt3d_kgs_conv3d_fwd_noalloc(
+        ctypes.byref(desc), ctypes.byref(info), _dev_ptr(blob_dev, "blob"), _dev_ptr(x, "x"),
+        _dev_ptr(bias, "bias"), _dev_ptr(residual, "residual"), _dev_ptr(y, "y"),
+        _stream_ptr(stream)))
 
 
 def rt3d_dense_pack_size(desc: Conv3dDesc) -> int:
