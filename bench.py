@@ -36,7 +36,9 @@ def parse():
     p.add_argument("--dtype", default="bf16", choices=["bf16", "f16", "f32"])
     p.add_argument("--rate", type=float, default=None,
                    help="whole-stack MAC pruning rate (KGS); default 3 (C3D) or 2.1 (S3D)")
-    p.add_argument("--mode", default="kgs", choices=["kgs", "vanilla"])
+    p.add_argument("--mode", default="kgs", choices=["kgs", "vanilla", "dense"],
+                   help="masks of the sparse stack (dense: every layer on the dense kernel; "
+                        "profiling modes only)")
     p.add_argument("--group", default="4x4", help="kernel group size g_MxG_N of the masks")
     p.add_argument("--no-graph", action="store_true", help="launch eagerly instead of a HIP graph")
     p.add_argument("--clock-warmup", type=float, default=0.5, metavar="SECONDS",
@@ -613,6 +615,8 @@ def main():
     if args.profile_layer:
         profile_layer(args, torch, stream)
         return
+    if args.mode == "dense":
+        sys.exit("--mode dense selects the profiled stack; the benchmark always times both")
     if args.profile_reweight:
         layer = next(l for l in synth.c3d_layers() if l.name == args.profile_reweight)
         r = reweight_layer(torch, layer, "bf16", True)

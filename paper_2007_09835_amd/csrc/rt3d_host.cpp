@@ -559,42 +559,61 @@ int kgs_tile_width(const Geom &g, const Tiling &tl, const Mask4 *m4) {
   return wide < 1.4 * narrow ? 4 : 1;
 }
 
+// Filter rows (of 16) per wave tile of the item kernels, then the brick.
+//
+// Dense layers share every B fragment across the wave's rows, KGS layers walk
+// the union of the tile's kernel groups' items (kgs_tile_width).  Dense: 64
+// filters (4 rows) for layers of 256+ filters with >= 2000 output voxels,
+// else 32; 16 for layers below 128 filters.  Layers of 128-255 filters take
+// 32-filter tiles, dense or KGS, when that still leaves 2048 waves (two per
+// SIMD): C3D conv2 at batch 1 dense 45.6 -> 38.7 us, KGS 40.9 -> 37.2 us, at
+// batch 32 1022 -> 893 and 916 -> 847 us.  A wave tile of two or more rows
+// runs on 64-slot bricks: on 128-slot bricks its accumulators and B ring
+// exceed 256 registers and leave one wave per SIMD (16-bit; batch-32 conv3a/3b/4b
+// 408/632/338 -> 350/597/309 us KGS, dense 410/643/340 -> 359/648/326 us).
+// Tuning switches dense_mfw, kgs_mfw and small_mfw override the width.
+struct ItemPlan {
+  Tiling tl;
+  int mfw;
+};
+
+ItemPlan item_plan(const Geom &g, const Mask4 *m4, bool small) {
+  ItemPlan ip{layer_tiling(g), 1};
+  const bool dense = m4 == nullptr;
+  if (small) {
+    // Up to 32 filters per wave: wider tiles hold 4x the weights in
+    // registers and drop residency to one wave per SIMD.
+    ip.mfw = g.c_out > 16 ? 2 : 1;
+    const int v = tune("small_mfw");
+    if (v == 1 || v == 2) ip.mfw = v;
+    return ip;
+  }
+  const long voxels = static_cast<long>(std::max(g.n, 1)) * g.to * g.ho * g.wo;
+  const bool mid = g.es == 2 && g.c_out >= 128 && g.c_out < 256 &&
+                   (voxels + 63) / 64 * ((g.c_out + 31) / 32) >= 2048;
+  if (dense) {
+    if (g.c_out >= 256) ip.mfw = voxels >= 2000 ? 4 : 2;
+    else if (mid) ip.mfw = 2;
+    const int v = tune("dense_mfw");
+    if (v == 1 || v == 2 || v == 4) ip.mfw = v;
+  } else {
+    ip.mfw = mid ? 2 : kgs_tile_width(g, ip.tl, m4);
+    const int v = tune("kgs_mfw");
+    if (v == 1 || v == 2 || v == 4) ip.mfw = v;
+  }
+  if (g.es == 2 && ip.mfw >= 2 && ip.tl.slots == 128 && tune("slots") != 128)
+    ip.tl = choose_tiling(g, 64);
+  return ip;
+}
+
 // 16-bit MFMA item layout (variants kVarDenseItems16, kVarKgsUnion16) and
 // the f32 16x16x4 dense layout (kVarDenseItemsF32).
 void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const Mask4 *m4,
-                        Layout &L, bool small = false) {
+                        Layout &L, bool small, int mfw) {
   const bool f32 = g.es == 4;
   const int ips = f32 ? 4 : 8;           // items per K-step
   const int epl = f32 ? 4 : 8;           // operand elements per lane
   const bool dense = m4 == nullptr;
-  // Dense layers share every B fragment across the wave's filter rows: use
-  // the widest wave tile that still leaves four wave tiles per workgroup.
-  // Dense wave-tile width (16*mfw filters sharing each B fragment): wider
-  // tiles cut LDS traffic but need c_out >= 64*mfw to keep four waves busy
-  // and enough voxels to keep the GPU filled without deep channel splits.
-  // Measured on MI355X over the C3D layers: 1 below 256 filters, 4 for wide
-  // layers with >= 2000 output voxels per launch, 2 otherwise.
-  int mfw = 1;
-  if (dense && g.c_out >= 256) {
-    const long voxels = static_cast<long>(std::max(g.n, 1)) * g.to * g.ho * g.wo;
-    mfw = voxels >= 2000 ? 4 : 2;
-  }
-  if (dense) {
-    // Tuning switch dense_mfw=1|2|4.
-    const int v = tune("dense_mfw");
-    if (v == 1 || v == 2 || v == 4) mfw = v;
-  } else if (!small) {
-    mfw = kgs_tile_width(g, tl, m4);
-    const int v = tune("kgs_mfw");
-    if (v == 1 || v == 2 || v == 4) mfw = v;
-  }
-  if (small) {
-    // Up to 32 filters per wave: wider tiles hold 4x the weights in
-    // registers and drop residency to one wave per SIMD.
-    mfw = g.c_out > 16 ? 2 : 1;
-    const int v = tune("small_mfw");
-    if (v == 1 || v == 2) mfw = v;
-  }
   const int wt_count = (g.c_out + 16 * mfw - 1) / (16 * mfw);
   L.variant = small ? (dense ? kVarSmallDense16 : kVarSmallKgs16)
                     : (dense ? (f32 ? kVarDenseItemsF32 : kVarDenseItems16) : kVarKgsUnion16);
@@ -679,7 +698,10 @@ struct ItemPair {
 // two groups first, then an item of either other group alone; items kept by
 // one group pair across groups, largest buckets first.  Every item lands in
 // exactly one pair.
-std::vector<ItemPair> pair_up(const std::vector<Item> &items) {
+std::vector<ItemPair> pair_up_wide(const std::vector<Item> &items);
+
+std::vector<ItemPair> pair_up(const std::vector<Item> &items, int groups = 4) {
+  if (groups > 4) return pair_up_wide(items);
   std::vector<Item> b[16];
   for (const Item &it : items) b[it.keep & 15u].push_back(it);
   std::vector<ItemPair> out;
@@ -716,6 +738,46 @@ std::vector<ItemPair> pair_up(const std::vector<Item> &items) {
     while (!b[m].empty()) out.push_back({take(m), none});
   // Ascending by position, then channel block: neighbouring pairs read
   // nearby halo rows.
+  std::stable_sort(out.begin(), out.end(), [](const ItemPair &u, const ItemPair &v) {
+    return u.x.pos != v.x.pos ? u.x.pos < v.x.pos : u.x.ql < v.x.ql;
+  });
+  return out;
+}
+
+// Pairing for wide tiles (8 or 16 kernel groups): most constrained first --
+// items in decreasing order of how many groups keep them, each taking the
+// disjoint partner kept by the most groups (greedy matching).
+std::vector<ItemPair> pair_up_wide(const std::vector<Item> &items) {
+  const size_t n = items.size();
+  std::vector<size_t> order(n);
+  std::iota(order.begin(), order.end(), 0);
+  auto pc = [&](size_t i) { return __builtin_popcount(items[i].keep); };
+  std::stable_sort(order.begin(), order.end(), [&](size_t u, size_t v) { return pc(u) > pc(v); });
+  std::vector<char> used(n, 0);
+  std::vector<ItemPair> out;
+  out.reserve(n);
+  const Item none{-1, 0, 0};
+  for (size_t a = 0; a < n; ++a) {
+    const size_t i = order[a];
+    if (used[i]) continue;
+    used[i] = 1;
+    size_t best = n;
+    int best_pc = -1;
+    for (size_t b = a + 1; b < n; ++b) {
+      const size_t j = order[b];
+      if (used[j] || (items[i].keep & items[j].keep)) continue;
+      if (pc(j) > best_pc) {
+        best_pc = pc(j);
+        best = j;
+      }
+    }
+    if (best < n) {
+      used[best] = 1;
+      out.push_back({items[i], items[best]});
+    } else {
+      out.push_back({items[i], none});
+    }
+  }
   std::stable_sort(out.begin(), out.end(), [](const ItemPair &u, const ItemPair &v) {
     return u.x.pos != v.x.pos ? u.x.pos < v.x.pos : u.x.ql < v.x.ql;
   });
@@ -778,11 +840,17 @@ void couple_pairs(std::vector<ItemPair> &prs, const Geom &g, const Tiling &tl, P
 // bits per compressed A element: (0, 1, 0, 1) = 0x44 selects X's channels of
 // a pair's two quads, (2, 3, 2, 3) = 0xEE selects Y's; pair 2g sits in bits
 // 0-7, pair 2g + 1 in bits 8-15.
+//
+// Wide tiles (mfw = 2 or 4: 32 or 64 filters, 8 or 16 kernel groups sharing
+// every B fragment): the pairs are disjoint over all the tile's groups, and
+// the weights stream in MFMA lane order, [step][16-filter row i][lane][8]
+// (zeros where a group keeps neither item of a pair), with the index
+// registers [step][i][lane] in the descriptor section.
 void build_pairs_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const Mask4 *m4,
-                        Layout &L) {
-  const int wt_count = (g.c_out + 15) / 16;
+                        Layout &L, int mfw) {
+  const int wt_count = (g.c_out + 16 * mfw - 1) / (16 * mfw);
   L.variant = kVarKgsPair16;
-  L.plan.mfw = 1;
+  L.plan.mfw = mfw;
   L.plan.wave_tiles = wt_count;
   L.plan.items_per_step = 16;
   L.step_ptr.assign(static_cast<size_t>(wt_count) * (tl.nchunks + 1), 0);
@@ -797,7 +865,8 @@ void build_pairs_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
     L.item_ptr[wt] = first;
     for (int ch = 0; ch < tl.nchunks; ++ch) {
       L.step_ptr[static_cast<size_t>(wt) * (tl.nchunks + 1) + ch] = step;
-      std::vector<ItemPair> prs = pair_up(chunk_items(g, m4, tl.cc, ch, wt * 4, 4));
+      std::vector<ItemPair> prs =
+          pair_up(chunk_items(g, m4, tl.cc, ch, wt * 4 * mfw, 4 * mfw), 4 * mfw);
       while (prs.size() % 8) prs.push_back({none, none});
       couple_pairs(prs, g, tl, cost);
       for (size_t s0 = 0; s0 < prs.size(); s0 += 8, ++step) {
@@ -807,6 +876,34 @@ void build_pairs_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
           L.items.push_back(off(sp[lg].y));
           L.items.push_back(off(sp[lg + 4].x));
           L.items.push_back(off(sp[lg + 4].y));
+        }
+        if (mfw > 1) {
+          // lane (m, ga) of row i: pairs 2ga, 2ga + 1 -> A elements 0-3, 4-7
+          const size_t base = L.a.size();
+          L.a.resize(base + static_cast<size_t>(mfw) * 64 * 8 * g.es);
+          for (int i = 0; i < mfw; ++i)
+            for (int lane = 0; lane < 64; ++lane) {
+              const int blk = 4 * i + ((lane & 15) >> 2);       // 4x4 block in the tile
+              const int m = wt * 16 * mfw + 16 * i + (lane & 15);
+              uint32_t idx = 0;
+              for (int h = 0; h < 2; ++h) {
+                const ItemPair &pr = sp[2 * (lane >> 4) + h];
+                const bool ky = (pr.y.keep >> blk) & 1u;
+                const bool kx = (pr.x.keep >> blk) & 1u;
+                idx |= (ky ? 0xEEu : 0x44u) << (8 * h);
+                uint8_t *dst = L.a.data() + base + ((static_cast<size_t>(i) * 64 + lane) * 8 + 4 * h) * g.es;
+                for (int c = 0; c < 4; ++c) {
+                  if (kx || ky) {
+                    const Item &it = ky ? pr.y : pr.x;
+                    src.copy(dst + c * g.es, m, 4 * (ch * (tl.cc / 4) + it.ql) + c, it.pos);
+                  } else {
+                    std::memset(dst + c * g.es, 0, g.es);
+                  }
+                }
+              }
+              L.keep.push_back(idx);
+            }
+          continue;
         }
         uint32_t keep = 0, side = 0;
         for (int j = 0; j < 8; ++j)
@@ -1007,6 +1104,15 @@ bool use_pairs(const Geom &g, const Mask4 *m4) {
   return tune("kgs_map") == 1;
 }
 
+// Filter rows (of 16) per wave tile of the pair mapping: tuning switch
+// pair_mfw=1|2|4, else 1.
+int pair_width(const Geom &g, const Mask4 *m4) {
+  (void)g;
+  (void)m4;
+  const int v = tune("pair_mfw");
+  return (v == 2 || v == 4) ? v : 1;
+}
+
 // Build everything for a KGS pack (w may be null when only sizing).
 rt3d_status plan_kgs(const rt3d_conv3d_desc *d, const uint8_t *mask, const uint8_t *w,
                      Canon &c, Layout &L, Tiling &tl, bool &vanilla) {
@@ -1023,9 +1129,10 @@ rt3d_status plan_kgs(const rt3d_conv3d_desc *d, const uint8_t *mask, const uint8
   }
   const Geom g = geom_of(d);
   const bool small = small_ok(g);
-  tl = layer_tiling(g);
-  if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
   Mask4 m4{mask, c.Q, ks, d->g_m / 4, d->g_n / 4};
+  const ItemPlan ip = item_plan(g, &m4, small);
+  tl = ip.tl;
+  if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
   static const uint8_t zero = 0;
   const uint8_t *wsrc = w ? w : &zero;
   if (!w) {
@@ -1050,9 +1157,9 @@ rt3d_status plan_kgs(const rt3d_conv3d_desc *d, const uint8_t *mask, const uint8
     if (!small && use_pairs(g, &m4)) {
       tl = choose_tiling(g, 64);
       if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
-      build_pairs_layout(g, tl, wsrc, &m4, L);
+      build_pairs_layout(g, tl, wsrc, &m4, L, pair_width(g, &m4));
     } else {
-      build_items_layout(g, tl, wsrc, &m4, L, small);
+      build_items_layout(g, tl, wsrc, &m4, L, small, ip.mfw);
     }
   }
   return ok();
@@ -1586,11 +1693,12 @@ rt3d_status rt3d_dense_pack_size(const rt3d_conv3d_desc *d, uint64_t *bytes) {
   if (!bytes) return fail(RT3D_ERR_INVALID_ARG, "bytes must be non-NULL");
   const Geom g = geom_of(d);
   const bool small = small_ok(g);
-  const Tiling tl = layer_tiling(g);
+  const ItemPlan ip = item_plan(g, nullptr, small);
+  const Tiling &tl = ip.tl;
   if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
   std::vector<uint8_t> scratch(static_cast<size_t>(g.c_out) * g.c_in * g.ks * g.es, 0);
   Layout L;
-  build_items_layout(g, tl, scratch.data(), nullptr, L, small);
+  build_items_layout(g, tl, scratch.data(), nullptr, L, small, ip.mfw);
   *bytes = section_offsets(nullptr, g.es, L).total;
   return ok();
 }
@@ -1603,10 +1711,11 @@ rt3d_status rt3d_dense_pack(const rt3d_conv3d_desc *d, const void *w_dense, void
     return fail(RT3D_ERR_INVALID_ARG, "w_dense, blob and info must be non-NULL");
   const Geom g = geom_of(d);
   const bool small = small_ok(g);
-  const Tiling tl = layer_tiling(g);
+  const ItemPlan ip = item_plan(g, nullptr, small);
+  const Tiling &tl = ip.tl;
   if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
   Layout L;
-  build_items_layout(g, tl, static_cast<const uint8_t *>(w_dense), nullptr, L, small);
+  build_items_layout(g, tl, static_cast<const uint8_t *>(w_dense), nullptr, L, small, ip.mfw);
   const Sections s = section_offsets(nullptr, g.es, L);
   if (blob_bytes < s.total)
     return fail(RT3D_ERR_BUFFER_TOO_SMALL, "blob needs %llu bytes, got %llu",

@@ -580,7 +580,9 @@ __device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, co
 // FAST: c_in is a multiple of 8 (branch-free halo staging).
 template <typename T, int MFW, int NF, bool FAST, bool PAIR = false>
 __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
-  static_assert(!PAIR || MFW == 1, "the pair mapping uses 16-filter tiles");
+  // PAIR with MFW > 1: 32- or 64-filter tiles share each B fragment; their
+  // weights and index registers stream in lane order (not compacted).
+  constexpr bool COMPACT = PAIR && MFW == 1;
   using V8 = std::conditional_t<std::is_same_v<T, __bf16>, bf16x8, f16x8>;
   using V16 = std::conditional_t<std::is_same_v<T, __bf16>, bf16x16, f16x16>;
   using BV = std::conditional_t<PAIR, V16, V8>;     // B fragment of one step
@@ -625,10 +627,11 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
   OFF roff[4];
   V8 ra[2][MFW];
   BV rb[2][NF];
-  // PAIR only: step descriptors (keep word, side word, first block) ride
-  // with the offsets; each A slot carries its 2-bit index register.
-  uint4 rdesc[PAIR ? 4 : 1];
-  uint32_t ridx[2] = {0u, 0u};
+  // PAIR: each A slot carries its 2-bit index registers; the compact stream's
+  // step descriptors ride with the offsets.
+  uint4 rdesc[COMPACT ? 4 : 1];
+  uint32_t ridx[2][MFW] = {};
+  const uint32_t *IDX = a.keep + lane;  // PAIR, MFW > 1: [step][i][lane]
   const uint32_t row8 = (lane & 3) * 8u;           // this lane's filter row within a block
   const __amdgpu_buffer_rsrc_t ares =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(a.a), 0, static_cast<int>(a.a_bytes), 0x00020000);
@@ -637,36 +640,47 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
   const uint4 *KD = reinterpret_cast<const uint4 *>(a.keep) + 4 * g + ((lane & 15) >> 2);
   auto fetch_off = [&](int slot, uint32_t s) {
     roff[slot] = IT[(static_cast<long>(row0) + (s - step0)) * 4];
-    if constexpr (PAIR) rdesc[slot] = KD[static_cast<long>(s) * 16];
+    if constexpr (COMPACT) rdesc[slot] = KD[static_cast<long>(s) * 16];
   };
   // dslot: the offsets-ring slot that holds step s's descriptor (PAIR).
   auto fetch_a = [&](int slot, uint32_t s, int dslot) {
-    if constexpr (PAIR) {
+    if constexpr (COMPACT) {
       // This lane's filter row of the two blocks (offsets >= 2^31 read zeros).
       const uint4 d = rdesc[dslot];
       const uint2 lo = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(ares, static_cast<int>(d.x + row8), 0, 0));
       const uint2 hi = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(ares, static_cast<int>(d.y + row8), 0, 0));
       ra[slot][0] = __builtin_bit_cast(V8, make_uint4(lo.x, lo.y, hi.x, hi.y));
-      ridx[slot] = d.z;
+      ridx[slot][0] = d.z;
     } else {
       (void)dslot;
       #pragma unroll
-      for (int i = 0; i < MFW; ++i) ra[slot][i] = A[(static_cast<long>(s) * MFW + i) * 64];
+      for (int i = 0; i < MFW; ++i) {
+        ra[slot][i] = A[(static_cast<long>(s) * MFW + i) * 64];
+        if constexpr (PAIR) ridx[slot][i] = IDX[(static_cast<long>(s) * MFW + i) * 64];
+      }
     }
   };
   auto load_b = [&](int slot, OFF off) {
     #pragma unroll
     for (int j = 0; j < NF; ++j) {
       if constexpr (PAIR) {
-        // Operand order (X.c01, Y.c01, X.c23, Y.c23) per pair.  Two 8-byte
-        // reads per pair and register moves to interleave them: LDS time
-        // follows the number of read instructions more than their width, and
-        // four 4-byte reads per pair measured about twice as slow.
+        // Two 8-byte reads per pair; operand order is (X.c01, Y.c01, X.c23,
+        // Y.c23).  Wide tiles keep the reads in load order (X.c01, X.c23,
+        // Y.c01, Y.c23), landing in place, and swap them in the MFMA stage a
+        // step later (swapping here waits for the reads every step; measured
+        // 808 -> 761 us on batch-32 conv3b); 16-filter tiles swap here (the
+        // deferred swap's extra registers cost them: conv2 54 -> 82 us).
+        // LDS time follows the number of read instructions more than their
+        // width: four 4-byte reads per pair that would land in operand order
+        // measured about twice as slow.
         const uint2 x0 = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.x);
         const uint2 y0 = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.y);
         const uint2 x1 = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.z);
         const uint2 y1 = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.w);
-        rb[slot][j] = __builtin_bit_cast(V16, u32x8{x0.x, y0.x, x0.y, y0.y, x1.x, y1.x, x1.y, y1.y});
+        if constexpr (MFW > 1)
+          rb[slot][j] = __builtin_bit_cast(V16, u32x8{x0.x, x0.y, y0.x, y0.y, x1.x, x1.y, y1.x, y1.y});
+        else
+          rb[slot][j] = __builtin_bit_cast(V16, u32x8{x0.x, y0.x, x0.y, y0.y, x1.x, y1.x, x1.y, y1.y});
       } else {
         const uint2 lo = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.x);
         const uint2 hi = *reinterpret_cast<const uint2 *>(lds + vb[j] + off.y);
@@ -676,22 +690,29 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
   };
   auto mma = [&](int slot) {
     #pragma unroll
-    for (int j = 0; j < NF; ++j)
+    for (int j = 0; j < NF; ++j) {
+      BV bj = rb[slot][j];
+      if constexpr (PAIR && MFW > 1) {
+        // load order (X.c01, X.c23, Y.c01, Y.c23) -> quads (X.c01, Y.c01), (X.c23, Y.c23)
+        u32x8 r = __builtin_bit_cast(u32x8, bj);
+        bj = __builtin_bit_cast(V16, u32x8{r[0], r[2], r[1], r[3], r[4], r[6], r[5], r[7]});
+      }
       #pragma unroll
       for (int i = 0; i < MFW; ++i) {
         if constexpr (PAIR) {
           if constexpr (std::is_same_v<T, __bf16>)
-            acc[i][j] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(ra[slot][i], rb[slot][j], acc[i][j],
-                                                                   static_cast<int>(ridx[slot]), 0, 0);
+            acc[i][j] = __builtin_amdgcn_smfmac_f32_16x16x64_bf16(ra[slot][i], bj, acc[i][j],
+                                                                   static_cast<int>(ridx[slot][i]), 0, 0);
           else
-            acc[i][j] = __builtin_amdgcn_smfmac_f32_16x16x64_f16(ra[slot][i], rb[slot][j], acc[i][j],
-                                                                  static_cast<int>(ridx[slot]), 0, 0);
+            acc[i][j] = __builtin_amdgcn_smfmac_f32_16x16x64_f16(ra[slot][i], bj, acc[i][j],
+                                                                  static_cast<int>(ridx[slot][i]), 0, 0);
         } else if constexpr (std::is_same_v<T, __bf16>) {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ra[slot][i], rb[slot][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ra[slot][i], bj, acc[i][j], 0, 0, 0);
         } else {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ra[slot][i], rb[slot][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ra[slot][i], bj, acc[i][j], 0, 0, 0);
         }
       }
+    }
   };
 
   int ch0, ch1;
@@ -752,17 +773,17 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
     // (n = steps of this chunk): rotate them to slot 0 for the next chunk.
     const uint32_t n = s_end - s_beg;
     rotate_ring(roff, static_cast<int>(n & 3));
-    if constexpr (PAIR) rotate_ring(rdesc, static_cast<int>(n & 3));
+    if constexpr (COMPACT) rotate_ring(rdesc, static_cast<int>(n & 3));
     if (n & 1) {
 #pragma unroll
       for (int i = 0; i < MFW; ++i) {
         const V8 t = ra[0][i];
         ra[0][i] = ra[1][i];
         ra[1][i] = t;
+        const uint32_t ti = ridx[0][i];
+        ridx[0][i] = ridx[1][i];
+        ridx[1][i] = ti;
       }
-      const uint32_t ti = ridx[0];
-      ridx[0] = ridx[1];
-      ridx[1] = ti;
     }
   }
   if (a.splits > 1) {
@@ -1887,9 +1908,17 @@ int conv_resident(int variant, int dtype, int mfw, int nf, size_t lds) {
 #undef RT3D_RES16
       return 0;
     case kVarKgsPair16:
-      if (mfw != 1 || nf != 4) return 0;
-      if (dtype == RT3D_BF16) return resident(items16_kernel<__bf16, 1, 4, true, true>, lds);
-      return resident(items16_kernel<_Float16, 1, 4, true, true>, lds);
+      if (nf != 4) return 0;
+      if (dtype == RT3D_BF16) {
+        if (mfw == 1) return resident(items16_kernel<__bf16, 1, 4, true, true>, lds);
+        if (mfw == 2) return resident(items16_kernel<__bf16, 2, 4, true, true>, lds);
+        if (mfw == 4) return resident(items16_kernel<__bf16, 4, 4, true, true>, lds);
+        return 0;
+      }
+      if (mfw == 1) return resident(items16_kernel<_Float16, 1, 4, true, true>, lds);
+      if (mfw == 2) return resident(items16_kernel<_Float16, 2, 4, true, true>, lds);
+      if (mfw == 4) return resident(items16_kernel<_Float16, 4, 4, true, true>, lds);
+      return 0;
     case kVarDenseItemsF32:
       if (nf == 4) {
         if (mfw == 1) return resident(items_f32_kernel<1, 4>, lds);
@@ -1968,14 +1997,21 @@ int launch_items16(const ConvArgs &a, int dtype, int mfw, bool pair, void *strea
   if (pair) {
     // 64-slot bricks only: with eight fragments the doubled B ring would
     // leave one wave per SIMD.
-    if (mfw != 1 || a.nf != 4) return hipErrorInvalidValue;
-#define RT3D_PAIR16(T)                                                                   \
+    if (a.nf != 4) return hipErrorInvalidValue;
+#define RT3D_PAIR16(T, M)                                                                \
   do {                                                                                   \
-    return fast ? launch_conv(items16_kernel<T, 1, 4, true, true>, a, stream)            \
-                : launch_conv(items16_kernel<T, 1, 4, false, true>, a, stream);          \
+    return fast ? launch_conv(items16_kernel<T, M, 4, true, true>, a, stream)            \
+                : launch_conv(items16_kernel<T, M, 4, false, true>, a, stream);          \
   } while (0)
-    if (dtype == RT3D_BF16) RT3D_PAIR16(__bf16);
-    if (dtype == RT3D_F16) RT3D_PAIR16(_Float16);
+    if (dtype == RT3D_BF16) {
+      if (mfw == 1) RT3D_PAIR16(__bf16, 1);
+      if (mfw == 2) RT3D_PAIR16(__bf16, 2);
+      if (mfw == 4) RT3D_PAIR16(__bf16, 4);
+    } else if (dtype == RT3D_F16) {
+      if (mfw == 1) RT3D_PAIR16(_Float16, 1);
+      if (mfw == 2) RT3D_PAIR16(_Float16, 2);
+      if (mfw == 4) RT3D_PAIR16(_Float16, 4);
+    }
 #undef RT3D_PAIR16
     return hipErrorInvalidValue;
   }

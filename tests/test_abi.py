@@ -150,28 +150,44 @@ def _brick_slots(desc):
     return int(np.frombuffer(bytes(info.plan), dtype=np.int32)[8])
 
 
+def _plan_mfw(desc):
+    w = _weights(np.random.default_rng(1), (desc.c_out, desc.c_in, desc.kt, desc.kh, desc.kw),
+                 {0: "f32", 1: "bf16", 2: "f16"}[desc.dtype])
+    _, info = rt3d.rt3d_dense_pack(desc, w)
+    return int(np.frombuffer(bytes(info.plan), dtype=np.int32)[10])
+
+
 def test_brick_width_follows_the_layer_size(monkeypatch):
-    """64-slot bricks when 128-slot bricks times 16-filter tiles give fewer
-    than 1024 waves (one per SIMD of the GPU) for pooled 16-bit layers, 8192
-    for unpooled 16-bit layers (their narrow-tile epilogue runs in
-    registers) and 256 for fp32; larger layers keep 128; RT3D_TUNE=slots=N
-    overrides the choice at pack time."""
+    """Brick rule (dense packs): 64-slot bricks when 128-slot bricks times
+    16-filter tiles give fewer than 1024 waves (one per SIMD of the GPU) for
+    pooled 16-bit layers, 8192 for unpooled 16-bit layers (their narrow-tile
+    epilogue runs in registers) and 256 for fp32, and for every 16-bit layer
+    whose wave tile has two or more 16-filter rows (on 128-slot bricks those
+    tiles leave one wave per SIMD); larger single-row layers keep 128;
+    RT3D_TUNE=slots=N overrides the choice at pack time."""
     monkeypatch.delenv("RT3D_TUNE", raising=False)
-    pooled_big = rt3d.make_desc(1, 64, 128, (16, 56, 56), dtype="bf16", pool=(2, 2, 2))  # 3136
+    pooled_big = rt3d.make_desc(1, 32, 64, (16, 56, 56), dtype="bf16", pool=(2, 2, 2))   # 1568
     pooled_small = rt3d.make_desc(1, 256, 256, (8, 28, 28), dtype="bf16", pool=(2, 2, 2))  # 784
-    unpooled = rt3d.make_desc(1, 64, 128, (16, 56, 56), dtype="bf16")       # 3136 waves
-    unpooled_big = rt3d.make_desc(4, 64, 128, (16, 56, 56), dtype="f16")    # 12544 waves
+    unpooled = rt3d.make_desc(1, 32, 64, (16, 56, 56), dtype="bf16")       # 1568 waves
+    unpooled_big = rt3d.make_desc(4, 32, 64, (16, 56, 56), dtype="f16")    # 6272 waves
+    unpooled_huge = rt3d.make_desc(8, 32, 64, (16, 56, 56), dtype="f16")   # 12544 waves
+    conv2 = rt3d.make_desc(1, 64, 128, (16, 56, 56), dtype="bf16", pool=(2, 2, 2))   # 32-filter tiles
+    wide32 = rt3d.make_desc(32, 256, 256, (8, 28, 28), dtype="bf16")       # 64-filter tiles
     f32 = rt3d.make_desc(1, 256, 256, (8, 28, 28), dtype="f32")             # 784 waves
     f32_small = rt3d.make_desc(1, 16, 32, (8, 28, 28), dtype="f32")         # 49 x 2 = 98 waves
     assert _brick_slots(pooled_big) == 128
     assert _brick_slots(pooled_small) == 64
     assert _brick_slots(unpooled) == 64
-    assert _brick_slots(unpooled_big) == 128
+    assert _brick_slots(unpooled_big) == 64
+    assert _brick_slots(unpooled_huge) == 128
+    assert (_plan_mfw(conv2), _brick_slots(conv2)) == (2, 64)
+    assert (_plan_mfw(wide32), _brick_slots(wide32)) == (4, 64)
     assert _brick_slots(f32) == 128
     assert _brick_slots(f32_small) == 64
     monkeypatch.setenv("RT3D_TUNE", "slots=128")
     assert _brick_slots(pooled_small) == 128
     assert _brick_slots(f32_small) == 128
+    assert _brick_slots(conv2) == 128
     monkeypatch.setenv("RT3D_TUNE", "slots=64")
     assert _brick_slots(pooled_big) == 64
     assert _brick_slots(f32) == 64

@@ -531,10 +531,14 @@ def test_s3d_layers_full_size(li):
 # default, so it is forced through the tuning switch.
 # ---------------------------------------------------------------------------
 
+PAIR_TUNES = ["kgs_map=1", "kgs_map=1,pair_mfw=2", "kgs_map=1,pair_mfw=4"]
+
+
+@pytest.mark.parametrize("tune", PAIR_TUNES)
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
 @pytest.mark.parametrize("si", range(len(SHAPES)))
-def test_pair_mapping_small_shapes(si, dtype, monkeypatch):
-    monkeypatch.setenv("RT3D_TUNE", "kgs_map=1")
+def test_pair_mapping_small_shapes(si, dtype, tune, monkeypatch):
+    monkeypatch.setenv("RT3D_TUNE", tune)
     tag, n, c_in, c_out, thw, k, stride, pad, keep = SHAPES[si]
     mask = masked(tag, c_out, c_in, k, min(keep, k[0] * k[1] * k[2]))
     case = LayerCase(tag + "p", n, c_in, c_out, thw, k, stride, pad, dtype, mask)
@@ -543,9 +547,10 @@ def test_pair_mapping_small_shapes(si, dtype, monkeypatch):
     check_full(case, f"pairs {tag} {dtype}")
 
 
+@pytest.mark.parametrize("tune", PAIR_TUNES)
 @pytest.mark.parametrize("pi", [0, 1, 4, 7, 8])
-def test_pair_mapping_pooled_and_split(pi, monkeypatch):
-    monkeypatch.setenv("RT3D_TUNE", "kgs_map=1")
+def test_pair_mapping_pooled_and_split(pi, tune, monkeypatch):
+    monkeypatch.setenv("RT3D_TUNE", tune)
     tag, n, c_in, c_out, thw, pool, dtype, sparse, residual = POOLED[pi]
     mask = masked(tag, c_out, c_in, (3, 3, 3), 9)
     case = LayerCase(tag + "p", n, c_in, c_out, thw, (3, 3, 3), (1, 1, 1), (1, 1, 1),
@@ -554,20 +559,22 @@ def test_pair_mapping_pooled_and_split(pi, monkeypatch):
     check_full(case, f"pairs pooled {tag}")
 
 
+@pytest.mark.parametrize("tune", PAIR_TUNES)
 @pytest.mark.parametrize("gi", [1, 3, 4])
-def test_pair_mapping_group_sizes(gi, monkeypatch):
-    monkeypatch.setenv("RT3D_TUNE", "kgs_map=1")
+def test_pair_mapping_group_sizes(gi, tune, monkeypatch):
+    monkeypatch.setenv("RT3D_TUNE", tune)
     tag, n, c_in, c_out, thw, k, stride, pad, g, keep = GROUPED[gi]
     mask = masked(tag, c_out, c_in, k, keep, g)
     case = LayerCase(tag + "p", n, c_in, c_out, thw, k, stride, pad, "bf16", mask, g=g)
     check_full(case, f"pairs {tag} g={g}")
 
 
+@pytest.mark.parametrize("tune", PAIR_TUNES)
 @pytest.mark.parametrize("variant", ["kgs3", "vanilla3"])
 @pytest.mark.parametrize("li", [1, 3, 6])
-def test_pair_mapping_c3d_layers(li, variant, monkeypatch):
+def test_pair_mapping_c3d_layers(li, variant, tune, monkeypatch):
     """Full-size C3D layers at batch 1 on the pair mapping, sampled outputs."""
-    monkeypatch.setenv("RT3D_TUNE", "kgs_map=1")
+    monkeypatch.setenv("RT3D_TUNE", tune)
     stack = synth.c3d_stack(3.0)
     l = stack[li]
     r = synth.rng_for("c3d-pair", variant, l.name, "mask")

@@ -127,7 +127,7 @@ def test_stack_as_benchmarked(net, batch, mode, rate):
         # the dominant layer of the default bench line runs this plan
         p = _plan(st.convs[1])
         assert p["pool"] == (2, 2, 2), p
-        assert (p["variant"], p["slots"], p["brick"]) == (3, 128, (4, 2, 16)), p
+        assert (p["variant"], p["slots"], p["brick"], p["mfw"]) == (3, 64, (2, 2, 16), 2), p
 
 
 def test_s3d_stack_as_benchmarked():

@@ -94,6 +94,31 @@ def decode(desc, info, blob):
         seen[m, c, pos] = True
         out[m, c, pos] = v
 
+    if info.variant == VAR_PAIR16 and p["mfw"] > 1:
+        mfw = p["mfw"]
+        idx_all = _u32(blob, p["keep"], (p["a"] - p["keep"]) // 4)
+        for wt in range(nwt):
+            for ch in range(nch):
+                for s in range(step_ptr[wt, ch], step_ptr[wt, ch + 1]):
+                    its = _u32(blob, p["items"] + 64 * s, 16)
+                    for i in range(mfw):
+                        base = (s * mfw + i) * 64
+                        for lane in range(64):
+                            m = wt * 16 * mfw + 16 * i + (lane & 15)
+                            idx = int(idx_all[base + lane])
+                            for h in range(2):
+                                j = 2 * (lane >> 4) + h
+                                lg, half = j % 4, (j // 4) * 2
+                                sel = (idx >> (8 * h)) & 0xFF
+                                assert sel in (0x44, 0xEE), hex(sel)
+                                off = int(its[4 * lg + half + (1 if sel == 0xEE else 0)])
+                                ql, pos = _item(p, off, kh, kw)
+                                for c in range(4):
+                                    streamed += 1
+                                    put(m, 4 * (ch * (cc // 4) + ql) + c, pos,
+                                        int(a16[(base + lane) * 8 + 4 * h + c]))
+        return out, seen, streamed
+
     if info.variant == VAR_PAIR16:
         used_blocks = set()
         for wt in range(nwt):
@@ -172,7 +197,8 @@ def _mask(rng, c_out, c_in, ks, g, keep):
     return m
 
 
-@pytest.mark.parametrize("tune", ["kgs_map=1", "kgs_map=0,kgs_mfw=1", "kgs_map=0,kgs_mfw=2",
+@pytest.mark.parametrize("tune", ["kgs_map=1", "kgs_map=1,pair_mfw=2", "kgs_map=1,pair_mfw=4",
+                                  "kgs_map=0,kgs_mfw=1", "kgs_map=0,kgs_mfw=2",
                                   "kgs_map=0,kgs_mfw=4", "kgs_map=0,kgs_mfw=1,slots=128"])
 @pytest.mark.parametrize("ci", range(len(CASES)))
 @pytest.mark.parametrize("dt", ["bf16", "f16"])
@@ -192,7 +218,7 @@ def test_kgs_layout_decodes_to_masked_weights(dt, ci, tune, monkeypatch):
     assert got.tobytes() == exp.tobytes()
     # every kept nonzero weight was found (random normal weights are nonzero)
     assert np.array_equal(seen, kept & (exp != 0))
-    if want_pair:
+    if want_pair and "pair_mfw" not in tune:
         # kept 4x4 blocks only: the stream is the canonical values' size
         # (partial trailing groups stream their zero rows and columns)
         if c_out % 4 == 0 and c_in % 4 == 0:
