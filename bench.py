@@ -63,6 +63,14 @@ def parse():
                    help="instead of the headline line, run the per-config measurement suite "
                         "(single layers, R(2+1)D, batch-32 rate sweep, warm/cold latency, oracle "
                         "timing) and write a markdown report to PATH (+ PATH.json)")
+    p.add_argument("--profile-stack", default=None, metavar="MANIFEST",
+                   help="launch every layer of the stack (--net/--batch/--mode) --layer-reps "
+                        "times back to back, in order, for rocprofv3; write the dispatch "
+                        "manifest (JSON) to MANIFEST")
+    p.add_argument("--summarize-profile", default=None, metavar="DIR",
+                   help="per-layer markdown table from the rocprofv3 runs of --profile-stack "
+                        "under DIR (subdirectories trace, fetch, write, sqa, sqb and "
+                        "manifest.json)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="with --profile-layer: also run a plain device copy of MIB MiB, the "
                         "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE")
@@ -168,17 +176,19 @@ def library_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(layer):
-    """HBM bytes per launch of `layer`'s KGS conv from the committed
-    rocprofv3 FETCH_SIZE / WRITE_SIZE summaries, or None when no summary
-    exists for it or the kernels changed since it was taken."""
+def measured_traffic(layer, net="c3d", batch=1, mode="kgs", dtype="bf16"):
+    """HBM bytes per launch of `layer`'s conv (and split reduction) from the
+    committed rocprofv3 FETCH_SIZE / WRITE_SIZE summaries, or None when no
+    summary exists for it or the kernels changed since it was taken."""
     import glob
-    for path in glob.glob(os.path.join(ROOT, "profiles", "*.md")):
+    want = {"layer": layer, "net": net, "batch": batch, "mode": mode, "dtype": dtype,
+            "source_hash": library_source_hash()}
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
         with open(path) as fh:
             for line in fh:
                 if line.startswith("traffic-json:"):
                     d = json.loads(line.split(":", 1)[1])
-                    if d.get("layer") == layer and d.get("source_hash") == library_source_hash():
+                    if all(d.get(k) == v for k, v in want.items()):
                         return d["traffic_bytes_per_launch"]
     return None
 
@@ -223,6 +233,164 @@ def profile_layer(args, torch, stream):
         torch.cuda.synchronize()
         out["copy_bytes_each_way"] = n * 4
     print(json.dumps(out), flush=True)
+
+
+def _copy_calibration(torch, mib):
+    """A plain device copy of `mib` MiB each way (the FETCH_SIZE / WRITE_SIZE
+    scale of the profiles)."""
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    return n * 4
+
+
+def profile_stack(args, torch, stream):
+    """Every conv of the stack launched --layer-reps times back to back (its
+    split reduction after each launch when it splits), layer after layer,
+    after one pass over the benchmark clip; then a plain copy of known size.
+    The manifest lists, per layer, the dispatches of one launch and the
+    algorithmic FLOPs and bytes, so a summary can attribute rocprofv3's
+    per-dispatch rows to layers by their order."""
+    from paper_2007_09835_amd import synth
+    from paper_2007_09835_amd.stack import make_stack
+    st = make_stack(args.net, args.batch, args.dtype, args.mode, args.rate,
+                    fuse_pool=not args.separate_pool, group=group_of(args))
+    l0 = st.layers[0]
+    st.x.copy_(synth.to_dtype(synth.clip_input("bench-clip", args.batch, "uniform01", l0.c_in,
+                                               l0.t, l0.h, l0.w), args.dtype)
+               .permute(0, 2, 3, 4, 1).contiguous().cuda())
+    layers = []
+    for (l, fn), conv in zip(st.layer_calls(), st.convs):
+        split = conv.workspace(args.batch) is not None
+        roof = layer_roofline(l, conv, args.batch, 1.0)
+        i32 = [int(v) for v in __import__("numpy").frombuffer(bytes(conv.info.plan), dtype="int32")[:11]]
+        layers.append({"layer": l.name, "kgs": conv.sparse, "dispatches": 2 if split else 1,
+                       "variant": int(conv.info.variant), "brick": i32[:3], "slots": i32[8],
+                       "mfw": i32[10], "kept_flops": roof["flops"], "bytes": roof["bytes"],
+                       "dense_flops": 2.0 * l.dense_macs(args.batch)})
+    st.forward()
+    torch.cuda.synchronize()
+    clock_warmup(torch, args.clock_warmup)
+    for (l, fn) in st.layer_calls():
+        for _ in range(args.layer_reps):
+            fn()
+        torch.cuda.synchronize()
+    copy_bytes = _copy_calibration(torch, args.copy_calibration or 256)
+    man = {"net": args.net, "batch": args.batch, "mode": args.mode, "dtype": args.dtype,
+           "rate": st.kept_rate(), "reps": args.layer_reps, "layers": layers,
+           "copy_bytes_each_way": copy_bytes, "source_hash": library_source_hash()}
+    with open(args.profile_stack, "w") as f:
+        json.dump(man, f)
+    print(json.dumps({"profile_stack": args.profile_stack, "layers": len(layers)}), flush=True)
+
+
+def _csv_rows(d, suffix):
+    import csv
+    import glob
+    paths = glob.glob(os.path.join(d, "**", "*" + suffix), recursive=True)
+    if not paths:
+        raise SystemExit("no %s under %s" % (suffix, d))
+    with open(paths[0]) as f:
+        return list(csv.DictReader(f))
+
+
+def _per_dispatch(d, kind):
+    """[(kernel name, {counter: value} or duration us)] of every dispatch in
+    order (rocprofv3 csv under d)."""
+    if kind == "trace":
+        rows = _csv_rows(d, "kernel_trace.csv")
+        rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+        return [(r["Kernel_Name"], (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+                for r in rows]
+    rows = _csv_rows(d, "counter_collection.csv")
+    by = {}
+    for r in rows:
+        k = int(r["Dispatch_Id"])
+        name, vals = by.setdefault(k, (r["Kernel_Name"], {}))
+        vals[r["Counter_Name"]] = vals.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return [by[k] for k in sorted(by)]
+
+
+def summarize_profile(args):
+    """Markdown table per layer from the five rocprofv3 runs of --profile-stack."""
+    d = args.summarize_profile
+    with open(os.path.join(d, "manifest.json")) as f:
+        man = json.load(f)
+    reps = man["reps"]
+
+    def attribute(kind):
+        seq = _per_dispatch(os.path.join(d, kind), kind)
+        ours = [x for x in seq if "rt3d" in x[0]]
+        other = [x for x in seq if "rt3d" not in x[0]]
+        fwd = sum(l["dispatches"] for l in man["layers"])
+        pos = fwd
+        out = []
+        for l in man["layers"]:
+            n = l["dispatches"]
+            chunk = ours[pos:pos + reps * n]
+            pos += reps * n
+            out.append(([chunk[i] for i in range(0, len(chunk), n)],
+                        [chunk[i] for i in range(1, len(chunk), n)] if n == 2 else []))
+        if pos != len(ours):
+            raise SystemExit("%s: %d library dispatches, the manifest accounts for %d"
+                             % (kind, len(ours), pos))
+        return out, other
+
+    def mean(xs, key=None):
+        v = [x[1] if key is None else x[1].get(key, 0.0) for x in xs]
+        return sum(v) / len(v) if v else 0.0
+
+    trace, _ = attribute("trace")
+    fetch, fo = attribute("fetch")
+    write, wo = attribute("write")
+    sqa, _ = attribute("sqa")
+    sqb, _ = attribute("sqb")
+    copy = man["copy_bytes_each_way"] / 1024.0
+    fscale = copy / max(x[1]["FETCH_SIZE"] for x in fo)
+    wscale = copy / max(x[1]["WRITE_SIZE"] for x in wo)
+    peak = PEAK_TFLOPS[man["dtype"]]
+    lines = ["| layer | map | plan | conv us | reduce us | traffic MB (conv+red) | algorithmic MB | "
+             "MfmaUtil % | MFMA exec / kept | VALU / MFMA | LDS / MFMA | LDS conflict | "
+             "roofline frac |", "|" + "---|" * 13]
+    js = []
+    for i, l in enumerate(man["layers"]):
+        conv_us = mean(trace[i][0])
+        red_us = mean(trace[i][1])
+        fb = (mean(fetch[i][0], "FETCH_SIZE") + mean(fetch[i][1], "FETCH_SIZE")) * 1024 * fscale
+        wb = (mean(write[i][0], "WRITE_SIZE") + mean(write[i][1], "WRITE_SIZE")) * 1024 * wscale
+        a = {k: mean(sqa[i][0], k) for k in sqa[i][0][0][1]}
+        a.update({k: mean(sqb[i][0], k) for k in sqb[i][0][0][1]})
+        mfma = a.get("SQ_INSTS_MFMA", 0.0)
+        gui = a.get("GRBM_GUI_ACTIVE", 1.0)
+        util = 100.0 * a.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / max(gui / 8.0 * 1024.0, 1.0)
+        # 16x16x32 (16-bit) MFMAs: 16384 FLOP each; 16x16x4 f32: 2048; 4x4x1 f32 (x16 blocks): 512
+        per = {"bf16": 16384.0, "f16": 16384.0, "f32": 2048.0}[man["dtype"]]
+        exec_ratio = mfma * per / l["kept_flops"] if l["kept_flops"] else 0.0
+        t = (conv_us + red_us) * 1e-6
+        frac = max(l["kept_flops"] / (peak * 1e12), l["bytes"] / (HBM_GBPS * 1e9)) / t
+        plan = "v%d %dx%dx%d/%d mfw%d" % (l["variant"], *l["brick"], l["slots"], l["mfw"])
+        lines.append("| %s | %s | %s | %.2f | %.2f | %.2f | %.2f | %.1f | %.2f | %.1f | %.2f | %.2f | %.3f |"
+                     % (l["layer"], "KGS" if l["kgs"] else "dense", plan, conv_us, red_us,
+                        (fb + wb) / 1e6, l["bytes"] / 1e6, util, exec_ratio,
+                        a.get("SQ_INSTS_VALU", 0.0) / max(mfma, 1.0),
+                        a.get("SQ_INSTS_LDS", 0.0) / max(mfma, 1.0),
+                        a.get("SQ_LDS_BANK_CONFLICT", 0.0) / max(a.get("SQ_LDS_IDX_ACTIVE", 1.0), 1.0),
+                        frac))
+        js.append({"layer": l["layer"], "kernel": plan, "source_hash": man["source_hash"],
+                   "net": man["net"], "batch": man["batch"], "mode": man["mode"],
+                   "dtype": man["dtype"], "conv_avg_us": round(conv_us, 3),
+                   "reduce_avg_us": round(red_us, 3), "traffic_bytes_per_launch": int(fb + wb),
+                   "fetch_scale": round(fscale, 4), "write_scale": round(wscale, 4),
+                   "mfma_util_pct": round(util, 2), "mfma_exec_over_kept": round(exec_ratio, 3)})
+    print("\n".join(lines))
+    print()
+    print("Traffic: FETCH_SIZE scaled by %.4f and WRITE_SIZE by %.4f (a plain device copy of %d MiB "
+          "each way in the same runs)." % (fscale, wscale, man["copy_bytes_each_way"] >> 20))
+    print()
+    for j in js:
+        print("traffic-json: " + json.dumps(j))
 
 
 def cpu_baseline(stack, fraction):
@@ -596,6 +764,9 @@ def main():
     args = parse()
     if args.rate is None:
         args.rate = 2.1 if args.net == "s3d" else 3.0
+    if args.summarize_profile:
+        summarize_profile(args)
+        return
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
               "(clips are independent, so --gpus N would be N copies of this run)",
@@ -614,6 +785,9 @@ def main():
 
     if args.profile_layer:
         profile_layer(args, torch, stream)
+        return
+    if args.profile_stack:
+        profile_stack(args, torch, stream)
         return
     if args.mode == "dense":
         sys.exit("--mode dense selects the profiled stack; the benchmark always times both")
@@ -722,9 +896,8 @@ def main():
                         if drow["kgs"] else l.dense_macs(args.batch))
     achieved = kept_flops / (drow["ms_sparse"] * 1e-3) / 1e12
     peak = PEAK_TFLOPS[args.dtype]
-    traffic = measured_traffic(l.name) if (args.batch == 1 and args.net == "c3d"
-                                           and args.dtype == "bf16" and args.mode == "kgs"
-                                           and group_of(args) == (4, 4)) else None
+    traffic = (measured_traffic(l.name, args.net, args.batch, args.mode, args.dtype)
+               if group_of(args) == (4, 4) else None)
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": traffic,
                 "kernel": "%s conv (%s)" % (l.name, "KGS" if drow["kgs"] else "dense"),

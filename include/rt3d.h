@@ -41,7 +41,9 @@
  *     per workgroup), kgs_mfw=1|2|4 and dense_mfw=1|2|4 (16-filter MFMA rows
  *     per wave tile), small_mfw=1|2 and small_kernel=0 (the small-input-channel
  *     kernel), kgs_map=0|1 (16-bit KGS mapping: 0 = union of the tile's kept
- *     items, 1 = disjoint item pairs on the 2:4 sparse MFMA).  Launch-time
+ *     items, 1 = disjoint item pairs on the 2:4 sparse MFMA), pair_mfw=1|2|4
+ *     (16-filter rows per pair-mapping tile), cc=N (at most N input channels
+ *     per staged chunk, 16-bit).  Launch-time
  *     keys change the launch of a forward call: splits=N (input-channel
  *     splits) and wg_order=0|1 (workgroup order).  Results stay within the
  *     documented accuracy under every setting.

@@ -228,7 +228,8 @@ Tiling choose_tiling(const Geom &g, int slots = kSlots) {
   // per thread (2048 per workgroup) and the LDS budget.
   if (best_cost >= 0 && g.es == 2) {
     int wide = best.cc;
-    while (wide < 128 && wide < g.c_in) {
+    const int cap = tune("cc") >= 8 ? tune("cc") : 128;  // tuning switch cc=N caps the width
+    while (wide < cap && wide < g.c_in) {
       const int next = wide * 2;
       int nrow = (next * g.es + 15) / 16 * 16;
       if ((nrow / 16) % 2 == 0) nrow += 16;
@@ -947,6 +948,87 @@ void build_pairs_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
   // each) end below byte 2^31: every kept offset stays below the not-kept mark.
 }
 
+// Block-pair layout (kVarKgsBlockPair16): the two items of a 2:4 slot are the
+// channel blocks 2i and 2i + 1 at one kernel position, which the kernel
+// stages interleaved so that one 16-byte LDS read is the slot's operand.  A
+// kernel group takes block 2i if it keeps it, else block 2i + 1 if it keeps
+// that; groups keeping both get block 2i + 1 in a second slot.  Per step 8
+// slots: 8 LDS offsets (lane group g: slots g and g + 4), the weights in MFMA
+// lane order [step][lane][8] and the index registers [step][lane].
+void build_block_pairs_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const Mask4 *m4,
+                              Layout &L) {
+  const int wt_count = (g.c_out + 15) / 16;
+  L.variant = kVarKgsBlockPair16;
+  L.plan.mfw = 1;
+  L.plan.wave_tiles = wt_count;
+  L.plan.items_per_step = 16;
+  L.step_ptr.assign(static_cast<size_t>(wt_count) * (tl.nchunks + 1), 0);
+  L.item_ptr.assign(wt_count, 0);
+  WeightSource src{w, g, m4};
+  const int q4_count = (g.c_in + 3) / 4, p4_count = (g.c_out + 3) / 4;
+  struct Slot {
+    uint32_t off;
+    int q4x, pos;
+    uint8_t sel[4];  // per kernel group: 0 none, 1 block 2i, 2 block 2i + 1
+  };
+  uint32_t step = 0;
+  for (int wt = 0; wt < wt_count; ++wt) {
+    const uint32_t first = step;
+    L.item_ptr[wt] = first;
+    for (int ch = 0; ch < tl.nchunks; ++ch) {
+      L.step_ptr[static_cast<size_t>(wt) * (tl.nchunks + 1) + ch] = step;
+      std::vector<Slot> slots;
+      for (int pos = 0; pos < g.ks; ++pos)
+        for (int i = 0; i < tl.cc / 8; ++i) {
+          const int qx = ch * (tl.cc / 4) + 2 * i, qy = qx + 1;
+          uint32_t kx = 0, ky = 0;
+          for (int gi = 0; gi < 4; ++gi) {
+            const int p4 = wt * 4 + gi;
+            if (p4 >= p4_count) continue;
+            if (qx < q4_count && m4->kept(p4, qx, pos)) kx |= 1u << gi;
+            if (qy < q4_count && m4->kept(p4, qy, pos)) ky |= 1u << gi;
+          }
+          if (!(kx | ky)) continue;
+          Slot s1{item_offset(g, tl, 2 * i, pos), qx, pos, {0, 0, 0, 0}};
+          Slot s2 = s1;
+          for (int gi = 0; gi < 4; ++gi) {
+            s1.sel[gi] = ((kx >> gi) & 1u) ? 1 : (((ky >> gi) & 1u) ? 2 : 0);
+            s2.sel[gi] = ((kx & ky) >> gi) & 1u ? 2 : 0;
+          }
+          slots.push_back(s1);
+          if (kx & ky) slots.push_back(s2);
+        }
+      while (slots.size() % 8) slots.push_back(Slot{0, -1, 0, {0, 0, 0, 0}});
+      for (size_t s0 = 0; s0 < slots.size(); s0 += 8, ++step) {
+        const Slot *sp = &slots[s0];
+        for (int lg = 0; lg < 4; ++lg) {
+          L.items.push_back(sp[lg].off);
+          L.items.push_back(sp[lg + 4].off);
+        }
+        const size_t base = L.a.size();
+        L.a.resize(base + 64 * 8 * static_cast<size_t>(g.es));
+        for (int lane = 0; lane < 64; ++lane) {
+          const int gi = (lane & 15) >> 2, m = wt * 16 + (lane & 15);
+          uint32_t idx = 0;
+          for (int h = 0; h < 2; ++h) {
+            const Slot &sl = sp[2 * (lane >> 4) + h];
+            const int sel = sl.q4x < 0 ? 0 : sl.sel[gi];
+            idx |= (sel == 2 ? 0xEEu : 0x44u) << (8 * h);
+            uint8_t *dst = L.a.data() + base + (static_cast<size_t>(lane) * 8 + 4 * h) * g.es;
+            for (int c = 0; c < 4; ++c) {
+              if (sel == 0) std::memset(dst + c * g.es, 0, g.es);
+              else src.copy(dst + c * g.es, m, 4 * (sl.q4x + sel - 1) + c, sl.pos);
+            }
+          }
+          L.keep.push_back(idx);
+        }
+      }
+    }
+    L.step_ptr[static_cast<size_t>(wt) * (tl.nchunks + 1) + tl.nchunks] = step;
+    L.plan.tile_steps = std::max<int32_t>(L.plan.tile_steps, static_cast<int32_t>(step - first));
+  }
+}
+
 // Exact f32 KGS layout (kVarKgsExactF32): per 16-filter tile and chunk, the
 // union items with their kept-group bits and one 64-float A column set each
 // (lane l = 4*(4*group + channel) + row).
@@ -1104,6 +1186,12 @@ bool use_pairs(const Geom &g, const Mask4 *m4) {
   return tune("kgs_map") == 1;
 }
 
+// Block pairs: tuning switch kgs_map=2.
+bool use_block_pairs(const Geom &g, const Mask4 *m4) {
+  (void)m4;
+  return g.es == 2 && tune("kgs_map") == 2;
+}
+
 // Filter rows (of 16) per wave tile of the pair mapping: tuning switch
 // pair_mfw=1|2|4, else 1.
 int pair_width(const Geom &g, const Mask4 *m4) {
@@ -1154,7 +1242,11 @@ rt3d_status plan_kgs(const rt3d_conv3d_desc *d, const uint8_t *mask, const uint8
       scratch.assign(static_cast<size_t>(g.c_out) * g.c_in * ks * g.es, 0);
       wsrc = scratch.data();
     }
-    if (!small && use_pairs(g, &m4)) {
+    if (!small && use_block_pairs(g, &m4)) {
+      tl = choose_tiling(g, 64);
+      if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
+      build_block_pairs_layout(g, tl, wsrc, &m4, L);
+    } else if (!small && use_pairs(g, &m4)) {
       tl = choose_tiling(g, 64);
       if (tl.cc == 0) return fail(RT3D_ERR_UNSUPPORTED, "no voxel tiling fits in LDS for this layer");
       build_pairs_layout(g, tl, wsrc, &m4, L, pair_width(g, &m4));
@@ -1178,7 +1270,8 @@ rt3d_status check_info(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, bo
   if (info->desc_hash != desc_hash(d))
     return fail(RT3D_ERR_BLOB_MISMATCH, "blob was packed for a different layer description");
   const bool is_sparse = info->variant == kVarKgsUnion16 || info->variant == kVarKgsExactF32 ||
-                         info->variant == kVarSmallKgs16 || info->variant == kVarKgsPair16;
+                         info->variant == kVarSmallKgs16 || info->variant == kVarKgsPair16 ||
+                         info->variant == kVarKgsBlockPair16;
   if (is_sparse != sparse)
     return fail(RT3D_ERR_BLOB_MISMATCH, sparse ? "dense blob passed to the KGS forward"
                                                : "KGS blob passed to the dense forward");
@@ -1436,10 +1529,13 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   switch (info->variant) {
     case kVarDenseItems16:
     case kVarKgsUnion16:
-      e = launch_items16(a, d->dtype, p.mfw, false, stream);
+      e = launch_items16(a, d->dtype, p.mfw, 0, stream);
       break;
     case kVarKgsPair16:
-      e = launch_items16(a, d->dtype, p.mfw, true, stream);
+      e = launch_items16(a, d->dtype, p.mfw, 1, stream);
+      break;
+    case kVarKgsBlockPair16:
+      e = launch_items16(a, d->dtype, p.mfw, 2, stream);
       break;
     case kVarSmallDense16:
     case kVarSmallKgs16: {

@@ -22,6 +22,8 @@ enum Variant : uint32_t {
   kVarSmallKgs16 = 6,    // KGS, c_in <= 4: as above over the union of the wave tile's items
   kVarKgsPair16 = 7,     // KGS, 2:4 sparse 16x16x64 MFMA over pairs of items no group keeps
                          // both of; compact weight stream (kept 4x4 blocks only)
+  kVarKgsBlockPair16 = 8,  // KGS, 2:4 sparse 16x16x64 MFMA over the channel-block pairs
+                           // (2i, 2i+1) at one position, one 16-byte LDS read each
 };
 
 // Voxel tiling shared by every conv kernel: a workgroup computes a brick of
@@ -128,7 +130,7 @@ void *noalloc_scratch();
 // Workgroups of the conv kernel for (variant, dtype, mfw, nf) that fit on one CU
 // with `lds` bytes of dynamic LDS each; 0 when the runtime cannot say.
 int conv_resident(int variant, int dtype, int mfw, int nf, size_t lds);
-int launch_items16(const ConvArgs &a, int dtype, int mfw, bool pair, void *stream);
+int launch_items16(const ConvArgs &a, int dtype, int mfw, int map, void *stream);
 int launch_small16(const ConvArgs &a, int dtype, int mfw, void *stream);
 size_t small_lds_bytes(const ConvArgs &a);
 int small_resident(const ConvArgs &a, int dtype, int mfw);

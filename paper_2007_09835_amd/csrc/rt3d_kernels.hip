@@ -190,7 +190,12 @@ struct SlotWalk {
 // Stage channels [c0, c0 + cc) of the input brick plus halo into LDS.
 // Row r of the halo (one input voxel) holds cc channels, zero where the
 // voxel is padding or the channel does not exist.
-template <int ES>
+// ILV (16-bit block-pair mapping): each 16-byte piece of 8 channels -- the
+// 4-channel blocks 2i and 2i + 1 -- is stored as dwords (c01, c45, c23, c67),
+// so one 16-byte read of a piece is the operand of a block pair.
+__device__ __forceinline__ uint4 interleave_blocks(uint4 v) { return make_uint4(v.x, v.z, v.y, v.w); }
+
+template <int ES, bool ILV = false>
 __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, const Brick &b,
                                            int c0) {
   constexpr int EPP = 16 / ES;                 // elements per 16-byte piece
@@ -226,6 +231,7 @@ __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, cons
         v = make_uint4(w[0], w[1], w[2], w[3]);
       }
     }
+    if constexpr (ILV) v = interleave_blocks(v);
     *reinterpret_cast<uint4 *>(lds + hv * a.row + piece * 16) = v;  // rows are 16-byte multiples
   }
 }
@@ -241,7 +247,7 @@ __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, cons
 // every piece is one 16-byte load from
 // a clamped, always valid address, and pieces that are padding are zeroed
 // at commit, so the loads issue back to back without branches.
-template <int ES, int MAXI, bool FAST = false>
+template <int ES, int MAXI, bool FAST = false, bool ILV = false>
 struct Stager {
   static constexpr int EPP = 16 / ES;
   int vox[MAXI];   // flat input voxel; -1 padding (zeros); -2 no piece
@@ -334,6 +340,7 @@ struct Stager {
         if constexpr (FAST) {
           if (!((live >> k) & 1u)) v = make_uint4(0, 0, 0, 0);
         }
+        if constexpr (ILV) v = interleave_blocks(v);
         *reinterpret_cast<uint4 *>(lds + (idx >> shift) * a.row + (idx & (ppr - 1)) * 16) = v;
       }
     }
@@ -578,15 +585,21 @@ __device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, co
 // ---------------------------------------------------------------------------
 
 // FAST: c_in is a multiple of 8 (branch-free halo staging).
-template <typename T, int MFW, int NF, bool FAST, bool PAIR = false>
+// MAP: 0 = dense / KGS union, 1 = pairs of any two items, 2 = block pairs.
+template <typename T, int MFW, int NF, bool FAST, int MAP = 0>
 __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
-  // PAIR with MFW > 1: 32- or 64-filter tiles share each B fragment; their
-  // weights and index registers stream in lane order (not compacted).
-  constexpr bool COMPACT = PAIR && MFW == 1;
+  constexpr bool PAIR = MAP != 0;
+  constexpr bool BPAIR = MAP == 2;
+  // Pairs of any two items on 16-filter tiles stream compact weights; wide
+  // pair tiles and block pairs stream weights and index registers in lane
+  // order.
+  constexpr bool COMPACT = MAP == 1 && MFW == 1;
   using V8 = std::conditional_t<std::is_same_v<T, __bf16>, bf16x8, f16x8>;
   using V16 = std::conditional_t<std::is_same_v<T, __bf16>, bf16x16, f16x16>;
   using BV = std::conditional_t<PAIR, V16, V8>;     // B fragment of one step
-  using OFF = std::conditional_t<PAIR, uint4, uint2>;  // LDS offsets of a lane group's items
+  // LDS offsets of a lane group's reads: 2 items (union), the X and Y items
+  // of 2 pairs (pairs), 2 block pairs (block pairs)
+  using OFF = std::conditional_t<MAP == 1, uint4, uint2>;
   // Software pipeline of a wave (step t = one K-step of 8 items):
   //   item offsets for step t+4 and the A operand for step t+2 are in flight
   //   from global memory, and the B fragments of step t+1 are read from LDS,
@@ -663,7 +676,13 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
   auto load_b = [&](int slot, OFF off) {
     #pragma unroll
     for (int j = 0; j < NF; ++j) {
-      if constexpr (PAIR) {
+      if constexpr (BPAIR) {
+        // One 16-byte read per block pair: the staged interleave makes it
+        // (X.c01, Y.c01, X.c23, Y.c23), the operand order.
+        const uint4 p0 = *reinterpret_cast<const uint4 *>(lds + vb[j] + off.x);
+        const uint4 p1 = *reinterpret_cast<const uint4 *>(lds + vb[j] + off.y);
+        rb[slot][j] = __builtin_bit_cast(V16, u32x8{p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w});
+      } else if constexpr (PAIR) {
         // Two 8-byte reads per pair; operand order is (X.c01, Y.c01, X.c23,
         // Y.c23).  Wide tiles keep the reads in load order (X.c01, X.c23,
         // Y.c01, Y.c23), landing in place, and swap them in the MFMA stage a
@@ -692,7 +711,7 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
     #pragma unroll
     for (int j = 0; j < NF; ++j) {
       BV bj = rb[slot][j];
-      if constexpr (PAIR && MFW > 1) {
+      if constexpr (MAP == 1 && MFW > 1) {
         // load order (X.c01, X.c23, Y.c01, Y.c23) -> quads (X.c01, Y.c01), (X.c23, Y.c23)
         u32x8 r = __builtin_bit_cast(u32x8, bj);
         bj = __builtin_bit_cast(V16, u32x8{r[0], r[2], r[1], r[3], r[4], r[6], r[5], r[7]});
@@ -725,7 +744,7 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
   const uint32_t S0 = uniform(sp[ch0]), S1 = uniform(sp[ch1]);
   const bool work = active && S1 > S0;
   const uint32_t LAST = work ? S1 - 1 : S0;
-  Stager<2, 8, FAST> st;
+  Stager<2, 8, FAST, BPAIR> st;
   st.init(a, b);
   if (st.ok && ch0 < ch1) st.issue(a, ch0 * a.cc);
   if (work) {
@@ -737,7 +756,7 @@ __global__ __launch_bounds__(256) void items16_kernel(ConvArgs a) {
   for (int ch = ch0; ch < ch1; ++ch) {
     __syncthreads();  // every wave is done with the previous chunk
     if (st.ok) st.commit(lds, a);
-    else stage_halo<2>(lds, a, b, ch * a.cc);
+    else stage_halo<2, BPAIR>(lds, a, b, ch * a.cc);
     __syncthreads();
     if (st.ok && ch + 1 < ch1) st.issue(a, (ch + 1) * a.cc);  // overlaps this chunk's MFMAs
     if (!work) continue;
@@ -1910,15 +1929,19 @@ int conv_resident(int variant, int dtype, int mfw, int nf, size_t lds) {
     case kVarKgsPair16:
       if (nf != 4) return 0;
       if (dtype == RT3D_BF16) {
-        if (mfw == 1) return resident(items16_kernel<__bf16, 1, 4, true, true>, lds);
-        if (mfw == 2) return resident(items16_kernel<__bf16, 2, 4, true, true>, lds);
-        if (mfw == 4) return resident(items16_kernel<__bf16, 4, 4, true, true>, lds);
+        if (mfw == 1) return resident(items16_kernel<__bf16, 1, 4, true, 1>, lds);
+        if (mfw == 2) return resident(items16_kernel<__bf16, 2, 4, true, 1>, lds);
+        if (mfw == 4) return resident(items16_kernel<__bf16, 4, 4, true, 1>, lds);
         return 0;
       }
-      if (mfw == 1) return resident(items16_kernel<_Float16, 1, 4, true, true>, lds);
-      if (mfw == 2) return resident(items16_kernel<_Float16, 2, 4, true, true>, lds);
-      if (mfw == 4) return resident(items16_kernel<_Float16, 4, 4, true, true>, lds);
+      if (mfw == 1) return resident(items16_kernel<_Float16, 1, 4, true, 1>, lds);
+      if (mfw == 2) return resident(items16_kernel<_Float16, 2, 4, true, 1>, lds);
+      if (mfw == 4) return resident(items16_kernel<_Float16, 4, 4, true, 1>, lds);
       return 0;
+    case kVarKgsBlockPair16:
+      if (nf != 4 || mfw != 1) return 0;
+      if (dtype == RT3D_BF16) return resident(items16_kernel<__bf16, 1, 4, true, 2>, lds);
+      return resident(items16_kernel<_Float16, 1, 4, true, 2>, lds);
     case kVarDenseItemsF32:
       if (nf == 4) {
         if (mfw == 1) return resident(items_f32_kernel<1, 4>, lds);
@@ -1992,16 +2015,26 @@ int small_resident(const ConvArgs &a, int dtype, int mfw) {
   return 0;
 }
 
-int launch_items16(const ConvArgs &a, int dtype, int mfw, bool pair, void *stream) {
+int launch_items16(const ConvArgs &a, int dtype, int mfw, int map, void *stream) {
   const bool fast = a.c_in % 8 == 0 && a.x_pitch % 8 == 0 && a.x_off % 8 == 0;
-  if (pair) {
+  if (map == 2) {
+    if (a.nf != 4 || mfw != 1) return hipErrorInvalidValue;
+    if (dtype == RT3D_BF16)
+      return fast ? launch_conv(items16_kernel<__bf16, 1, 4, true, 2>, a, stream)
+                  : launch_conv(items16_kernel<__bf16, 1, 4, false, 2>, a, stream);
+    if (dtype == RT3D_F16)
+      return fast ? launch_conv(items16_kernel<_Float16, 1, 4, true, 2>, a, stream)
+                  : launch_conv(items16_kernel<_Float16, 1, 4, false, 2>, a, stream);
+    return hipErrorInvalidValue;
+  }
+  if (map == 1) {
     // 64-slot bricks only: with eight fragments the doubled B ring would
     // leave one wave per SIMD.
     if (a.nf != 4) return hipErrorInvalidValue;
 #define RT3D_PAIR16(T, M)                                                                \
   do {                                                                                   \
-    return fast ? launch_conv(items16_kernel<T, M, 4, true, true>, a, stream)            \
-                : launch_conv(items16_kernel<T, M, 4, false, true>, a, stream);          \
+    return fast ? launch_conv(items16_kernel<T, M, 4, true, 1>, a, stream)               \
+                : launch_conv(items16_kernel<T, M, 4, false, 1>, a, stream);             \
   } while (0)
     if (dtype == RT3D_BF16) {
       if (mfw == 1) RT3D_PAIR16(__bf16, 1);

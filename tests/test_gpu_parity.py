@@ -531,7 +531,7 @@ def test_s3d_layers_full_size(li):
 # default, so it is forced through the tuning switch.
 # ---------------------------------------------------------------------------
 
-PAIR_TUNES = ["kgs_map=1", "kgs_map=1,pair_mfw=2", "kgs_map=1,pair_mfw=4"]
+PAIR_TUNES = ["kgs_map=2", "kgs_map=1", "kgs_map=1,pair_mfw=2", "kgs_map=1,pair_mfw=4"]
 
 
 @pytest.mark.parametrize("tune", PAIR_TUNES)
@@ -543,8 +543,8 @@ def test_pair_mapping_small_shapes(si, dtype, tune, monkeypatch):
     mask = masked(tag, c_out, c_in, k, min(keep, k[0] * k[1] * k[2]))
     case = LayerCase(tag + "p", n, c_in, c_out, thw, k, stride, pad, dtype, mask)
     if c_in > 4:
-        assert case.conv.info.variant == 7
-    check_full(case, f"pairs {tag} {dtype}")
+        assert case.conv.info.variant == (8 if tune == "kgs_map=2" else 7)
+    check_full(case, f"pairs {tag} {dtype} {tune}")
 
 
 @pytest.mark.parametrize("tune", PAIR_TUNES)
@@ -555,8 +555,8 @@ def test_pair_mapping_pooled_and_split(pi, tune, monkeypatch):
     mask = masked(tag, c_out, c_in, (3, 3, 3), 9)
     case = LayerCase(tag + "p", n, c_in, c_out, thw, (3, 3, 3), (1, 1, 1), (1, 1, 1),
                      "bf16" if dtype == "f32" else dtype, mask, residual=residual, pool=pool)
-    assert case.conv.info.variant == 7
-    check_full(case, f"pairs pooled {tag}")
+    assert case.conv.info.variant == (8 if tune == "kgs_map=2" else 7)
+    check_full(case, f"pairs pooled {tag} {tune}")
 
 
 @pytest.mark.parametrize("tune", PAIR_TUNES)
@@ -582,5 +582,5 @@ def test_pair_mapping_c3d_layers(li, variant, tune, monkeypatch):
             else synth.kgs_mask(r, *l.groups, l.ks, l.keep))
     case = LayerCase(f"pair-{variant}-{l.name}", 1, l.c_in, l.c_out, (l.t, l.h, l.w), l.k,
                      l.stride, l.pad, "bf16", mask)
-    assert case.conv.info.variant == 7
-    check_sampled(case, f"pairs c3d {variant} {l.name}", count=2000)
+    assert case.conv.info.variant == (8 if tune == "kgs_map=2" else 7)
+    check_sampled(case, f"pairs c3d {variant} {l.name} {tune}", count=2000)

@@ -32,7 +32,7 @@ def built():
     build.build(force=False)
 
 
-VAR_DENSE16, VAR_UNION16, VAR_PAIR16 = 1, 3, 7
+VAR_DENSE16, VAR_UNION16, VAR_PAIR16, VAR_BLOCKPAIR16 = 1, 3, 7, 8
 
 
 def _bf16_bits(rng, shape, dt):
@@ -93,6 +93,29 @@ def decode(desc, info, blob):
         assert not seen[m, c, pos], ("weight streamed twice", m, c, pos)
         seen[m, c, pos] = True
         out[m, c, pos] = v
+
+    if info.variant == VAR_BLOCKPAIR16:
+        idx_all = _u32(blob, p["keep"], (p["a"] - p["keep"]) // 4)
+        for wt in range(nwt):
+            for ch in range(nch):
+                for s in range(step_ptr[wt, ch], step_ptr[wt, ch + 1]):
+                    its = _u32(blob, p["items"] + 32 * s, 8)
+                    for lane in range(64):
+                        m = wt * 16 + (lane & 15)
+                        idx = int(idx_all[s * 64 + lane])
+                        for h in range(2):
+                            j = 2 * (lane >> 4) + h           # slot of this A half
+                            off = int(its[2 * (j % 4) + j // 4])
+                            ql, pos = _item(p, off, kh, kw)
+                            assert ql % 2 == 0, "block pairs start at an even channel block"
+                            sel = (idx >> (8 * h)) & 0xFF
+                            assert sel in (0x44, 0xEE), hex(sel)
+                            ql += 1 if sel == 0xEE else 0
+                            for c in range(4):
+                                streamed += 1
+                                put(m, 4 * (ch * (cc // 4) + ql) + c, pos,
+                                    int(a16[(s * 64 + lane) * 8 + 4 * h + c]))
+        return out, seen, streamed
 
     if info.variant == VAR_PAIR16 and p["mfw"] > 1:
         mfw = p["mfw"]
@@ -197,7 +220,7 @@ def _mask(rng, c_out, c_in, ks, g, keep):
     return m
 
 
-@pytest.mark.parametrize("tune", ["kgs_map=1", "kgs_map=1,pair_mfw=2", "kgs_map=1,pair_mfw=4",
+@pytest.mark.parametrize("tune", ["kgs_map=2", "kgs_map=1", "kgs_map=1,pair_mfw=2", "kgs_map=1,pair_mfw=4",
                                   "kgs_map=0,kgs_mfw=1", "kgs_map=0,kgs_mfw=2",
                                   "kgs_map=0,kgs_mfw=4", "kgs_map=0,kgs_mfw=1,slots=128"])
 @pytest.mark.parametrize("ci", range(len(CASES)))
@@ -212,7 +235,8 @@ def test_kgs_layout_decodes_to_masked_weights(dt, ci, tune, monkeypatch):
     desc = rt3d.make_desc(n, c_in, c_out, thw, k, stride, pad, g, dt)
     blob, info = rt3d.rt3d_kgs_pack(desc, w, mask)
     want_pair = tune.startswith("kgs_map=1")
-    assert info.variant == (VAR_PAIR16 if want_pair else VAR_UNION16), info.variant
+    want = {"kgs_map=1": VAR_PAIR16, "kgs_map=2": VAR_BLOCKPAIR16}.get(tune.split(",")[0], VAR_UNION16)
+    assert info.variant == want, info.variant
     got, seen, streamed = decode(desc, info, blob)
     exp, kept = expected(w, mask, g)
     assert got.tobytes() == exp.tobytes()
