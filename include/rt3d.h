@@ -40,8 +40,9 @@
  *     change the kernel layout written into a blob: slots=64|128 (voxel slots
  *     per workgroup), kgs_mfw=1|2|4 and dense_mfw=1|2|4 (16-filter MFMA rows
  *     per wave tile), small_mfw=1|2 and small_kernel=0 (the small-input-channel
- *     kernel), kgs_map=0|1 (16-bit KGS mapping: 0 = union of the tile's kept
- *     items, 1 = disjoint item pairs on the 2:4 sparse MFMA), pair_mfw=1|2|4
+ *     kernel), kgs_map=0|1|2 (16-bit KGS mapping: 0 = union of the tile's
+ *     kept items, 1 = disjoint item pairs on the 2:4 sparse MFMA, 2 = pairs
+ *     of adjacent channel blocks on the 2:4 sparse MFMA), pair_mfw=1|2|4
  *     (16-filter rows per pair-mapping tile), cc=N (at most N input channels
  *     per staged chunk, 16-bit).  Launch-time
  *     keys change the launch of a forward call: splits=N (input-channel
