@@ -283,3 +283,45 @@ def test_pair_stream_is_the_kept_weights_for_c3d_layers(monkeypatch):
         p = _plan(info)
         a_bytes = info.packed_bytes - p["a"]
         assert a_bytes <= info.canon_bytes[3] + 255, (l.name, a_bytes, info.canon_bytes[3])
+
+
+# ---------------------------------------------------------------------------
+# Randomised shapes: group sizes, partial groups, strides, paddings, kernel
+# extents and kept counts drawn by hypothesis, every mapping decoded.
+# ---------------------------------------------------------------------------
+
+from hypothesis import HealthCheck, given, settings, strategies as st  # noqa: E402
+
+MAPPINGS = ["kgs_map=0,kgs_mfw=1", "kgs_map=0,kgs_mfw=2", "kgs_map=0,kgs_mfw=4", "kgs_map=1",
+            "kgs_map=1,pair_mfw=2", "kgs_map=1,pair_mfw=4", "kgs_map=2"]
+
+
+@st.composite
+def _layer(draw):
+    g = draw(st.sampled_from([(4, 4), (8, 4), (16, 4), (4, 8), (16, 8)]))
+    c_in = draw(st.integers(5, 72))
+    c_out = draw(st.integers(1, 80))
+    k = draw(st.sampled_from([(3, 3, 3), (1, 3, 3), (3, 1, 1), (1, 1, 1), (1, 5, 5)]))
+    stride = draw(st.sampled_from([(1, 1, 1), (2, 2, 2), (1, 2, 2)]))
+    pad = tuple(kk // 2 for kk in k)
+    thw = (draw(st.integers(k[0], 6)), draw(st.integers(k[1], 9)), draw(st.integers(k[2], 9)))
+    ks = k[0] * k[1] * k[2]
+    keep = draw(st.integers(0, ks))
+    return c_in, c_out, thw, k, stride, pad, g, keep
+
+
+@settings(max_examples=80, deadline=None, suppress_health_check=[HealthCheck.function_scoped_fixture])
+@given(case=_layer(), tune=st.sampled_from(MAPPINGS), dt=st.sampled_from(["bf16", "f16"]),
+       seed=st.integers(0, 2**31 - 1))
+def test_random_layers_decode_to_masked_weights(case, tune, dt, seed, monkeypatch):
+    monkeypatch.setenv("RT3D_TUNE", tune)
+    c_in, c_out, thw, k, stride, pad, g, keep = case
+    rng = np.random.default_rng(seed)
+    w = _bf16_bits(rng, (c_out, c_in, *k), dt)
+    mask = _mask(rng, c_out, c_in, k[0] * k[1] * k[2], g, keep)
+    desc = rt3d.make_desc(1, c_in, c_out, thw, k, stride, pad, g, dt)
+    blob, info = rt3d.rt3d_kgs_pack(desc, w, mask)
+    got, seen, _ = decode(desc, info, blob)
+    exp, kept = expected(w, mask, g)
+    assert got.tobytes() == exp.tobytes()
+    assert np.array_equal(seen, kept & (exp != 0))
