@@ -44,7 +44,8 @@
  *     kept items, 1 = disjoint item pairs on the 2:4 sparse MFMA, 2 = pairs
  *     of adjacent channel blocks on the 2:4 sparse MFMA), pair_mfw=1|2|4
  *     (16-filter rows per pair-mapping tile), cc=N (at most N input channels
- *     per staged chunk, 16-bit).  Launch-time
+ *     per staged chunk, 16-bit), kgs_f32=0|1 (fp32 KGS: exact 4x4 blocks or
+ *     the union of a 16-filter tile's items).  Launch-time
  *     keys change the launch of a forward call: splits=N (input-channel
  *     splits) and wg_order=0|1 (workgroup order).  Results stay within the
  *     documented accuracy under every setting.

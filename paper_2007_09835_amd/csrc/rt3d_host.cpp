@@ -617,7 +617,8 @@ void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
   const bool dense = m4 == nullptr;
   const int wt_count = (g.c_out + 16 * mfw - 1) / (16 * mfw);
   L.variant = small ? (dense ? kVarSmallDense16 : kVarSmallKgs16)
-                    : (dense ? (f32 ? kVarDenseItemsF32 : kVarDenseItems16) : kVarKgsUnion16);
+                    : (dense ? (f32 ? kVarDenseItemsF32 : kVarDenseItems16)
+                             : (f32 ? kVarKgsUnionF32 : kVarKgsUnion16));
   L.plan.mfw = mfw;
   L.plan.wave_tiles = wt_count;
   L.plan.items_per_step = ips;
@@ -1186,6 +1187,23 @@ bool use_pairs(const Geom &g, const Mask4 *m4) {
   return tune("kgs_map") == 1;
 }
 
+// fp32 KGS: the exact 4x4x1 kernel (only kept blocks are multiplied; one
+// loop iteration per item), or the dense 16x16x4 kernel over the union of
+// each 16-filter tile's kept items (pruned entries multiplied as zeros; one
+// iteration per four items).  The exact kernel wins whenever its MFMA work
+// matters (config 2, 256->256: 162 against 220 us; every C3D layer); a layer
+// whose kept MACs take under 5 us at the exact kernel's measured rate
+// (71 TMAC/s) is bound by per-iteration latency instead, and there the
+// union's four-fold fewer iterations win (config 1, 16->32 on 8x28x28:
+// 18.1 -> 12.4 us, below the dense kernel's 13.7).  Tuning switch kgs_f32=0|1.
+bool use_f32_union(const Geom &g, uint64_t kept_weights) {
+  if (g.es != 4) return false;
+  const int v = tune("kgs_f32");
+  if (v == 0 || v == 1) return v == 1;
+  const double voxels = static_cast<double>(std::max(g.n, 1)) * g.to * g.ho * g.wo;
+  return voxels * static_cast<double>(kept_weights) / 71e12 < 5e-6;
+}
+
 // Block pairs: tuning switch kgs_map=2.
 bool use_block_pairs(const Geom &g, const Mask4 *m4) {
   (void)m4;
@@ -1229,13 +1247,14 @@ rt3d_status plan_kgs(const rt3d_conv3d_desc *d, const uint8_t *mask, const uint8
     // The layout size does not depend on weight values.
   }
   if (g.es == 4) {
+    std::vector<uint8_t> scratch;
     if (!w) {
       // size-only pass: reuse the builders with a scratch weight tensor
-      std::vector<uint8_t> scratch(static_cast<size_t>(g.c_out) * g.c_in * ks * g.es, 0);
-      build_exact_f32_layout(g, tl, scratch.data(), &m4, L);
-    } else {
-      build_exact_f32_layout(g, tl, wsrc, &m4, L);
+      scratch.assign(static_cast<size_t>(g.c_out) * g.c_in * ks * g.es, 0);
+      wsrc = scratch.data();
     }
+    if (use_f32_union(g, c.nvals)) build_items_layout(g, tl, wsrc, &m4, L, false, 1);
+    else build_exact_f32_layout(g, tl, wsrc, &m4, L);
   } else {
     std::vector<uint8_t> scratch;
     if (!w) {
@@ -1270,6 +1289,7 @@ rt3d_status check_info(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, bo
   if (info->desc_hash != desc_hash(d))
     return fail(RT3D_ERR_BLOB_MISMATCH, "blob was packed for a different layer description");
   const bool is_sparse = info->variant == kVarKgsUnion16 || info->variant == kVarKgsExactF32 ||
+                         info->variant == kVarKgsUnionF32 ||
                          info->variant == kVarSmallKgs16 || info->variant == kVarKgsPair16 ||
                          info->variant == kVarKgsBlockPair16;
   if (is_sparse != sparse)
@@ -1552,6 +1572,7 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
       break;
     }
     case kVarDenseItemsF32:
+    case kVarKgsUnionF32:
       e = launch_items_f32(a, p.mfw, stream);
       break;
     case kVarKgsExactF32:

@@ -24,6 +24,7 @@ enum Variant : uint32_t {
                          // both of; compact weight stream (kept 4x4 blocks only)
   kVarKgsBlockPair16 = 8,  // KGS, 2:4 sparse 16x16x64 MFMA over the channel-block pairs
                            // (2i, 2i+1) at one position, one 16-byte LDS read each
+  kVarKgsUnionF32 = 9,   // KGS, 16x16x4 f32 MFMA over the union of a 16-filter tile's items
 };
 
 // Voxel tiling shared by every conv kernel: a workgroup computes a brick of

@@ -1946,6 +1946,7 @@ int conv_resident(int variant, int dtype, int mfw, int nf, size_t lds) {
       if (dtype == RT3D_BF16) return resident(items16_kernel<__bf16, 1, 4, true, 2>, lds);
       return resident(items16_kernel<_Float16, 1, 4, true, 2>, lds);
     case kVarDenseItemsF32:
+    case kVarKgsUnionF32:
       if (nf == 4) {
         if (mfw == 1) return resident(items_f32_kernel<1, 4>, lds);
         if (mfw == 2) return resident(items_f32_kernel<2, 4>, lds);

@@ -98,9 +98,12 @@ def test_canonical_pack_matches_oracle_bitwise(ci, dt):
     assert out.tobytes() == expect.tobytes()
 
 
-def test_pack_never_reads_pruned_weights():
+@pytest.mark.parametrize("tune", ["kgs_f32=0", "kgs_f32=1"])
+def test_pack_never_reads_pruned_weights(tune, monkeypatch):
     """Pruned positions hold NaN; the blob must be identical to packing the
-    zero-filled weights (except nothing reads them at all)."""
+    zero-filled weights (except nothing reads them at all), for the exact
+    fp32 layout and the fp32 union layout."""
+    monkeypatch.setenv("RT3D_TUNE", tune)
     rng = np.random.default_rng(5)
     w = rng.standard_normal((16, 8, 3, 3, 3)).astype(np.float32)
     mask = (rng.random((4, 2, 27)) < 0.3).astype(np.uint8)
@@ -110,6 +113,7 @@ def test_pack_never_reads_pruned_weights():
     for dt_w in (w_nan, w_zero):
         desc = rt3d.make_desc(1, 8, 16, (4, 4, 4), dtype="f32")
         blob, info = rt3d.rt3d_kgs_pack(desc, dt_w, mask)
+        assert info.variant == (9 if tune.endswith("1") else 4)
         if dt_w is w_nan:
             b_nan = blob
         else:

@@ -89,6 +89,20 @@ def test_kgs_small_shapes(si, dtype):
     check_full(case, f"kgs {tag} {dtype}")
 
 
+@pytest.mark.parametrize("tune", ["kgs_f32=0", "kgs_f32=1"])
+@pytest.mark.parametrize("si", range(len(SHAPES)))
+def test_f32_kgs_both_mappings(si, tune, monkeypatch):
+    """fp32 KGS on the exact 4x4x1 kernel (kgs_f32=0) and on the 16x16x4
+    kernel over the tile's union of kept items (kgs_f32=1), forced; the
+    planner picks the union only for layers too small to be MFMA-bound."""
+    monkeypatch.setenv("RT3D_TUNE", tune)
+    tag, n, c_in, c_out, thw, k, stride, pad, keep = SHAPES[si]
+    mask = masked(tag, c_out, c_in, k, min(keep, k[0] * k[1] * k[2]))
+    case = LayerCase(tag + "f" + tune[-1], n, c_in, c_out, thw, k, stride, pad, "f32", mask)
+    assert case.conv.info.variant == (9 if tune.endswith("1") else 4)
+    check_full(case, f"kgs f32 {tag} {tune}")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 @pytest.mark.parametrize("si", range(len(SHAPES)))
 def test_dense_small_shapes(si, dtype):
