@@ -200,8 +200,9 @@ rt3d_status rt3d_conv3d_workspace_size(const rt3d_conv3d_desc *desc,
  * pruned group costs nothing when its tile-mates prune the same channels).
  * How a kept item is multiplied depends on the mapping chosen at pack time:
  * the exact fp32 kernel issues one 4x4 MFMA per kept (group, item); the
- * 16-bit union mapping multiplies the tile's other groups at that item by
- * zero weights; the 16-bit pair mapping packs two items whose kept groups
+ * union mappings (16-bit, and fp32 for layers too small to be bound by
+ * their MFMA work) multiply the tile's other groups at that item by zero
+ * weights; the 16-bit pair mapping packs two items whose kept groups
  * are disjoint into one 2:4 sparse MFMA slot and streams kept weights only.
  * Asynchronous on `stream`.  Per-call limits (RT3D_ERR_UNSUPPORTED,
  * checked before any launch; the same for rt3d_conv3d_dense_fwd): fewer
