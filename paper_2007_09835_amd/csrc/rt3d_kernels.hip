@@ -472,6 +472,15 @@ __device__ __forceinline__ float4 shfl_xor4(float4 v, int m) {
 
 
 // r[k] <- r[(k + by) % R] for a wave-uniform 0 <= by < R.
+// Every lane of a quad takes lane P of the quad's value (DPP quad_perm).
+template <int P>
+__device__ __forceinline__ uint2 quad_bcast(uint2 v) {
+  constexpr int ctrl = P | (P << 2) | (P << 4) | (P << 6);
+  return make_uint2(
+      static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v.x), ctrl, 0xF, 0xF, false)),
+      static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v.y), ctrl, 0xF, 0xF, false)));
+}
+
 template <int R, typename X>
 __device__ __forceinline__ void rotate_ring(X (&r)[R], int by) {
   static_for<R - 1>([&](auto kc) {
@@ -586,11 +595,12 @@ __device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, co
 
 // FAST: c_in is a multiple of 8 (branch-free halo staging).
 // MAP: 0 = dense / KGS union, 1 = pairs of any two items, 2 = block pairs.
-// The pair mappings ask for two waves per SIMD: left to itself the compiler
-// spends registers down to one wave (the index registers ride with A), and
-// a lone wave cannot hide its LDS reads behind the other's MFMAs.
+// The pair mappings and the 64-slot tiles ask for two waves per SIMD: left
+// to itself the compiler spends registers down to one wave (the pairs' index
+// registers ride with A; the union's unrolled passes lengthen live ranges),
+// and a lone wave cannot hide its LDS reads behind the other's MFMAs.
 template <typename T, int MFW, int NF, bool FAST, int MAP = 0>
-__global__ __launch_bounds__(256, MAP != 0 ? 2 : 1) void items16_kernel(ConvArgs a) {
+__global__ __launch_bounds__(256, (MAP != 0 || NF == 4) ? 2 : 1) void items16_kernel(ConvArgs a) {
   constexpr bool PAIR = MAP != 0;
   constexpr bool BPAIR = MAP == 2;
   // Pairs of any two items on 16-filter tiles stream compact weights; wide
@@ -604,9 +614,10 @@ __global__ __launch_bounds__(256, MAP != 0 ? 2 : 1) void items16_kernel(ConvArgs
   // of 2 pairs (pairs), 2 block pairs (block pairs)
   using OFF = std::conditional_t<MAP == 1, uint4, uint2>;
   // Software pipeline of a wave (step t = one K-step of 8 items):
-  //   item offsets for step t+4 and the A operand for step t+2 are in flight
-  //   from global memory, and the B fragments of step t+1 are read from LDS,
-  //   while the MFMAs of step t run.  Rings: offsets 4, A 2, B 2.
+  //   item offsets four or more steps ahead and the A operand for step t+2
+  //   are in flight from global memory, and the B fragments of step t+1 are
+  //   read from LDS, while the MFMAs of step t run.  Rings: A 2, B 2;
+  //   offsets 4 (pair mappings) or two blocks of four steps (union / dense).
   extern __shared__ __align__(16) uint8_t lds[];
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
@@ -740,9 +751,11 @@ __global__ __launch_bounds__(256, MAP != 0 ? 2 : 1) void items16_kernel(ConvArgs
   int ch0, ch1;
   split_range(a, wg.split, ch0, ch1);
   // The wave's steps over all chunks of its split form one stream
-  // [S0, S1): item offsets and A are prefetched along it straight across
-  // chunk boundaries (indices clamped to the last step: a harmless re-read,
-  // so the loop body stays straight-line and the wait counters exact).
+  // [S0, S1) (indices clamped to the last step: a harmless re-read, so the
+  // loop bodies stay straight-line and the wait counters exact).  The pair
+  // mappings prefetch offsets and A along it straight across chunk
+  // boundaries; union / dense reload the next chunk's first offsets and A
+  // slots at each chunk's end, so that their step tail can run branch-free.
   // Only the B fragments wait for a new chunk to reach LDS.
   const uint32_t S0 = uniform(sp[ch0]), S1 = uniform(sp[ch1]);
   const bool work = active && S1 > S0;
@@ -750,9 +763,25 @@ __global__ __launch_bounds__(256, MAP != 0 ? 2 : 1) void items16_kernel(ConvArgs
   Stager<2, 8, FAST, BPAIR> st;
   st.init(a, b);
   if (st.ok && ch0 < ch1) st.issue(a, ch0 * a.cc);
+  // Union / dense: the item offsets travel in blocks of four steps.  Lane
+  // (n, g) of a block holds the two offsets of step base + (n & 3) for its
+  // lane group g, and a quad broadcast (DPP) hands step base + d to all four
+  // lanes of a quad, so one load serves four steps.  ob[0] and ob[1] hold
+  // the blocks at chunk-relative steps 0 and 4 of each group of eight.
+  uint2 ob[2];
+  const uint2 *ITB = reinterpret_cast<const uint2 *>(a.items) + g;
+  auto fetch_blk = [&](int slot, uint32_t base) {
+    const uint32_t sl = min(base + static_cast<uint32_t>(lane & 3), LAST);
+    ob[slot] = ITB[(static_cast<long>(row0) + (sl - step0)) * 4];
+  };
   if (work) {
+    if constexpr (MAP == 0) {
+      fetch_blk(0, S0);
+      fetch_blk(1, S0 + 4);
+    } else {
 #pragma unroll
-    for (int d = 0; d < 4; ++d) fetch_off(d, min(S0 + d, LAST));
+      for (int d = 0; d < 4; ++d) fetch_off(d, min(S0 + d, LAST));
+    }
 #pragma unroll
     for (int d = 0; d < 2; ++d) fetch_a(d, min(S0 + d, LAST), d);
   }
@@ -765,6 +794,58 @@ __global__ __launch_bounds__(256, MAP != 0 ? 2 : 1) void items16_kernel(ConvArgs
     if (!work) continue;
     const uint32_t s_beg = uniform(sp[ch]), s_end = uniform(sp[ch + 1]);
     if (s_beg == s_end) continue;
+    if constexpr (MAP == 0) {
+      // Local step i: A slot i&1, B slot i&1, offsets from block (i >> 2) & 1
+      // at quad position i & 3.  Eight steps per pass; block 0 is refilled
+      // after its last use (step 3) with steps 8..11, block 1 after step 7
+      // with steps 12..15.
+      load_b(0, quad_bcast<0>(ob[0]));
+      uint32_t s = s_beg;
+      for (; s + 8 <= s_end; s += 8) {
+        static_for<8>([&](auto dc) {
+          constexpr int D = decltype(dc)::value;
+          load_b((D + 1) & 1, quad_bcast<(D + 1) & 3>(ob[((D + 1) >> 2) & 1]));
+          mma(D & 1);
+          fetch_a(D & 1, min(s + D + 2, LAST), 0);
+          if constexpr (D == 3) fetch_blk(0, s + 8);
+          if constexpr (D == 7) fetch_blk(1, s + 12);
+          __builtin_amdgcn_sched_barrier(0);
+        });
+      }
+      // 0..7 steps remain: one pass of four when at least four do, then up
+      // to three.  The last three issue every load whether or not its step
+      // exists (addresses clamped; unused data is never read) and only their
+      // MFMAs depend on the step count, so their waits stay exact.
+      const uint32_t rem = s_end - s;
+      if (rem >= 4) {
+        static_for<4>([&](auto dc) {
+          constexpr int D = decltype(dc)::value;
+          load_b((D + 1) & 1, quad_bcast<(D + 1) & 3>(ob[(D + 1) >> 2]));
+          mma(D & 1);
+          fetch_a(D & 1, min(s + D + 2, LAST), 0);
+          __builtin_amdgcn_sched_barrier(0);
+        });
+        s += 4;
+      }
+      const bool hi = rem >= 4;
+      const uint2 b0 = ob[0], b1 = ob[1];
+      const uint2 blk = make_uint2(hi ? b1.x : b0.x, hi ? b1.y : b0.y);
+      const uint32_t r = rem & 3;
+      static_for<3>([&](auto dc) {
+        constexpr int D = decltype(dc)::value;
+        if constexpr (D < 2) load_b((D + 1) & 1, quad_bcast<D + 1>(blk));
+        if (D < r) mma(D & 1);
+        if constexpr (D == 0) fetch_a(0, min(s + 2, LAST), 0);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      // The next chunk starts at s_end: load its first A slots and offset
+      // blocks now (they land during the chunk barrier).
+      fetch_a(0, min(s_end, LAST), 0);
+      fetch_a(1, min(s_end + 1, LAST), 0);
+      fetch_blk(0, s_end);
+      fetch_blk(1, s_end + 4);
+      continue;
+    }
     // Ring slots are relative to the chunk's first step: offsets slot i&3,
     // A slot i&1, B slot i&1 for local step i.
     load_b(0, roff[0]);
