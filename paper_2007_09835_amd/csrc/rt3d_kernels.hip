@@ -291,6 +291,9 @@ struct Stager {
       unsigned bits = 0;
 #pragma unroll
       for (int k = 0; k < MAXI; ++k) {
+        // Rounds k with no piece in the whole workgroup issue no load (a
+        // uniform branch: the halo size is the same for every thread).
+        if (k * static_cast<int>(blockDim.x) >= total) break;
         const int idx = threadIdx.x + k * blockDim.x;
         const int c = c0 + (idx & (ppr - 1)) * EPP;
         const bool in = vox[k] >= 0 && c < a.c_in;
