@@ -598,3 +598,51 @@ def test_pair_mapping_c3d_layers(li, variant, tune, monkeypatch):
                      l.stride, l.pad, "bf16", mask)
     assert case.conv.info.variant == (8 if tune == "kgs_map=2" else 7)
     check_sampled(case, f"pairs c3d {variant} {l.name} {tune}", count=2000)
+
+
+# ---------------------------------------------------------------------------
+# Step counts of every residue: a chunk of the 16-bit union kernel runs
+# eight-step passes, at most one four-step pass and a three-step tail whose
+# loads are unconditional; each 16-filter tile below keeps exactly 8 n - r
+# items (all four groups keep the same ones), so its chunks take n steps for
+# n = 1..16, 20 and 27 and every n mod 8.
+# ---------------------------------------------------------------------------
+
+STEP_COUNTS = [1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16, 20, 27]
+
+
+def step_count_mask(c_in, chunk_q, seed):
+    """KGS mask [P][Q][27] where tile t keeps, in every chunk of chunk_q
+    channel groups, exactly 8 n_t - (t % 8) items (n_t = STEP_COUNTS[t],
+    at least one item); the four groups of a tile share their items."""
+    rng = np.random.default_rng(seed)
+    P, Q = 4 * len(STEP_COUNTS), c_in // 4
+    mask = np.zeros((P, Q, 27), dtype=np.uint8)
+    for t, n in enumerate(STEP_COUNTS):
+        for q0 in range(0, Q, chunk_q):
+            slots = chunk_q * 27
+            k = max(1, min(slots, 8 * n - (t % 8)))
+            pick = rng.choice(slots, size=k, replace=False)
+            for s in pick:
+                mask[4 * t:4 * t + 4, q0 + s // 27, s % 27] = 1
+    return mask
+
+
+@pytest.mark.parametrize("tune", ["kgs_mfw=1", "kgs_mfw=2", "kgs_mfw=4"])
+@pytest.mark.parametrize("c_in", [32, 64])
+def test_union_every_step_count(c_in, tune, monkeypatch):
+    """Union tiles whose chunks take 1..16, 20 and 27 K-steps (every
+    residue mod 8, below and above the eight-step pass), one or two channel
+    chunks, 16/32/64-filter tiles, in full against the oracle; with a
+    workspace the two-chunk layer also runs split (the second split starts
+    mid-stream)."""
+    monkeypatch.setenv("RT3D_TUNE", tune + ",cc=32")
+    mask = step_count_mask(c_in, 8, 1000 + c_in)
+    c_out = 4 * mask.shape[0]
+    case = LayerCase(f"steps{c_in}{tune[-1]}", 1, c_in, c_out, (3, 5, 6), (3, 3, 3), (1, 1, 1),
+                     (1, 1, 1), "bf16", mask)
+    assert case.conv.info.variant == 3
+    got, ref = check_full(case, f"union step counts c_in={c_in} {tune}")
+    x = to_device_ndhwc(case.x_t)
+    unsplit = from_device_ndhwc(case.conv(x, None, use_workspace=False))
+    assert_within_bound(unsplit, ref, case.bound_full(ref), f"unsplit {c_in} {tune}")
