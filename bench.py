@@ -176,10 +176,10 @@ def library_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(layer, net="c3d", batch=1, mode="kgs", dtype="bf16"):
-    """HBM bytes per launch of `layer`'s conv (and split reduction) from the
-    committed rocprofv3 FETCH_SIZE / WRITE_SIZE summaries, or None when no
-    summary exists for it or the kernels changed since it was taken."""
+def measured_profile(layer, net="c3d", batch=1, mode="kgs", dtype="bf16"):
+    """The committed rocprofv3 summary row of `layer` (HBM bytes per launch of
+    its conv and split reduction, MFMA work executed over kept), or None when
+    no summary exists for it or the kernels changed since it was taken."""
     import glob
     want = {"layer": layer, "net": net, "batch": batch, "mode": mode, "dtype": dtype,
             "source_hash": library_source_hash()}
@@ -189,8 +189,14 @@ def measured_traffic(layer, net="c3d", batch=1, mode="kgs", dtype="bf16"):
                 if line.startswith("traffic-json:"):
                     d = json.loads(line.split(":", 1)[1])
                     if all(d.get(k) == v for k, v in want.items()):
-                        return d["traffic_bytes_per_launch"]
+                        return d
     return None
+
+
+def measured_traffic(layer, net="c3d", batch=1, mode="kgs", dtype="bf16"):
+    """HBM bytes per launch of `layer`'s conv (and split reduction), or None."""
+    d = measured_profile(layer, net, batch, mode, dtype)
+    return None if d is None else d["traffic_bytes_per_launch"]
 
 
 def profile_layer(args, torch, stream):
@@ -580,7 +586,7 @@ def suite(args, torch, stream):
     md = ["# Measurement suite (MI355X, one GPU)", "",
           "Latencies are per launch from HIP events (p10 / p50 / p90 over %d launches); warm = "
           "back-to-back launches, cold = 1 GiB written before each launch. Dense-equivalent "
-          "TFLOP/s = 2 x dense MACs / time; executed = 2 x kept MACs / time." % iters, "",
+          "TFLOP/s = 2 x dense MACs / time; kept = 2 x kept MACs / time." % iters, "",
           "Command: `python bench.py --suite <path>`", ""]
     cores_all = oracle.num_threads()
 
@@ -642,7 +648,7 @@ def suite(args, torch, stream):
                 rows.append({"config": cname, "dtype": dtype, "variant": "KGS" if sparse else "dense",
                              "warm": warm, "cold": cold, "relL2": err, "oracle_outputs": n_or,
                              "dense_eq_tflops": 2 * dense_macs / warm["p50"] / 1e9,
-                             "executed_tflops": 2 * kept / warm["p50"] / 1e9,
+                             "kept_tflops": 2 * kept / warm["p50"] / 1e9,
                              "rate": dense_macs / kept,
                              "oracle_s_all_threads_per_output": t_all / n_or,
                              "oracle_s_one_thread_per_output": t_one / len(idx1)})
@@ -650,12 +656,12 @@ def suite(args, torch, stream):
                     (cname, dtype, rows[-1]["variant"], warm["p50"], cold["p50"], err))
     out["configs"]["1-2"] = rows
     md += ["## Configs 1 and 2: single layers", "",
-           "| cfg | dtype | variant | R | warm p10/p50/p90 ms | cold p50 ms | dense-eq TF | executed TF | relL2 vs oracle | oracle us/output (%d thr / 1 thr) |" % cores_all,
+           "| cfg | dtype | variant | R | warm p10/p50/p90 ms | cold p50 ms | dense-eq TF | kept TF | relL2 vs oracle | oracle us/output (%d thr / 1 thr) |" % cores_all,
            "|---|---|---|---|---|---|---|---|---|---|"]
     for r in rows:
         md.append("| %s | %s | %s | %.2f | %.4f / %.4f / %.4f | %.4f | %.1f | %.1f | %.2e (%d outputs) | %.2f / %.2f |" % (
             r["config"], r["dtype"], r["variant"], r["rate"], r["warm"]["p10"], r["warm"]["p50"],
-            r["warm"]["p90"], r["cold"]["p50"], r["dense_eq_tflops"], r["executed_tflops"], r["relL2"],
+            r["warm"]["p90"], r["cold"]["p50"], r["dense_eq_tflops"], r["kept_tflops"], r["relL2"],
             r["oracle_outputs"], 1e6 * r["oracle_s_all_threads_per_output"],
             1e6 * r["oracle_s_one_thread_per_output"]))
     md.append("")
@@ -875,16 +881,16 @@ def main():
             "ms_sparse": lay_s[i], "ms_dense": lay_d[i], "rate": r,
             "speedup": lay_d[i] / lay_s[i], "speedup_over_rate": lay_d[i] / lay_s[i] / r,
             "dense_equiv_tflops": 2 * macs_dense / lay_s[i] / 1e9,
-            "executed_tflops": 2 * kept / lay_s[i] / 1e9,
+            "kept_tflops": 2 * kept / lay_s[i] / 1e9,
             "dense_kernel_tflops": 2 * macs_dense / lay_d[i] / 1e9,
             "roofline_sparse": layer_roofline(l, sparse.convs[i], args.batch, lay_s[i]),
             "roofline_dense": layer_roofline(dense.layers[i], dense.convs[i], args.batch, lay_d[i]),
         })
         row = rows[-1]
-        log("%-10s %5d->%-5d R=%.2f  kgs %.4f ms (%.0f/%.0f TF eq/exec, %.3f of %s roofline)  "
+        log("%-10s %5d->%-5d R=%.2f  kgs %.4f ms (%.0f/%.0f TF eq/kept, %.3f of %s roofline)  "
             "dense %.4f ms (%.0f TF, %.3f)  speedup %.2f (%.2f R)" % (
                 l.name, l.c_in, l.c_out, r, lay_s[i], row["dense_equiv_tflops"],
-                row["executed_tflops"], row["roofline_sparse"]["frac"],
+                row["kept_tflops"], row["roofline_sparse"]["frac"],
                 row["roofline_sparse"]["bound"], lay_d[i], row["dense_kernel_tflops"],
                 row["roofline_dense"]["frac"], row["speedup"], row["speedup_over_rate"]))
 
@@ -896,12 +902,19 @@ def main():
                         if drow["kgs"] else l.dense_macs(args.batch))
     achieved = kept_flops / (drow["ms_sparse"] * 1e-3) / 1e12
     peak = PEAK_TFLOPS[args.dtype]
-    traffic = (measured_traffic(l.name, args.net, args.batch, args.mode, args.dtype)
-               if group_of(args) == (4, 4) else None)
+    prof = (measured_profile(l.name, args.net, args.batch, args.mode, args.dtype)
+            if group_of(args) == (4, 4) else None)
+    traffic = None if prof is None else prof["traffic_bytes_per_launch"]
+    # MFMA work the kernel executes (the union's zero weights included) over
+    # the kept MACs, from the same counter summary (SQ_INSTS_MFMA).
+    exec_over_kept = None if prof is None else prof.get("mfma_exec_over_kept")
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": traffic,
                 "kernel": "%s conv (%s)" % (l.name, "KGS" if drow["kgs"] else "dense"),
-                "flops_per_launch": kept_flops}
+                "flops_per_launch": kept_flops,
+                "mfma_exec_over_kept": exec_over_kept,
+                "mfma_executed_tflops": (None if exec_over_kept is None
+                                         else round(achieved * exec_over_kept, 2))}
 
     dense_flops = 2.0 * sparse.dense_macs()
     value = dense_flops / (ms_sparse * 1e-3) / 1e12
@@ -927,7 +940,7 @@ def main():
             "batch": args.batch, "clip": list(clip_thw), "pruning_rate": round(rate, 4),
         },
         "ms_per_clip": round(ms_sparse / args.batch, 5),
-        "executed_tflops": round(dense_flops / rate / (ms_sparse * 1e-3) / 1e12, 3),
+        "kept_tflops": round(dense_flops / rate / (ms_sparse * 1e-3) / 1e12, 3),
         "dense_ms_per_step": round(ms_dense, 5),
         "dense_tflops": round(dense_flops / (ms_dense * 1e-3) / 1e12, 3),
         "speedup_vs_dense": round(ms_dense / ms_sparse, 4),
