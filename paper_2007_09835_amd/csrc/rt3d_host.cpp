@@ -368,8 +368,12 @@ Tiling layer_tiling(const Geom &g) {
 struct Mask4 {
   const uint8_t *mask;
   int Q, ks, gm4, gn4;  // gm4 = g_m / 4
+  // Optional order of the 4-filter blocks (g_m = 4 only): block p4 of the
+  // layout is block perm[p4] of the layer.
+  const int32_t *perm = nullptr;
   bool kept(int p4, int q4, int pos) const {
-    return mask[(static_cast<size_t>(p4 / gm4) * Q + q4 / gn4) * ks + pos] == 1;
+    const int p = perm ? perm[p4] : p4;
+    return mask[(static_cast<size_t>(p / gm4) * Q + q4 / gn4) * ks + pos] == 1;
   }
 };
 
@@ -392,7 +396,8 @@ struct WeightSource {
   const Mask4 *m4;  // nullptr for dense
   void copy(uint8_t *dst, int m, int c, int pos) const {
     if (m < g.c_out && c < g.c_in && (!m4 || m4->kept(m / 4, c / 4, pos))) {
-      const size_t idx = (static_cast<size_t>(m) * g.c_in + c) * g.ks + pos;
+      const int mo = m4 && m4->perm ? 4 * m4->perm[m / 4] + (m & 3) : m;  // layer filter
+      const size_t idx = (static_cast<size_t>(mo) * g.c_in + c) * g.ks + pos;
       std::memcpy(dst, w + idx * g.es, g.es);
     } else {
       std::memset(dst, 0, g.es);
@@ -607,8 +612,101 @@ ItemPlan item_plan(const Geom &g, const Mask4 *m4, bool small) {
   return ip;
 }
 
+// Order of the 4-filter blocks for a 16-bit union layout (g_m = 4): the
+// blocks that share a wave tile should keep many of the same (channel block,
+// position) items, since the tile multiplies the union of its blocks' items.
+// Greedy (each tile grows by the block that adds the fewest new items to its
+// union), then swaps of two blocks between two tiles that shrink the sum of
+// the unions (a fixed pseudo-random sequence of candidate swaps, so packing
+// is deterministic).  Returns layout block -> layer block, c_out / 4 entries.
+std::vector<int32_t> cluster_blocks(const Geom &g, const Mask4 &m4, int tile_blocks) {
+  const int P4 = g.c_out / 4, Q4 = (g.c_in + 3) / 4;
+  const int words = (Q4 * g.ks + 63) / 64;
+  std::vector<uint64_t> bits(static_cast<size_t>(P4) * words, 0);
+  for (int p = 0; p < P4; ++p)
+    for (int q = 0; q < Q4; ++q)
+      for (int pos = 0; pos < g.ks; ++pos)
+        if (m4.kept(p, q, pos)) {
+          const int b = q * g.ks + pos;
+          bits[static_cast<size_t>(p) * words + b / 64] |= 1ull << (b % 64);
+        }
+  auto row = [&](int p) { return &bits[static_cast<size_t>(p) * words]; };
+  auto union_size = [&](const int32_t *members, int n) {
+    int total = 0;
+    for (int w = 0; w < words; ++w) {
+      uint64_t u = 0;
+      for (int k = 0; k < n; ++k) u |= row(members[k])[w];
+      total += __builtin_popcountll(u);
+    }
+    return total;
+  };
+  std::vector<int32_t> order;
+  order.reserve(P4);
+  std::vector<char> used(P4, 0);
+  std::vector<uint64_t> acc(words);
+  for (int t0 = 0; t0 < P4; t0 += tile_blocks) {
+    int seed = 0;
+    while (used[seed]) ++seed;
+    used[seed] = 1;
+    order.push_back(seed);
+    std::copy(row(seed), row(seed) + words, acc.begin());
+    for (int k = 1; k < tile_blocks && t0 + k < P4; ++k) {
+      int best = -1, best_add = 0;
+      for (int p = 0; p < P4; ++p) {
+        if (used[p]) continue;
+        int add = 0;
+        for (int w = 0; w < words; ++w) add += __builtin_popcountll(row(p)[w] & ~acc[w]);
+        if (best < 0 || add < best_add) best = p, best_add = add;
+      }
+      used[best] = 1;
+      order.push_back(best);
+      for (int w = 0; w < words; ++w) acc[w] |= row(best)[w];
+    }
+  }
+  const int tiles = (P4 + tile_blocks - 1) / tile_blocks;
+  if (tiles > 1) {
+    uint64_t lcg = 0x9E3779B97F4A7C15ull;
+    auto next = [&](int n) {
+      lcg = lcg * 6364136223846793005ull + 1442695040888963407ull;
+      return static_cast<int>((lcg >> 33) % static_cast<uint64_t>(n));
+    };
+    auto tile_n = [&](int t) { return std::min(tile_blocks, P4 - t * tile_blocks); };
+    std::vector<int32_t> ta(tile_blocks), tb(tile_blocks);
+    for (int it = 0; it < 40 * P4; ++it) {
+      const int a = next(tiles), b = next(tiles);
+      if (a == b) continue;
+      const int na = tile_n(a), nb = tile_n(b);
+      const int i = next(na), j = next(nb);
+      int32_t *pa = &order[static_cast<size_t>(a) * tile_blocks];
+      int32_t *pb = &order[static_cast<size_t>(b) * tile_blocks];
+      std::copy(pa, pa + na, ta.begin());
+      std::copy(pb, pb + nb, tb.begin());
+      std::swap(ta[i], tb[j]);
+      if (union_size(ta.data(), na) + union_size(tb.data(), nb) <
+          union_size(pa, na) + union_size(pb, nb))
+        std::swap(pa[i], pb[j]);
+    }
+  }
+  return order;
+}
+
+// K-steps of a union layout: every wave tile's items of every chunk, padded
+// to whole steps.
+long union_steps(const Geom &g, const Tiling &tl, const Mask4 &m4, int mfw) {
+  const int wt_count = (g.c_out + 16 * mfw - 1) / (16 * mfw);
+  long steps = 0;
+  for (int wt = 0; wt < wt_count; ++wt)
+    for (int ch = 0; ch < tl.nchunks; ++ch)
+      steps += (static_cast<long>(chunk_items(g, &m4, tl.cc, ch, wt * 4 * mfw, 4 * mfw).size()) + 7) / 8;
+  return steps;
+}
+
 // 16-bit MFMA item layout (variants kVarDenseItems16, kVarKgsUnion16) and
-// the f32 16x16x4 dense layout (kVarDenseItemsF32).
+// the f32 16x16x4 dense layout (kVarDenseItemsF32).  For kVarKgsUnion16 the
+// 4-filter blocks may be reordered (cluster_blocks, tuning switch
+// kgs_order=1) when that saves K-steps; the keep section then maps each wave
+// tile's block slots to layer blocks.
+
 void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const Mask4 *m4,
                         Layout &L, bool small, int mfw) {
   const bool f32 = g.es == 4;
@@ -624,6 +722,25 @@ void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
   L.plan.items_per_step = ips;
   L.step_ptr.assign(static_cast<size_t>(wt_count) * (tl.nchunks + 1), 0);
   L.item_ptr.assign(wt_count, 0);
+  Mask4 reordered{};
+  std::vector<int32_t> perm;
+  // Off unless asked for (kgs_order=1): on MI355X the shorter unions did not
+  // pay for the scattered output stores (a tile's four lane groups then
+  // write four separate 8-byte pieces per voxel instead of 32 contiguous
+  // bytes).
+  if (!dense && !f32 && !small && m4->gm4 == 1 && g.c_out % 4 == 0 && wt_count > 1 &&
+      tune("kgs_order") == 1) {
+    perm = cluster_blocks(g, *m4, 4 * mfw);
+    reordered = *m4;
+    reordered.perm = perm.data();
+    if (union_steps(g, tl, reordered, mfw) < union_steps(g, tl, *m4, mfw)) {
+      m4 = &reordered;
+      L.plan.gmap = 1;
+      const int P4 = g.c_out / 4;
+      for (int b = 0; b < wt_count * 4 * mfw; ++b)
+        L.keep.push_back(static_cast<uint32_t>(b < P4 ? perm[b] : b));
+    }
+  }
   WeightSource src{w, g, m4};
 
   PassCost cost(g, tl);
@@ -1509,6 +1626,8 @@ rt3d_status run_conv(const rt3d_conv3d_desc *d, const rt3d_pack_info *info, cons
   a.item_ptr = reinterpret_cast<const uint32_t *>(b + p.item_ptr_off);
   a.items = reinterpret_cast<const uint32_t *>(b + p.items_off);
   a.keep = reinterpret_cast<const uint32_t *>(b + p.keep_off);
+  a.gmap = info->variant == kVarKgsUnion16 && p.gmap ? a.keep : nullptr;
+  a.gmap_slots = a.gmap ? p.wave_tiles * 4 * p.mfw : 0;
   a.a = b + p.a_off;
   a.a_bytes = static_cast<int32_t>(std::min<uint64_t>(info->packed_bytes - p.a_off, 0x7fffffffu));
   a.n = g.n; a.c_in = g.c_in; a.c_out = g.c_out; a.t = g.t; a.h = g.h; a.w = g.w;

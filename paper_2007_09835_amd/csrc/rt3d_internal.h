@@ -9,7 +9,7 @@
 namespace rt3d {
 
 constexpr uint64_t kMagic = 0x314b4e3344335452ull;  // "RT3D3NK1" little-endian
-constexpr uint32_t kVersion = 2;
+constexpr uint32_t kVersion = 3;
 constexpr uint64_t kAlign = 256;                    // section alignment in a blob
 
 // Kernel mappings (the `variant` field of rt3d_pack_info).
@@ -48,12 +48,16 @@ struct Plan {
   int32_t wave_tiles;      // number of wave tiles
   int32_t items_per_step;  // items consumed per K-step
   int32_t tile_steps;      // most K-steps of one wave tile over all chunks
+  int32_t gmap;            // kVarKgsUnion16: 1 if the keep section maps each wave tile's
+                           // 4-filter block slots to the layer's blocks (u32 per slot)
+  int32_t reserved;
   uint64_t step_ptr_off;   // u32 [wave_tiles][nchunks + 1]
   uint64_t item_ptr_off;   // u32 [wave_tiles]
   uint64_t items_off;      // u32 [...] LDS byte offset of each item
   uint64_t a_off;          // dtype [...], MFMA operand order
   uint64_t keep_off;       // u32 [...] (exact f32 variant: kept-group bits per item;
-                           // pair variant: uint4 per step {keep, side, first block, 0})
+                           // pair variant: uint4 per step {keep, side, first block, 0};
+                           // union variant with gmap: layer block of each tile slot)
 };
 static_assert(sizeof(Plan) <= sizeof(((rt3d_pack_info *)0)->plan), "plan does not fit");
 
@@ -67,6 +71,7 @@ struct ConvArgs {
   const uint32_t *item_ptr;
   const uint32_t *items;
   const uint32_t *keep;
+  const uint32_t *gmap;  // layer 4-filter block of each wave-tile block slot, or NULL (identity)
   const void *a;
   int32_t n, c_in, c_out, t, h, w, to, ho, wo;
   int32_t st, sh, sw, pt, ph, pw;
@@ -93,6 +98,7 @@ struct ConvArgs {
   int32_t x_off;      // first channel of x this layer reads
   int32_t nf;         // 16-slot voxel fragments per wave (slots / 16)
   int32_t a_bytes;    // bytes of the weight stream (pair variant: its buffer extent)
+  int32_t gmap_slots; // entries of gmap (wave_tiles * 4 * mfw)
 };
 
 // Launch shape chosen at forward time from the batch size.

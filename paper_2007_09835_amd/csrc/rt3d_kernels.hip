@@ -522,6 +522,14 @@ __device__ __forceinline__ void put_partial(const ConvArgs &a, const Slot &sl, i
   *reinterpret_cast<f32x4 *>(a.ws + (static_cast<long>(split) * a.total_vox + sl.out) * a.c_out4 + m0) = v;
 }
 
+// First filter (layer order) of 4-filter block slot `slot` of the wave
+// tiles (slots 4*mfw*wt ... belong to wave tile wt): a union layout may have
+// reordered the blocks so that tile-mates keep similar items.  Slots past
+// the last wave tile (a workgroup's idle waves) stay past c_out.
+__device__ __forceinline__ int block_filter0(const ConvArgs &a, int slot) {
+  return 4 * (a.gmap && slot < a.gmap_slots ? static_cast<int>(a.gmap[slot]) : slot);
+}
+
 template <typename T>
 __device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, const uint8_t *lds,
                                            int m_wg0) {
@@ -530,7 +538,7 @@ __device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, co
   const int cg = a.c_wg >> 2;
   const int step = blockDim.x / cg;
   const int c4 = threadIdx.x % cg;
-  const int m0 = m_wg0 + 4 * c4;
+  const int m0 = block_filter0(a, (m_wg0 >> 2) + c4);
   const bool live = m0 < a.c_out;
   const float4 bb = load_bias4(a, m0);
   const uint8_t *col = lds + c4 * 16;
@@ -639,6 +647,11 @@ __global__ __launch_bounds__(256, (MAP != 0 || NF == 4) ? 2 : 1) void items16_ke
       sw.next(a);
     }
   }
+
+  // First filter (layer order) of this lane's 4-filter block in each row.
+  int mf0[MFW];
+#pragma unroll
+  for (int i = 0; i < MFW; ++i) mf0[i] = block_filter0(a, wt * 4 * MFW + 4 * i + g);
 
   f32x4 acc[MFW][NF];
   #pragma unroll
@@ -902,7 +915,7 @@ __global__ __launch_bounds__(256, (MAP != 0 || NF == 4) ? 2 : 1) void items16_ke
         sw.next(a);
 #pragma unroll
         for (int i = 0; i < MFW; ++i)
-          put_partial(a, sl, wt * 16 * MFW + 16 * i + 4 * g, wg.split, acc[i][j]);
+          put_partial(a, sl, mf0[i], wg.split, acc[i][j]);
       }
     }
     return;
@@ -915,7 +928,7 @@ __global__ __launch_bounds__(256, (MAP != 0 || NF == 4) ? 2 : 1) void items16_ke
     if (active) {
       float4 bb[MFW];
 #pragma unroll
-      for (int i = 0; i < MFW; ++i) bb[i] = load_bias4(a, wt * 16 * MFW + 16 * i + 4 * g);
+      for (int i = 0; i < MFW; ++i) bb[i] = load_bias4(a, mf0[i]);
       SlotWalk sw;
       sw.init(a, lane & 15, 16);
 #pragma unroll
@@ -925,7 +938,7 @@ __global__ __launch_bounds__(256, (MAP != 0 || NF == 4) ? 2 : 1) void items16_ke
         if (!sl.valid) continue;
 #pragma unroll
         for (int i = 0; i < MFW; ++i) {
-          const int m0 = wt * 16 * MFW + 16 * i + 4 * g;
+          const int m0 = mf0[i];
           if (m0 >= a.c_out) continue;
           const float4 raw = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
           put4<T>(a, sl.out, m0, activate4<T>(a, sl.out, m0, raw, bb[i]));
@@ -944,7 +957,7 @@ __global__ __launch_bounds__(256, (MAP != 0 || NF == 4) ? 2 : 1) void items16_ke
       const int n = lane & 15;
 #pragma unroll
       for (int i = 0; i < MFW; ++i) {
-        const int m0 = wt * 16 * MFW + 16 * i + 4 * g;
+        const int m0 = mf0[i];
         if (m0 >= a.c_out) continue;
         const float4 bb = load_bias4(a, m0);
         float4 best = make_float4(0.f, 0.f, 0.f, 0.f);

@@ -646,3 +646,40 @@ def test_union_every_step_count(c_in, tune, monkeypatch):
     x = to_device_ndhwc(case.x_t)
     unsplit = from_device_ndhwc(case.conv(x, None, use_workspace=False))
     assert_within_bound(unsplit, ref, case.bound_full(ref), f"unsplit {c_in} {tune}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("si", range(len(SHAPES)))
+def test_union_block_order(si, dtype, monkeypatch):
+    """The 16-bit union with its 4-filter blocks reordered (kgs_order=1, so
+    that tile-mates keep similar items; the epilogue writes every filter to
+    its layer position) on the small shapes, both brick widths' plans, in
+    full against the oracle."""
+    monkeypatch.setenv("RT3D_TUNE", "kgs_order=1,kgs_mfw=1")
+    tag, n, c_in, c_out, thw, k, stride, pad, keep = SHAPES[si]
+    mask = masked(tag, c_out, c_in, k, min(keep, k[0] * k[1] * k[2]))
+    case = LayerCase(tag + "o", n, c_in, c_out, thw, k, stride, pad, dtype, mask)
+    check_full(case, f"kgs block order {tag} {dtype}")
+
+
+@pytest.mark.parametrize("tune", ["kgs_mfw=1", "kgs_mfw=4,slots=128"])
+def test_union_block_order_alike_pairs(tune, monkeypatch):
+    """Alternate blocks keep two disjoint item sets, so reordering halves the
+    K-steps (the planner's CPU test pins that); pooled and split variants of
+    the same layer run through the register, LDS-tile and split-reduction
+    epilogues with the block map, in full against the oracle."""
+    monkeypatch.setenv("RT3D_TUNE", tune + ",kgs_order=1")
+    c_in, c_out = 64, 96
+    P, Q = c_out // 4, c_in // 4
+    mask = np.zeros((P, Q, 27), np.uint8)
+    mask[0::2, :, 0:9] = 1
+    mask[1::2, :, 9:18] = 1
+    for pool, thw in (((1, 1, 1), (3, 6, 7)), ((2, 2, 2), (4, 6, 8))):
+        case = LayerCase("alike" + tune[-1] + str(pool[0]), 1, c_in, c_out, thw, (3, 3, 3),
+                         (1, 1, 1), (1, 1, 1), "bf16", mask, pool=pool, residual=pool == (1, 1, 1))
+        check_full(case, f"alike blocks {tune} pool={pool}")
+        x = to_device_ndhwc(case.x_t)
+        res = None if case.res_t is None else to_device_ndhwc(case.res_t)
+        unsplit = from_device_ndhwc(case.conv(x, res, use_workspace=False))
+        ref = case.oracle_full()
+        assert_within_bound(unsplit, ref, case.bound_full(ref), f"alike unsplit {tune} {pool}")

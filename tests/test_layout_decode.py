@@ -49,8 +49,8 @@ def _plan(info):
     t = dict(zip(("bt", "bh", "bw", "ht", "hh", "hw", "cc", "row", "slots", "nchunks"),
                  map(int, i32[:10])))
     t.update(mfw=int(i32[10]), wave_tiles=int(i32[11]), ips=int(i32[12]),
-             tile_steps=int(i32[13]), step_ptr=int(u64[7]), item_ptr=int(u64[8]),
-             items=int(u64[9]), a=int(u64[10]), keep=int(u64[11]))
+             tile_steps=int(i32[13]), gmap=int(i32[14]), step_ptr=int(u64[8]),
+             item_ptr=int(u64[9]), items=int(u64[10]), a=int(u64[11]), keep=int(u64[12]))
     return t
 
 
@@ -175,6 +175,14 @@ def decode(desc, info, blob):
     mfw = p["mfw"]
     items = _u32(blob, p["items"], (len(blob) - p["items"]) // 4)
     dense = info.variant == VAR_DENSE16
+    # Union layouts may reorder the 4-filter blocks: the keep section then
+    # holds the layer block of every wave-tile block slot.
+    gmap = None
+    if p["gmap"]:
+        assert info.variant == VAR_UNION16
+        gmap = _u32(blob, p["keep"], nwt * 4 * mfw)
+        real = [int(b) for b in gmap if b < (M + 3) // 4]
+        assert sorted(real) == list(range((M + 3) // 4)), "block map is not a permutation"
     for wt in range(nwt):
         row0, step0 = int(item_ptr[wt]), int(step_ptr[wt, 0])
         for ch in range(nch):
@@ -184,6 +192,8 @@ def decode(desc, info, blob):
                     base = (s * mfw + i) * 64 * 8
                     for lane in range(64):
                         m = wt * 16 * mfw + 16 * i + (lane & 15)
+                        if gmap is not None:
+                            m = 4 * int(gmap[m // 4]) + m % 4
                         for e in range(8):
                             ql, pos = _item(p, int(its[2 * (lane >> 4) + e // 4]), kh, kw)
                             streamed += 1
@@ -325,3 +335,38 @@ def test_random_layers_decode_to_masked_weights(case, tune, dt, seed, monkeypatc
     exp, kept = expected(w, mask, g)
     assert got.tobytes() == exp.tobytes()
     assert np.array_equal(seen, kept & (exp != 0))
+
+
+@pytest.mark.parametrize("mfw", ["1", "2"])
+def test_union_reorders_blocks_that_keep_alike(mfw, monkeypatch):
+    """Blocks 0, 2, 4, ... keep one item set and blocks 1, 3, 5, ... a
+    disjoint one: in layer order every wave tile multiplies both sets, so the
+    planner must put alike blocks together (a block map in the keep
+    section), shrink the K-steps to one set's worth, and the layout must
+    still decode to W * expand(mask); with reordering switched off the steps
+    are the union of both sets."""
+    c_in, c_out, k = 32, 64, (3, 3, 3)
+    ks = 27
+    rng = np.random.default_rng(5)
+    w = _bf16_bits(rng, (c_out, c_in, *k), "bf16")
+    P, Q = c_out // 4, c_in // 4
+    mask = np.zeros((P, Q, ks), np.uint8)
+    mask[0::2, :, 0:9] = 1
+    mask[1::2, :, 9:18] = 1
+    desc = rt3d.make_desc(1, c_in, c_out, (4, 6, 6), k, (1, 1, 1), (1, 1, 1), (4, 4), "bf16")
+    steps = {}
+    for order in ("1", "0"):
+        monkeypatch.setenv("RT3D_TUNE", "kgs_map=0,kgs_mfw=%s,kgs_order=%s" % (mfw, order))
+        blob, info = rt3d.rt3d_kgs_pack(desc, w, mask)
+        assert info.variant == VAR_UNION16
+        p = _plan(info)
+        assert p["gmap"] == (1 if order == "1" else 0)
+        got, _, _ = decode(desc, info, blob)
+        exp, _ = expected(w, mask, (4, 4))
+        assert got.tobytes() == exp.tobytes()
+        nwt, nch = p["wave_tiles"], p["nchunks"]
+        sp = _u32(blob, p["step_ptr"], nwt * (nch + 1)).reshape(nwt, nch + 1)
+        steps[order] = int((sp[:, nch] - sp[:, 0]).sum())
+    # 8 channel blocks x 9 positions per set: 9 steps per tile and chunk
+    # when alike blocks share a tile, 18 when each tile mixes both sets.
+    assert steps["1"] * 2 == steps["0"], steps
