@@ -573,10 +573,14 @@ int kgs_tile_width(const Geom &g, const Tiling &tl, const Mask4 *m4) {
 // else 32; 16 for layers below 128 filters.  Layers of 128-255 filters take
 // 32-filter tiles, dense or KGS, when that still leaves 2048 waves (two per
 // SIMD): C3D conv2 at batch 1 dense 45.6 -> 38.7 us, KGS 40.9 -> 37.2 us, at
-// batch 32 1022 -> 893 and 916 -> 847 us.  A wave tile of two or more rows
-// runs on 64-slot bricks: on 128-slot bricks its accumulators and B ring
-// exceed 256 registers and leave one wave per SIMD (16-bit; batch-32 conv3a/3b/4b
+// batch 32 1022 -> 893 and 916 -> 847 us.  A wave tile of four rows runs
+// on 64-slot bricks: on 128-slot bricks its accumulators and B ring exceed
+// 256 registers and leave one wave per SIMD (16-bit; batch-32 conv3a/3b/4b
 // 408/632/338 -> 350/597/309 us KGS, dense 410/643/340 -> 359/648/326 us).
+// Two rows keep the brick width brick_slots chose: the kernel is held to
+// two waves per SIMD there (a few spilled registers), and 128-slot bricks
+// halve the weight loads per MFMA (C3D conv2 KGS batch 32 771 -> 693 us,
+// dense 808 -> 723 us; batch 1 34.1 -> 33.0 us).
 // Tuning switches dense_mfw, kgs_mfw and small_mfw override the width.
 struct ItemPlan {
   Tiling tl;
@@ -607,7 +611,7 @@ ItemPlan item_plan(const Geom &g, const Mask4 *m4, bool small) {
     const int v = tune("kgs_mfw");
     if (v == 1 || v == 2 || v == 4) ip.mfw = v;
   }
-  if (g.es == 2 && ip.mfw >= 2 && ip.tl.slots == 128 && tune("slots") != 128)
+  if (g.es == 2 && ip.mfw >= 4 && ip.tl.slots == 128 && tune("slots") != 128)
     ip.tl = choose_tiling(g, 64);
   return ip;
 }

@@ -606,12 +606,14 @@ __device__ __forceinline__ void tile_store(const ConvArgs &a, const Brick &b, co
 
 // FAST: c_in is a multiple of 8 (branch-free halo staging).
 // MAP: 0 = dense / KGS union, 1 = pairs of any two items, 2 = block pairs.
-// The pair mappings and the 64-slot tiles ask for two waves per SIMD: left
-// to itself the compiler spends registers down to one wave (the pairs' index
-// registers ride with A; the union's unrolled passes lengthen live ranges),
-// and a lone wave cannot hide its LDS reads behind the other's MFMAs.
+// The pair mappings, the 64-slot tiles and the two-row 128-slot tiles ask
+// for two waves per SIMD: left to itself the compiler spends registers down
+// to one wave (the pairs' index registers ride with A; the union's unrolled
+// passes lengthen live ranges; two rows of eight fragments spill a few
+// registers to fit), and a lone wave cannot hide its LDS reads behind the
+// other's MFMAs.
 template <typename T, int MFW, int NF, bool FAST, int MAP = 0>
-__global__ __launch_bounds__(256, (MAP != 0 || NF == 4) ? 2 : 1) void items16_kernel(ConvArgs a) {
+__global__ __launch_bounds__(256, (MAP != 0 || NF == 4 || MFW == 2) ? 2 : 1) void items16_kernel(ConvArgs a) {
   constexpr bool PAIR = MAP != 0;
   constexpr bool BPAIR = MAP == 2;
   // Pairs of any two items on 16-filter tiles stream compact weights; wide

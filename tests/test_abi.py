@@ -166,8 +166,8 @@ def test_brick_width_follows_the_layer_size(monkeypatch):
     16-filter tiles give fewer than 1024 waves (one per SIMD of the GPU) for
     pooled 16-bit layers, 8192 for unpooled 16-bit layers (their narrow-tile
     epilogue runs in registers) and 256 for fp32, and for every 16-bit layer
-    whose wave tile has two or more 16-filter rows (on 128-slot bricks those
-    tiles leave one wave per SIMD); larger single-row layers keep 128;
+    whose wave tile has four 16-filter rows (on 128-slot bricks those tiles
+    leave one wave per SIMD); larger one- and two-row layers keep 128;
     RT3D_TUNE=slots=N overrides the choice at pack time."""
     monkeypatch.delenv("RT3D_TUNE", raising=False)
     pooled_big = rt3d.make_desc(1, 32, 64, (16, 56, 56), dtype="bf16", pool=(2, 2, 2))   # 1568
@@ -184,7 +184,7 @@ def test_brick_width_follows_the_layer_size(monkeypatch):
     assert _brick_slots(unpooled) == 64
     assert _brick_slots(unpooled_big) == 64
     assert _brick_slots(unpooled_huge) == 128
-    assert (_plan_mfw(conv2), _brick_slots(conv2)) == (2, 64)
+    assert (_plan_mfw(conv2), _brick_slots(conv2)) == (2, 128)
     assert (_plan_mfw(wide32), _brick_slots(wide32)) == (4, 64)
     assert _brick_slots(f32) == 128
     assert _brick_slots(f32_small) == 64

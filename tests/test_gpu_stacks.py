@@ -124,10 +124,15 @@ def test_stack_as_benchmarked(net, batch, mode, rate):
         _check_layer(st, i, net, mode, rate, clips, 1500 if net == "r2plus1d" else 2500,
                      f"{net} b{batch} {mode}")
     if net == "c3d" and batch == 1 and mode == "kgs":
-        # the dominant layer of the default bench line runs this plan
+        # the plans of the default bench line's two largest layers: conv2
+        # (32-filter union tiles on 128-slot bricks, pooled through the LDS
+        # tile) and conv3b (its dominant layer by time)
         p = _plan(st.convs[1])
         assert p["pool"] == (2, 2, 2), p
-        assert (p["variant"], p["slots"], p["brick"], p["mfw"]) == (3, 64, (2, 2, 16), 2), p
+        assert (p["variant"], p["slots"], p["brick"], p["mfw"]) == (3, 128, (4, 2, 16), 2), p
+        p = _plan(st.convs[3])
+        assert p["pool"] == (2, 2, 2), p
+        assert (p["variant"], p["slots"], p["brick"], p["mfw"]) == (3, 64, (2, 2, 16), 1), p
 
 
 def test_s3d_stack_as_benchmarked():
