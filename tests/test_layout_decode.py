@@ -303,7 +303,8 @@ def test_pair_stream_is_the_kept_weights_for_c3d_layers(monkeypatch):
 from hypothesis import HealthCheck, given, settings, strategies as st  # noqa: E402
 
 MAPPINGS = ["kgs_map=0,kgs_mfw=1", "kgs_map=0,kgs_mfw=2", "kgs_map=0,kgs_mfw=4", "kgs_map=1",
-            "kgs_map=1,pair_mfw=2", "kgs_map=1,pair_mfw=4", "kgs_map=2"]
+            "kgs_map=1,pair_mfw=2", "kgs_map=1,pair_mfw=4", "kgs_map=2",
+            "kgs_map=0,kgs_mfw=1,kgs_order=1", "kgs_map=0,kgs_mfw=2,kgs_order=1"]
 
 
 @st.composite
