@@ -949,11 +949,11 @@ __global__ __launch_bounds__(256, (MAP != 0 || NF == 4 || MFW == 2) ? 2 : 1) voi
     }
     return;
   }
-  if (NF == 4 && MFW <= 2 && a.qt == 2 && a.qh == 2 && a.qw == 2 && a.bt == 2 && a.bh == 2 &&
+  if (MFW <= 2 && a.qt == 2 && a.qh == 2 && a.qw == 2 && a.bt == NF / 2 && a.bh == 2 &&
       a.bw == 16) {
-    // 2x2x2 pooling on a 2x2x16 brick: fragment j is the w-row (t, h) =
-    // (j / 2, j % 2) and lane n its voxel w, so a window is the four
-    // fragments of lanes n and n ^ 1 (every voxel of an output window lies
+    // 2x2x2 pooling on a (NF/2)x2x16 brick: fragment j is the w-row (t, h) =
+    // (j / 2, j % 2) and lane n its voxel w, so a window is fragments 4p ..
+    // 4p + 3 of lanes n and n ^ 1 (every voxel of an output window lies
     // inside the output; other lanes' values are never stored).
     if (active) {
       const int n = lane & 15;
@@ -962,20 +962,24 @@ __global__ __launch_bounds__(256, (MAP != 0 || NF == 4 || MFW == 2) ? 2 : 1) voi
         const int m0 = mf0[i];
         if (m0 >= a.c_out) continue;
         const float4 bb = load_bias4(a, m0);
-        float4 best = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int j = 0; j < NF; ++j) {
-          const int ot = b.ot0 + (j >> 1), oh = b.oh0 + (j & 1), ow = b.ow0 + n;
-          const bool ok = ot < a.to && oh < a.ho && ow < a.wo;
-          const long vox = ((static_cast<long>(b.nb) * a.to + ot) * a.ho + oh) * a.wo + ow;
-          const float4 raw = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
-          const float4 v = ok ? activate4<T>(a, vox, m0, raw, bb) : raw;
-          best = j ? max4(best, v) : v;
+        for (int p = 0; p < NF / 4; ++p) {
+          float4 best = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const int j = 4 * p + k;
+            const int ot = b.ot0 + (j >> 1), oh = b.oh0 + (j & 1), ow = b.ow0 + n;
+            const bool ok = ot < a.to && oh < a.ho && ow < a.wo;
+            const long vox = ((static_cast<long>(b.nb) * a.to + ot) * a.ho + oh) * a.wo + ow;
+            const float4 raw = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            const float4 v = ok ? activate4<T>(a, vox, m0, raw, bb) : raw;
+            best = k ? max4(best, v) : v;
+          }
+          best = max4(best, swap_pairs4(best));  // lanes n, n ^ 1 share g: both active
+          const int pt = (b.ot0 >> 1) + p, ph = b.oh0 >> 1, pw = (b.ow0 + n) >> 1;
+          if ((n & 1) == 0 && pt < a.pto && ph < a.pho && pw < a.pwo)
+            put4<T>(a, ((static_cast<long>(b.nb) * a.pto + pt) * a.pho + ph) * a.pwo + pw, m0, best);
         }
-        best = max4(best, swap_pairs4(best));  // lanes n, n ^ 1 share g: both active
-        const int pt = b.ot0 >> 1, ph = b.oh0 >> 1, pw = (b.ow0 + n) >> 1;
-        if ((n & 1) == 0 && pt < a.pto && ph < a.pho && pw < a.pwo)
-          put4<T>(a, ((static_cast<long>(b.nb) * a.pto + pt) * a.pho + ph) * a.pwo + pw, m0, best);
       }
     }
     return;
