@@ -922,11 +922,10 @@ __global__ __launch_bounds__(256, (MAP != 0 || NF == 4 || MFW == 2) ? 2 : 1) voi
     }
     return;
   }
-  if (NF == 4 && MFW <= 2 && a.qt * a.qh * a.qw == 1) {
+  if (NF == 4 && MFW <= 4 && a.qt * a.qh * a.qw == 1) {
     // No pooling: a lane's accumulator holds 4 consecutive filters of one
     // voxel slot, so the epilogue runs on registers and stores straight to
-    // y (no LDS tile, no barriers).  Narrow tiles only: in the wider ones
-    // the extra live registers would cost the second wave per SIMD.
+    // y (no LDS tile, no barriers).
     if (active) {
       float4 bb[MFW];
 #pragma unroll
