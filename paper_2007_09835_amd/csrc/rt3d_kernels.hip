@@ -948,8 +948,7 @@ __global__ __launch_bounds__(256, (MAP != 0 || NF == 4 || MFW == 2) ? 2 : 1) voi
     }
     return;
   }
-  if (MFW <= 2 && a.qt == 2 && a.qh == 2 && a.qw == 2 && a.bt == NF / 2 && a.bh == 2 &&
-      a.bw == 16) {
+  if (a.qt == 2 && a.qh == 2 && a.qw == 2 && a.bt == NF / 2 && a.bh == 2 && a.bw == 16) {
     // 2x2x2 pooling on a (NF/2)x2x16 brick: fragment j is the w-row (t, h) =
     // (j / 2, j % 2) and lane n its voxel w, so a window is fragments 4p ..
     // 4p + 3 of lanes n and n ^ 1 (every voxel of an output window lies
