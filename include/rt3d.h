@@ -45,9 +45,10 @@
  *     of adjacent channel blocks on the 2:4 sparse MFMA), pair_mfw=1|2|4
  *     (16-filter rows per pair-mapping tile), cc=N (at most N input channels
  *     per staged chunk, 16-bit), kgs_f32=0|1 (fp32 KGS: exact 4x4 blocks or
- *     the union of a 16-filter tile's items), kgs_order=1 (16-bit union with
- *     4x4 groups: place 4-filter blocks that keep similar items in the same
- *     tile when that saves K-steps; off by default).  Launch-time
+ *     the union of a 16-filter tile's items), kgs_order=0|1 (16-bit union
+ *     with 4x4 groups: 4-filter blocks that keep similar items share a tile
+ *     when that saves at least 5% of the K-steps by default; 1 = whenever it
+ *     saves any, 0 = never).  Launch-time
  *     keys change the launch of a forward call: splits=N (input-channel
  *     splits) and wg_order=0|1 (workgroup order).  Results stay within the
  *     documented accuracy under every setting.
@@ -204,9 +205,9 @@ rt3d_status rt3d_conv3d_workspace_size(const rt3d_conv3d_desc *desc,
  * the exact fp32 kernel issues one 4x4 MFMA per kept (group, item); the
  * union mappings (16-bit, and fp32 for layers too small to be bound by
  * their MFMA work) multiply the tile's other groups at that item by zero
- * weights (with kgs_order=1 the 16-bit union places 4-filter blocks that
- * keep similar items in the same tile; outputs land in layer order either
- * way); the 16-bit pair mapping packs two items whose kept groups
+ * weights (the 16-bit union may place 4-filter blocks that keep similar
+ * items in the same tile; outputs land in layer order either way); the
+ * 16-bit pair mapping packs two items whose kept groups
  * are disjoint into one 2:4 sparse MFMA slot and streams kept weights only.
  * Asynchronous on `stream`.  Per-call limits (RT3D_ERR_UNSUPPORTED,
  * checked before any launch; the same for rt3d_conv3d_dense_fwd): fewer

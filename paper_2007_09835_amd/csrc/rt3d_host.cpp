@@ -707,9 +707,9 @@ long union_steps(const Geom &g, const Tiling &tl, const Mask4 &m4, int mfw) {
 
 // 16-bit MFMA item layout (variants kVarDenseItems16, kVarKgsUnion16) and
 // the f32 16x16x4 dense layout (kVarDenseItemsF32).  For kVarKgsUnion16 the
-// 4-filter blocks may be reordered (cluster_blocks, tuning switch
-// kgs_order=1) when that saves K-steps; the keep section then maps each wave
-// tile's block slots to layer blocks.
+// 4-filter blocks may be reordered (cluster_blocks) when that saves enough
+// K-steps; the keep section then maps each wave tile's block slots to layer
+// blocks.
 
 void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const Mask4 *m4,
                         Layout &L, bool small, int mfw) {
@@ -728,16 +728,20 @@ void build_items_layout(const Geom &g, const Tiling &tl, const uint8_t *w, const
   L.item_ptr.assign(wt_count, 0);
   Mask4 reordered{};
   std::vector<int32_t> perm;
-  // Off unless asked for (kgs_order=1): on MI355X the shorter unions did not
-  // pay for the scattered output stores (a tile's four lane groups then
-  // write four separate 8-byte pieces per voxel instead of 32 contiguous
-  // bytes).
+  // Used when it saves at least 5% of the K-steps (tuning switch
+  // kgs_order=1: any saving, 0: never): a reordered tile's four lane groups
+  // store four separate 8-byte pieces per voxel instead of 32 contiguous
+  // bytes, which ate the 3% that i.i.d. KGS masks gain (whole-group vanilla
+  // masks cluster better: 11%, 1.5-2.3% faster).
+  const int order = tune("kgs_order");
   if (!dense && !f32 && !small && m4->gm4 == 1 && g.c_out % 4 == 0 && wt_count > 1 &&
-      tune("kgs_order") == 1) {
+      order != 0) {
     perm = cluster_blocks(g, *m4, 4 * mfw);
     reordered = *m4;
     reordered.perm = perm.data();
-    if (union_steps(g, tl, reordered, mfw) < union_steps(g, tl, *m4, mfw)) {
+    const long natural = union_steps(g, tl, *m4, mfw);
+    const long clustered = union_steps(g, tl, reordered, mfw);
+    if (order == 1 ? clustered < natural : clustered <= natural - natural / 20) {
       m4 = &reordered;
       L.plan.gmap = 1;
       const int P4 = g.c_out / 4;
