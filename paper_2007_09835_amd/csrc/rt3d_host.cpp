@@ -570,7 +570,9 @@ int kgs_tile_width(const Geom &g, const Tiling &tl, const Mask4 *m4) {
 // Dense layers share every B fragment across the wave's rows, KGS layers walk
 // the union of the tile's kernel groups' items (kgs_tile_width).  Dense: 64
 // filters (4 rows) for layers of 256+ filters with >= 2000 output voxels,
-// else 32; 16 for layers below 128 filters.  Layers of 128-255 filters take
+// 16 (16-bit) for those with fewer than 256 (a few bricks, split many ways:
+// at batch 1 C3D conv5a/b 14.7 -> 13.2 us, R(2+1)D layer 5 and S3D Mixed_5
+// convs 5-10% faster), else 32; 16 for layers below 128 filters.  Layers of 128-255 filters take
 // 32-filter tiles, dense or KGS, when that still leaves 2048 waves (two per
 // SIMD): C3D conv2 at batch 1 dense 45.6 -> 38.7 us, KGS 40.9 -> 37.2 us, at
 // batch 32 1022 -> 893 and 916 -> 847 us.  A wave tile of four rows runs
@@ -602,7 +604,7 @@ ItemPlan item_plan(const Geom &g, const Mask4 *m4, bool small) {
   const bool mid = g.es == 2 && g.c_out >= 128 && g.c_out < 256 &&
                    (voxels + 63) / 64 * ((g.c_out + 31) / 32) >= 2048;
   if (dense) {
-    if (g.c_out >= 256) ip.mfw = voxels >= 2000 ? 4 : 2;
+    if (g.c_out >= 256) ip.mfw = voxels >= 2000 ? 4 : (g.es == 2 && voxels < 256 ? 1 : 2);
     else if (mid) ip.mfw = 2;
     const int v = tune("dense_mfw");
     if (v == 1 || v == 2 || v == 4) ip.mfw = v;
