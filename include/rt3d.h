@@ -33,8 +33,9 @@
  *     a kernel surface at the next synchronisation of that stream.
  *   - Ownership: the caller owns every buffer.  The library never allocates
  *     caller-visible memory, never frees or retains a pointer past a call,
- *     and keeps no state except a thread-local error message and a per-device
- *     cache of runtime queries (compute-unit count, kernel occupancy).
+ *     and keeps no state except a thread-local error message, a per-device
+ *     cache of runtime queries (compute-unit count, kernel occupancy) and the
+ *     split-K scratch array of rt3d_kgs_conv3d_fwd_noalloc (one per device).
  *   - Tuning switch (benchmarks only; leave unset): the environment variable
  *     RT3D_TUNE="key=value,..." overrides planner choices.  Pack-time keys
  *     change the kernel layout written into a blob: slots=64|128 (voxel slots
