@@ -565,6 +565,48 @@ int kgs_tile_width(const Geom &g, const Tiling &tl, const Mask4 *m4) {
   return wide < 1.4 * narrow ? 4 : 1;
 }
 
+// Channel splits trade per-workgroup fixed cost (prologue, first halo load,
+// epilogue) and a reduction pass against parallelism.  The split count
+// minimises a time model in cycles:
+//   rounds * kFixed + chunks per workgroup * steps per chunk * step cycles
+//   * (1 + kShare * (workgroups per CU - 1)) + [s > 1] (kReduce + partial
+//   bytes written and read back / kPartialBytesPerCycle),
+// with constants fitted to per-wave timestamps and per-layer traces of the
+// C3D and R(2+1)D layers on MI355X.  wgs: workgroups of one split;
+// per_cu_split / per_cu_whole: resident workgroups per CU of split and
+// unsplit launches; cus: compute units.
+int model_splits(const Geom &g, const Tiling &tl, int mfw, double chunk_steps, uint32_t variant,
+                 long wgs, int per_cu_split, int per_cu_whole, long cus) {
+  const long total_vox = static_cast<long>(g.n) * g.to * g.ho * g.wo;
+  const double partial_bytes = 2.0 * static_cast<double>(total_vox) * ((g.c_out + 3) / 4 * 4) * 4;
+  constexpr double kFixed = 12000, kReduce = 9600, kShare = 0.2, kPartialBytesPerCycle = 4200;
+  // Pair steps read twice the items of a union step (an estimate until
+  // measured per layer).
+  const double step_cycles = variant == kVarKgsPair16 ? 600.0
+                             : (mfw == 1 ? 380.0 : (mfw == 2 ? 555.0 : 815.0));
+  // A chunk costs its K-steps, but no less than the exposed latency of its
+  // halo load, plus the barriers and LDS commit around it.
+  constexpr double kChunkLatency = 5000, kChunkFixed = 2000;
+  const double chunk_cycles = std::max(chunk_steps * step_cycles, kChunkLatency) + kChunkFixed;
+  int splits = 1;
+  double best = -1;
+  for (int s = 1; s <= tl.nchunks; ++s) {
+    if (s > 1 && (tl.nchunks + s - 1) / s == (tl.nchunks + s - 2) / (s - 1)) continue;  // same chunks per WG
+    const long n = wgs * s;
+    const long per_cu = s > 1 ? per_cu_split : per_cu_whole;
+    const long per = std::min<long>((n + cus - 1) / cus, per_cu);          // workgroups per CU at once
+    const long rounds = (n + cus * per - 1) / (cus * per);
+    const double t = rounds * (kFixed + ((tl.nchunks + s - 1) / s) * chunk_cycles *
+                                            (1.0 + kShare * static_cast<double>(per - 1))) +
+                     (s > 1 ? kReduce + s * partial_bytes / kPartialBytesPerCycle : 0.0);
+    if (best < 0 || t < best) {
+      best = t;
+      splits = s;
+    }
+  }
+  return splits;
+}
+
 // Filter rows (of 16) per wave tile of the item kernels, then the brick.
 //
 // Dense layers share every B fragment across the wave's rows, KGS layers walk
@@ -606,6 +648,29 @@ ItemPlan item_plan(const Geom &g, const Mask4 *m4, bool small) {
   if (dense) {
     if (g.c_out >= 256) ip.mfw = voxels >= 2000 ? 4 : (g.es == 2 && voxels < 256 ? 1 : 2);
     else if (mid) ip.mfw = 2;
+    // A shallow reduction (c_in taps < 4096) that the wide tiles would split
+    // across workgroups runs unsplit on 16-filter tiles when those fill the
+    // GPU without a split: the wide tiles' fp32 partials and reduction pass
+    // cost more than the narrow tiles' unshared B fragments (batch 1: C3D
+    // conv3a 32 -> 24 us, R(2+1)D layer-4 first spatial conv 17.6 -> 12.8 us,
+    // S3D Mixed_4e/4f branch-1 spatial convs 13 -> 11 us; deeper layers such
+    // as C3D conv3b ran slower unsplit).  Splits are judged by the launch
+    // model at two resident workgroups per CU on 256 CUs.
+    const long taps = static_cast<long>(g.c_in) * g.kt * g.kh * g.kw;
+    if (g.es == 2 && g.c_out >= 256 && ip.mfw > 1 && taps < 4096) {
+      auto splits_at = [&](int mfw) {
+        const Tiling t = mfw >= 4 && ip.tl.slots == 128 ? choose_tiling(g, 64) : ip.tl;
+        const long bricks = static_cast<long>(std::max(g.n, 1)) * ((g.to + t.bt - 1) / t.bt) *
+                            ((g.ho + t.bh - 1) / t.bh) * ((g.wo + t.bw - 1) / t.bw);
+        const long ntg = ((g.c_out + 16 * mfw - 1) / (16 * mfw) + 3) / 4;
+        long steps = 0;
+        for (int ch = 0; ch < t.nchunks; ++ch)
+          steps += ((std::min(t.cc, g.c_in - ch * t.cc) + 3) / 4 * g.ks + 7) / 8;
+        return model_splits(g, t, mfw, static_cast<double>(steps) / t.nchunks, kVarDenseItems16,
+                            bricks * ntg, 2, 2, 256);
+      };
+      if (splits_at(ip.mfw) > 1 && splits_at(1) == 1) ip.mfw = 1;
+    }
     const int v = tune("dense_mfw");
     if (v == 1 || v == 2 || v == 4) ip.mfw = v;
   } else {
@@ -1537,14 +1602,6 @@ Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint32_t variant, u
   if (variant == kVarSmallDense16 || variant == kVarSmallKgs16) return L;  // one chunk, no split
   const long ntg = (p.wave_tiles + L.wpw - 1) / L.wpw;
   const long wgs = bricks * ntg;
-  // Channel splits trade per-workgroup fixed cost (prologue, first halo
-  // load, epilogue) and a reduction pass against parallelism.  The split
-  // count minimises a time model in cycles:
-  //   rounds * kFixed + chunks per workgroup * steps per chunk * step cycles
-  //   * (1 + kShare * (workgroups per CU - 1)) + [s > 1] (kReduce + partial
-  //   bytes written and read back / kPartialBytesPerCycle),
-  // with constants fitted to per-wave timestamps and per-layer traces of the
-  // C3D and R(2+1)D layers on MI355X.
   // LDS per workgroup as the launch requests it: split launches keep only
   // the halo (partials are stored from registers); unsplit ones also reuse
   // it as the epilogue tile of 16 * nf voxel slots x 64 * mfw filters.
@@ -1555,35 +1612,9 @@ Launch plan_launch(const rt3d_conv3d_desc *d, const Plan &p, uint32_t variant, u
       cached_resident(static_cast<int>(variant), d->dtype, p.mfw, tl.slots / 16, std::max(halo, tile));
   if (per_cu_split <= 0) per_cu_split = 2;
   if (per_cu_whole <= 0) per_cu_whole = per_cu_split;
-  const long cus = device_cus();
-  const long total_vox_ = static_cast<long>(g.n) * g.to * g.ho * g.wo;
-  const double partial_bytes = 2.0 * static_cast<double>(total_vox_) * ((g.c_out + 3) / 4 * 4) * 4;
-  constexpr double kFixed = 12000, kReduce = 9600, kShare = 0.2, kPartialBytesPerCycle = 4200;
-  // Pair steps read twice the items of a union step (an estimate until
-  // measured per layer).
-  const double step_cycles = variant == kVarKgsPair16 ? 600.0
-                             : (p.mfw == 1 ? 380.0 : (p.mfw == 2 ? 555.0 : 815.0));
   const double chunk_steps = p.tile_steps > 0 ? static_cast<double>(p.tile_steps) / tl.nchunks : 24.0;
-  // A chunk costs its K-steps, but no less than the exposed latency of its
-  // halo load, plus the barriers and LDS commit around it.
-  constexpr double kChunkLatency = 5000, kChunkFixed = 2000;
-  const double chunk_cycles = std::max(chunk_steps * step_cycles, kChunkLatency) + kChunkFixed;
-  int splits = 1;
-  double best = -1;
-  for (int s = 1; s <= tl.nchunks; ++s) {
-    if (s > 1 && (tl.nchunks + s - 1) / s == (tl.nchunks + s - 2) / (s - 1)) continue;  // same chunks per WG
-    const long n = wgs * s;
-    const long per_cu = s > 1 ? per_cu_split : per_cu_whole;
-    const long per = std::min<long>((n + cus - 1) / cus, per_cu);          // workgroups per CU at once
-    const long rounds = (n + cus * per - 1) / (cus * per);
-    const double t = rounds * (kFixed + ((tl.nchunks + s - 1) / s) * chunk_cycles *
-                                            (1.0 + kShare * static_cast<double>(per - 1))) +
-                     (s > 1 ? kReduce + s * partial_bytes / kPartialBytesPerCycle : 0.0);
-    if (best < 0 || t < best) {
-      best = t;
-      splits = s;
-    }
-  }
+  int splits = model_splits(g, tl, p.mfw, chunk_steps, variant, wgs, per_cu_split, per_cu_whole,
+                            device_cus());
   if (tune("splits") > 0) splits = std::max(1, std::min(tl.nchunks, tune("splits")));
   const long total_vox = static_cast<long>(g.n) * g.to * g.ho * g.wo;
   const uint64_t per_split = static_cast<uint64_t>(total_vox) * ((g.c_out + 3) / 4 * 4) * 4;
