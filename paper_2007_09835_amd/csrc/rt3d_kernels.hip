@@ -195,6 +195,39 @@ struct SlotWalk {
 // so one 16-byte read of a piece is the operand of a block pair.
 __device__ __forceinline__ uint4 interleave_blocks(uint4 v) { return make_uint4(v.x, v.z, v.y, v.w); }
 
+// One 16-byte halo piece whose channels are not all present or not 16-byte
+// aligned: its first n_el (< 16 / ES) elements, zeros after them.  pairs
+// (16-bit elements, even pitch and offset: the piece starts on a 4-byte
+// boundary) reads two elements per 4-byte load; a last odd element's load
+// also covers the element after it, which still lies inside the voxel's row
+// (an even pitch leaves room for it) and is masked off.  Otherwise one load
+// per element.
+template <int ES>
+__device__ __forceinline__ uint4 load_ragged(const uint8_t *src, int n_el, bool pairs) {
+  constexpr int EPP = 16 / ES;
+  uint32_t w[4] = {0u, 0u, 0u, 0u};
+  if (ES == 2 && pairs) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (2 * q < n_el) {
+        const uint32_t d = reinterpret_cast<const uint32_t *>(src)[q];
+        w[q] = 2 * q + 1 < n_el ? d : (d & 0xffffu);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < EPP; ++e) {
+      if (e < n_el) {
+        uint32_t bits;
+        if constexpr (ES == 4) bits = reinterpret_cast<const uint32_t *>(src)[e];
+        else bits = reinterpret_cast<const uint16_t *>(src)[e];
+        w[(e * ES) >> 2] |= bits << (((e * ES) & 3) * 8);
+      }
+    }
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 template <int ES, bool ILV = false>
 __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, const Brick &b,
                                            int c0) {
@@ -202,6 +235,7 @@ __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, cons
   const int ppr = a.cc / EPP;                  // pieces per halo row
   const int total = a.ht * a.hh * a.hw * ppr;
   const bool vec = (a.c_in % EPP) == 0 && (a.x_pitch % EPP) == 0 && (a.x_off % EPP) == 0;
+  const bool pairs = ES == 2 && (a.x_pitch % 2) == 0 && (a.x_off % 2) == 0;
   const uint8_t *xb = static_cast<const uint8_t *>(a.x);
   for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
     const DivMod p = divmod(idx, ppr), x = divmod(p.q, a.hw), y = divmod(x.q, a.hh);
@@ -216,19 +250,7 @@ __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, cons
       if (vec) {
         v = *reinterpret_cast<const uint4 *>(src);
       } else {
-        // Channel count not a multiple of the piece: element-wise, zero tail.
-        const int n_el = min(EPP, a.c_in - c);
-        uint32_t w[4] = {0u, 0u, 0u, 0u};
-#pragma unroll
-        for (int e = 0; e < EPP; ++e) {
-          if (e < n_el) {
-            uint32_t bits;
-            if constexpr (ES == 4) bits = reinterpret_cast<const uint32_t *>(src)[e];
-            else bits = reinterpret_cast<const uint16_t *>(src)[e];
-            w[(e * ES) >> 2] |= bits << (((e * ES) & 3) * 8);
-          }
-        }
-        v = make_uint4(w[0], w[1], w[2], w[3]);
+        v = load_ragged<ES>(src, min(EPP, a.c_in - c), pairs);
       }
     }
     if constexpr (ILV) v = interleave_blocks(v);
@@ -306,6 +328,7 @@ struct Stager {
       return;
     }
     const bool vec = (a.c_in % EPP) == 0 && (a.x_pitch % EPP) == 0 && (a.x_off % EPP) == 0;
+    const bool pairs = ES == 2 && (a.x_pitch % 2) == 0 && (a.x_off % 2) == 0;
 #pragma unroll
     for (int k = 0; k < MAXI; ++k) {
       const int idx = threadIdx.x + k * blockDim.x;
@@ -316,18 +339,7 @@ struct Stager {
         if (vec) {
           v = *reinterpret_cast<const uint4 *>(src);
         } else {
-          const int n_el = min(EPP, a.c_in - c);
-          uint32_t w[4] = {0u, 0u, 0u, 0u};
-#pragma unroll
-          for (int e = 0; e < EPP; ++e) {
-            if (e < n_el) {
-              uint32_t bits;
-              if constexpr (ES == 4) bits = reinterpret_cast<const uint32_t *>(src)[e];
-              else bits = reinterpret_cast<const uint16_t *>(src)[e];
-              w[(e * ES) >> 2] |= bits << (((e * ES) & 3) * 8);
-            }
-          }
-          v = make_uint4(w[0], w[1], w[2], w[3]);
+          v = load_ragged<ES>(src, min(EPP, a.c_in - c), pairs);
         }
       }
       d[k] = v;

@@ -244,6 +244,27 @@ def test_vanilla_pruned_group_ignores_its_channels(dtype):
     check_full(case, f"vanilla {dtype}")
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("sparse", [True, False])
+def test_odd_channel_slice_of_a_wider_input(dtype, sparse):
+    """A layer of 13 input channels reads channels 2..14 of a 16-channel
+    input (even pitch and offset: the halo staging reads two channels per
+    4-byte load and masks the one past the slice).  The channels outside the
+    slice hold NaN, so any of them reaching a product shows in the output."""
+    mask = masked("oddslice", 24, 13, (3, 3, 3), 11) if sparse else None
+    case = LayerCase("oddslice", 2, 13, 24, (4, 7, 9), (3, 3, 3), (1, 1, 1), (1, 1, 1), dtype, mask)
+    x = to_device_ndhwc(case.x_t)
+    wide = torch.full((*x.shape[:-1], 16), float("nan"), dtype=x.dtype, device=x.device)
+    wide[..., 2:15] = x
+    got = from_device_ndhwc(case.conv(wide, None, x_off=2))
+    ref = case.oracle_full()
+    assert np.isfinite(got).all()
+    err = rel_l2(got, ref)
+    print(f"odd slice {dtype} sparse={sparse}: relL2={err:.3e}", flush=True)
+    assert err <= TOL[dtype], err
+    assert_within_bound(got, ref, case.bound_full(ref), "odd slice")
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("sparse", [True, False])
 def test_split_k_matches_unsplit(dtype, sparse):
