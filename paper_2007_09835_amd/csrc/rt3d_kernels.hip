@@ -195,6 +195,17 @@ struct SlotWalk {
 // so one 16-byte read of a piece is the operand of a block pair.
 __device__ __forceinline__ uint4 interleave_blocks(uint4 v) { return make_uint4(v.x, v.z, v.y, v.w); }
 
+// The first n (< 16 / ES) elements of a 16-byte piece, zeros after them.
+template <int ES>
+__device__ __forceinline__ uint4 cut_piece(uint4 v, int n) {
+  const int keep = n * ES;  // bytes
+  const auto dw = [&](uint32_t x, int j) {
+    const int kb = keep - 4 * j;
+    return kb >= 4 ? x : (kb <= 0 ? 0u : x & ((1u << (8 * kb)) - 1u));
+  };
+  return make_uint4(dw(v.x, 0), dw(v.y, 1), dw(v.z, 2), dw(v.w, 3));
+}
+
 // One 16-byte halo piece whose channels are not all present or not 16-byte
 // aligned: its first n_el (< 16 / ES) elements, zeros after them.  pairs
 // (16-bit elements, even pitch and offset: the piece starts on a 4-byte
@@ -234,7 +245,9 @@ __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, cons
   constexpr int EPP = 16 / ES;                 // elements per 16-byte piece
   const int ppr = a.cc / EPP;                  // pieces per halo row
   const int total = a.ht * a.hh * a.hw * ppr;
-  const bool vec = (a.c_in % EPP) == 0 && (a.x_pitch % EPP) == 0 && (a.x_off % EPP) == 0;
+  // vec: every piece that starts inside the layer's channels lies inside
+  // its 16-byte aligned row (a ragged channel count's last piece is cut).
+  const bool vec = (a.x_pitch % EPP) == 0 && (a.x_off % EPP) == 0;
   const bool pairs = ES == 2 && (a.x_pitch % 2) == 0 && (a.x_off % 2) == 0;
   const uint8_t *xb = static_cast<const uint8_t *>(a.x);
   for (int idx = threadIdx.x; idx < total; idx += blockDim.x) {
@@ -249,6 +262,7 @@ __device__ __forceinline__ void stage_halo(uint8_t *lds, const ConvArgs &a, cons
       const uint8_t *src = xb + (vox * a.x_pitch + a.x_off + c) * ES;
       if (vec) {
         v = *reinterpret_cast<const uint4 *>(src);
+        if (a.c_in - c < EPP) v = cut_piece<ES>(v, a.c_in - c);
       } else {
         v = load_ragged<ES>(src, min(EPP, a.c_in - c), pairs);
       }
@@ -327,7 +341,7 @@ struct Stager {
       live = bits;
       return;
     }
-    const bool vec = (a.c_in % EPP) == 0 && (a.x_pitch % EPP) == 0 && (a.x_off % EPP) == 0;
+    const bool vec = (a.x_pitch % EPP) == 0 && (a.x_off % EPP) == 0;  // as in stage_halo
     const bool pairs = ES == 2 && (a.x_pitch % 2) == 0 && (a.x_off % 2) == 0;
 #pragma unroll
     for (int k = 0; k < MAXI; ++k) {
@@ -338,6 +352,7 @@ struct Stager {
         const uint8_t *src = xb + (static_cast<long>(vox[k]) * a.x_pitch + a.x_off + c) * ES;
         if (vec) {
           v = *reinterpret_cast<const uint4 *>(src);
+          if (a.c_in - c < EPP) v = cut_piece<ES>(v, a.c_in - c);
         } else {
           v = load_ragged<ES>(src, min(EPP, a.c_in - c), pairs);
         }

@@ -60,13 +60,21 @@ class Stack:
         # activation buffers (channels-last), allocated once
         self.x = torch.zeros((batch, self.layers[0].t, self.layers[0].h, self.layers[0].w,
                               self.layers[0].c_in), dtype=tdt, device=device)
+        # A layer output whose channel count is not a multiple of 8 (the
+        # R(2+1)D mid widths) gets a channel pitch rounded up to 8, so the
+        # next layer stages its halo with whole 16-byte loads; the pad
+        # channels stay zero.  Residual sources keep their exact width.
         self.bufs: Dict[str, torch.Tensor] = {}
         self.pool_bufs: Dict[str, torch.Tensor] = {}
+        residual_sources = {l.residual_from for l in self.layers if l.residual_from}
         for l, c in zip(self.layers, self.convs):
-            self.bufs[l.name] = torch.empty(c.out_shape(batch), dtype=tdt, device=device)
+            shape = list(c.out_shape(batch))
+            if shape[-1] % 8 and l.name not in residual_sources:
+                shape[-1] = (shape[-1] + 7) // 8 * 8
+            self.bufs[l.name] = torch.zeros(shape, dtype=tdt, device=device)
             if l.pool_after and not fuse_pool:
                 k, s = l.pool_after
-                n, t, h, w, ch = c.out_shape(batch)
+                n, t, h, w, ch = self.bufs[l.name].shape
                 self.pool_bufs[l.name] = torch.empty(
                     (n, (t - k[0]) // s[0] + 1, (h - k[1]) // s[1] + 1, (w - k[2]) // s[2] + 1, ch),
                     dtype=tdt, device=device)

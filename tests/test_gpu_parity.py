@@ -244,19 +244,22 @@ def test_vanilla_pruned_group_ignores_its_channels(dtype):
     check_full(case, f"vanilla {dtype}")
 
 
+@pytest.mark.parametrize("x_off", [0, 2])
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
 @pytest.mark.parametrize("sparse", [True, False])
-def test_odd_channel_slice_of_a_wider_input(dtype, sparse):
-    """A layer of 13 input channels reads channels 2..14 of a 16-channel
-    input (even pitch and offset: the halo staging reads two channels per
-    4-byte load and masks the one past the slice).  The channels outside the
-    slice hold NaN, so any of them reaching a product shows in the output."""
+def test_odd_channel_slice_of_a_wider_input(dtype, sparse, x_off):
+    """A layer of 13 input channels reads channels x_off..x_off+12 of a
+    16-channel input.  Offset 0: pitch and offset are multiples of 8, so the
+    halo staging loads whole 16-byte pieces and cuts each row's last piece
+    to the layer's channels; offset 2: it reads two channels per 4-byte load
+    and masks the one past the slice.  The channels outside the slice hold
+    NaN, so any of them reaching a product shows in the output."""
     mask = masked("oddslice", 24, 13, (3, 3, 3), 11) if sparse else None
     case = LayerCase("oddslice", 2, 13, 24, (4, 7, 9), (3, 3, 3), (1, 1, 1), (1, 1, 1), dtype, mask)
     x = to_device_ndhwc(case.x_t)
     wide = torch.full((*x.shape[:-1], 16), float("nan"), dtype=x.dtype, device=x.device)
-    wide[..., 2:15] = x
-    got = from_device_ndhwc(case.conv(wide, None, x_off=2))
+    wide[..., x_off:x_off + 13] = x
+    got = from_device_ndhwc(case.conv(wide, None, x_off=x_off))
     ref = case.oracle_full()
     assert np.isfinite(got).all()
     err = rel_l2(got, ref)

@@ -84,11 +84,11 @@ def _check_layer(st, i, tag, mode, rate, clips, count, label):
     d = synth.layer_params(tag, l, mask_kind=mode, rate=rate)
     mask = st.masks[i]
     src, res = _layer_inputs(st, i)
-    x64 = from_device_ndhwc(src[clips])
-    r64 = None if res is None else from_device_ndhwc(res[clips])
+    x64 = from_device_ndhwc(src[clips])[:, :l.c_in]   # buffers may carry pad channels
+    r64 = None if res is None else from_device_ndhwc(res[clips])[:, :l.c_out]
     w64 = synth.to_dtype(d.w, "bf16").double().numpy()
     b64 = d.bias.astype(np.float32).astype(np.float64)
-    got = from_device_ndhwc(st.bufs[l.name][clips])
+    got = from_device_ndhwc(st.bufs[l.name][clips])[:, :l.c_out]
     to, ho, wo = l.out_thw
     full_shape = (len(clips), l.c_out, to, ho, wo)
     pool = _plan(conv)["pool"]
