@@ -140,7 +140,7 @@ class S3DStack:
 
     def __init__(self, batch: int = 1, dtype: str = "bf16", mode: str = "kgs",
                  rate: float = 2.1, tag: str = "s3d", device: str = "cuda", group=(4, 4),
-                 clip=(16, 224), n_streams: int = 4):
+                 clip=(16, 224), n_streams: int = 2):
         """``clip`` = (frames, height = width) of the input; ``n_streams``
         streams run independent ops concurrently (1 = strictly in order)."""
         self.batch, self.dtype, self.mode, self.rate = batch, dtype, mode, rate
@@ -271,7 +271,7 @@ class S3DStack:
 
 
 def make_stack(net: str, batch: int = 1, dtype: str = "bf16", mode: str = "kgs",
-               rate: float = 3.0, fuse_pool: bool = True, group=(4, 4), streams: int = 4):
+               rate: float = 3.0, fuse_pool: bool = True, group=(4, 4), streams: int = 2):
     """The named stack (c3d, r2plus1d or s3d; ``streams`` applies to s3d)."""
     if net == "s3d":
         return S3DStack(batch, dtype, mode, rate, group=group, n_streams=streams)

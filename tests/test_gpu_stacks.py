@@ -41,7 +41,7 @@ def _plan(conv):
 
 def _bench_stack(net, batch, mode, rate):
     """The stack and input exactly as bench.py sets them up."""
-    st = make_stack(net, batch, "bf16", mode, rate, fuse_pool=True, group=(4, 4), streams=4)
+    st = make_stack(net, batch, "bf16", mode, rate, fuse_pool=True, group=(4, 4))
     l0 = st.layers[0]
     clip = synth.clip_input("bench-clip", batch, "uniform01", l0.c_in, l0.t, l0.h, l0.w)
     st.x.copy_(synth.to_dtype(clip, "bf16").permute(0, 2, 3, 4, 1).contiguous().cuda())
@@ -136,7 +136,7 @@ def test_stack_as_benchmarked(net, batch, mode, rate):
 
 
 def test_s3d_stack_as_benchmarked():
-    """bench.py --net s3d: 59 conv launches over four streams in one graph,
+    """bench.py --net s3d: 59 conv launches over two streams in one graph,
     13 pools; every op's output against the oracle on its GPU input."""
     from paper_2007_09835_amd.stack import S3DStack
     st = S3DStack(1, "bf16", "kgs", 2.1)
