@@ -197,6 +197,33 @@ def test_brick_width_follows_the_layer_size(monkeypatch):
     assert _brick_slots(f32) == 64
 
 
+def test_dense_tile_width_rules(monkeypatch):
+    """Dense 16-bit tile widths for layers of 256+ filters: 64 filters with
+    2000+ output voxels, 32 below; 16 for fewer than 256 output voxels, and
+    for a shallow reduction (c_in taps < 4096) that the launch model would
+    split on wider tiles but not on 16-filter ones (C3D conv3a at batch 1,
+    not conv3b, whose reduction is twice as deep; at batch 32 the wide tiles
+    fill the GPU unsplit).  fp32 keeps the voxel rule."""
+    monkeypatch.delenv("RT3D_TUNE", raising=False)
+    k3 = dict(k=(3, 3, 3), pad=(1, 1, 1))
+    conv3a = rt3d.make_desc(1, 128, 256, (8, 28, 28), dtype="bf16", **k3)
+    conv3b = rt3d.make_desc(1, 256, 256, (8, 28, 28), dtype="bf16", **k3)
+    conv3a_b32 = rt3d.make_desc(32, 128, 256, (8, 28, 28), dtype="bf16", **k3)
+    conv4b = rt3d.make_desc(1, 512, 512, (4, 14, 14), dtype="bf16", **k3)
+    conv5a = rt3d.make_desc(1, 512, 512, (2, 7, 7), dtype="bf16", **k3)
+    conv5a_b32 = rt3d.make_desc(32, 512, 512, (2, 7, 7), dtype="bf16", **k3)
+    conv5a_f32 = rt3d.make_desc(1, 512, 512, (2, 7, 7), dtype="f32", **k3)
+    assert _plan_mfw(conv3a) == 1
+    assert _plan_mfw(conv3b) == 4
+    assert _plan_mfw(conv3a_b32) == 4
+    assert _plan_mfw(conv4b) == 2
+    assert _plan_mfw(conv5a) == 1
+    assert _plan_mfw(conv5a_b32) == 4
+    assert _plan_mfw(conv5a_f32) == 2
+    monkeypatch.setenv("RT3D_TUNE", "dense_mfw=4")
+    assert _plan_mfw(conv3a) == 4
+
+
 def test_kgs_tile_width_follows_union_size(monkeypatch):
     """KGS layers with 256+ filters and a 64-filter wave per SIMD walk the
     union of 16 kernel groups (64-filter tiles) when the 16-filter union
