@@ -441,3 +441,25 @@ def test_small_channel_kernel_choice():
     assert variant(4, 40, (1, 2, 2), (1, 2, 2), (0, 0, 0)) == 1
     # stems: 1x7x7 stride (1, 2, 2) on RGB, 207 elements per line
     assert variant(3, 224, (1, 7, 7), (1, 2, 2), (0, 3, 3)) == 5
+
+
+def test_stack_pads_ragged_channel_pitch():
+    """The R(2+1)D stack gives layer outputs whose channel count is not a
+    multiple of 8 a pitch rounded up to 8 (zero pad channels), so the next
+    layer stages whole 16-byte pieces; residual sources keep their width.
+    Built on the host (packing and buffers only, no launch)."""
+    from paper_2007_09835_amd.stack import Stack
+    st = Stack("r2plus1d", 1, "bf16", "kgs", 3.0, device="cpu")
+    residual_sources = {l.residual_from for l in st.layers if l.residual_from}
+    padded = {}
+    for l in st.layers:
+        b = st.bufs[l.name]
+        if l.name in residual_sources:
+            assert b.shape[-1] == l.c_out
+        assert b.shape[-1] % 8 == 0 or l.name in residual_sources, l.name
+        assert b.shape[-1] - l.c_out < 8
+        if b.shape[-1] != l.c_out:
+            padded[l.name] = (l.c_out, b.shape[-1])
+            assert float(b[..., l.c_out:].abs().sum()) == 0.0
+    assert padded == {"stem_s": (45, 48), "l3b0c0_s": (230, 232), "l4b0c0_s": (460, 464),
+                      "l5b0c0_s": (921, 928)}
