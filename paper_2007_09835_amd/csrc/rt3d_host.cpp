@@ -225,8 +225,15 @@ Tiling choose_tiling(const Geom &g, int slots = kSlots) {
   // 16-bit layers with a small halo (few kernel taps) take wider channel
   // chunks: each chunk then carries more K-steps per halo load, barrier and
   // pipeline restart.  Limits: the register stager's 8 pieces of 16 bytes
-  // per thread (2048 per workgroup) and the LDS budget.
-  if (best_cost >= 0 && g.es == 2) {
+  // per thread (2048 per workgroup) and the LDS budget.  Layers of fewer
+  // than 256 output voxels whose narrow chunks already carry 16 or more
+  // K-steps keep them: they split their channels across workgroups, and
+  // finer chunks balance the splits (C3D conv5a/b at batch 1: 12.6 -> 11.6
+  // us KGS, 13.4 -> 12.1 dense; factorised 1x3x3 / 3x1x1 layers of that size
+  // ran 1-2 us slower on narrow chunks).
+  const long out_vox = static_cast<long>(std::max(g.n, 1)) * g.to * g.ho * g.wo;
+  const bool keep_narrow = out_vox < 256 && (best.cc / 4) * g.ks / 8 >= 16;
+  if (best_cost >= 0 && g.es == 2 && !keep_narrow) {
     int wide = best.cc;
     const int cap = tune("cc") >= 8 ? tune("cc") : 128;  // tuning switch cc=N caps the width
     while (wide < cap && wide < g.c_in) {
