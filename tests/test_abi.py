@@ -463,3 +463,26 @@ def test_stack_pads_ragged_channel_pitch():
             assert float(b[..., l.c_out:].abs().sum()) == 0.0
     assert padded == {"stem_s": (45, 48), "l3b0c0_s": (230, 232), "l4b0c0_s": (460, 464),
                       "l5b0c0_s": (921, 928)}
+
+
+def test_channel_chunk_width_rule(monkeypatch):
+    """16-bit chunks of 32 channels widen while the halo fits, except on
+    layers of fewer than 256 output voxels whose 32-channel chunks carry 16
+    or more K-steps (C3D conv5a at batch 1 keeps 32; conv4b and a 1x3x3
+    layer of the same size widen)."""
+    monkeypatch.delenv("RT3D_TUNE", raising=False)
+
+    def cc(desc):
+        w = _weights(np.random.default_rng(1), (desc.c_out, desc.c_in, desc.kt, desc.kh, desc.kw),
+                     "bf16")
+        _, info = rt3d.rt3d_dense_pack(desc, w)
+        return int(np.frombuffer(bytes(info.plan), dtype=np.int32)[6])
+
+    conv5a = rt3d.make_desc(1, 512, 512, (2, 7, 7), dtype="bf16")
+    conv5a_b32 = rt3d.make_desc(32, 512, 512, (2, 7, 7), dtype="bf16")
+    conv4b = rt3d.make_desc(1, 512, 512, (4, 14, 14), dtype="bf16")
+    spatial = rt3d.make_desc(1, 512, 512, (2, 7, 7), k=(1, 3, 3), pad=(0, 1, 1), dtype="bf16")
+    assert cc(conv5a) == 32
+    assert cc(conv5a_b32) > 32
+    assert cc(conv4b) > 32
+    assert cc(spatial) > 32
